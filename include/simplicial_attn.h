@@ -1,0 +1,115 @@
+/*
+ * simplicial_attn.h -- C ABI of the MI355X (gfx950) causal sliding-window
+ * 2-simplicial (trilinear) attention library, libsimplicial_attn.so.
+ *
+ * The operation (arXiv 2507.02754, Section 4 Eqs. (3d-attention), (softmax),
+ * (attenval), over the sliding windows of Section 6): for every batch b, head h
+ * and query i,
+ *
+ *     A[i,j,k] = scale * sum_d Q[i,d] K[j,d] K'[k,d]      j in (i-w1, i], k in (i-w2, i]
+ *     P[i,j,k] = exp(A[i,j,k] - LSE[i]),  LSE[i] = log sum_{j,k} exp(A[i,j,k])
+ *     O[i,d]   = sum_{j,k} P[i,j,k] V[j,d] V'[k,d]
+ *
+ * Windows are clipped at 0 and include the diagonal, so every query has at
+ * least the pair (i, i). The backward computes the gradients of Section 7's
+ * equations (dQ, dK, dK' carry one factor of `scale`; dV, dV' none).
+ *
+ * Conventions shared by every entry point
+ *   Layout   Q, K, K', V, V', O, dO and all gradients are contiguous row-major
+ *            [B, N, H, D] (batch, sequence, head, head_dim). LSE is contiguous
+ *            [B, H, N] float32, natural logarithm.
+ *   dtype    SA_DTYPE_F32 or SA_DTYPE_BF16, applied to every tensor except LSE
+ *            (always float32). bf16 data is accumulated in float32.
+ *   Pointers device pointers (hipMalloc'd or torch CUDA tensors), 16-byte
+ *            aligned. The caller owns every buffer; the library allocates no
+ *            device memory and keeps no state between calls (re-entrant).
+ *   Stream   a hipStream_t passed as void* (NULL = the default stream). Calls
+ *            only enqueue work on it and return without synchronising.
+ *   Errors   each call returns SA_OK (0) or an SA_ERR_* code. All argument
+ *            validation happens on the host before any HIP call, so invalid
+ *            calls are rejected even where no GPU is present. No C++ exception
+ *            crosses the ABI and the library never aborts. A kernel launch
+ *            failure is reported as SA_ERR_HIP; an asynchronous device fault
+ *            surfaces on the caller's next synchronisation.
+ */
+#ifndef SIMPLICIAL_ATTN_H
+#define SIMPLICIAL_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SIMPLICIAL_ATTN_ABI_VERSION 1
+
+#define SA_DTYPE_F32 0
+#define SA_DTYPE_BF16 1
+
+#define SA_OK 0
+#define SA_ERR_INVALID 1     /* null pointer, non-positive size, w < 1, misaligned pointer, overflow */
+#define SA_ERR_UNSUPPORTED 2 /* head_dim or dtype this build does not implement */
+#define SA_ERR_WORKSPACE 3   /* workspace smaller than simplicial_attn_bwd_workspace_size() */
+#define SA_ERR_HIP 4         /* HIP runtime reported an error when launching */
+
+/*
+ * Forward pass (Section 4 equations over Section 6's windows).
+ *   q, k, kp, v, vp  inputs Q, K, K', V, V'   [B, N, H, D], dtype
+ *   out              output O                 [B, N, H, D], dtype, fully overwritten
+ *   lse              log-sum-exp per query    [B, H, N], float32, fully overwritten
+ *   B, N, H, D       sizes; D in {16, 32, 64, 128}
+ *   w1, w2           window lengths of K/V and K'/V' (>= 1; larger than N is legal)
+ *   scale            logit scale (the paper's 1/sqrt(D)); any finite value
+ *   dtype            SA_DTYPE_F32 or SA_DTYPE_BF16
+ *   stream           hipStream_t or NULL
+ */
+int simplicial_attn_fwd(const void* q, const void* k, const void* kp, const void* v, const void* vp,
+                        void* out, float* lse, int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1,
+                        int32_t w2, float scale, int32_t dtype, void* stream);
+
+/*
+ * Bytes of device workspace simplicial_attn_bwd needs for these sizes (the
+ * per-query Delta = <dO_i, O_i> and the partial sums the backward reduces
+ * deterministically). Returns 0 for arguments simplicial_attn_bwd would reject.
+ */
+size_t simplicial_attn_bwd_workspace_size(int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1,
+                                          int32_t w2, int32_t dtype);
+
+/*
+ * Backward pass (Section 7's gradient equations; dsoftmax read as
+ * dS = P * (dP - Delta_i), Delta_i = <dO_i, O_i>).
+ *   q, k, kp, v, vp    forward inputs                    [B, N, H, D], dtype
+ *   out, lse           forward outputs of the same call  [B, N, H, D] dtype / [B, H, N] f32
+ *   dout               upstream gradient dO               [B, N, H, D], dtype
+ *   dq, dk, dkp, dv, dvp  gradients, fully overwritten   [B, N, H, D], dtype
+ *   workspace          device scratch of at least simplicial_attn_bwd_workspace_size()
+ *                      bytes, 16-byte aligned; contents on entry are ignored
+ *   other arguments    as simplicial_attn_fwd
+ * The result is bitwise deterministic: no floating-point atomics are used.
+ */
+int simplicial_attn_bwd(const void* q, const void* k, const void* kp, const void* v, const void* vp,
+                        const void* out, const void* dout, const float* lse, void* dq, void* dk,
+                        void* dkp, void* dv, void* dvp, void* workspace, size_t workspace_bytes,
+                        int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1, int32_t w2,
+                        float scale, int32_t dtype, void* stream);
+
+/* Static, NUL-terminated description of a status code ("unknown status" otherwise). */
+const char* simplicial_attn_error_string(int code);
+
+/* SIMPLICIAL_ATTN_ABI_VERSION of the loaded library. */
+int simplicial_attn_abi_version(void);
+
+/*
+ * Name of the kernel path the forward (which = 0) or backward (which = 1) would
+ * take for these sizes, e.g. "mfma_bf16" or "generic"; "invalid" when the
+ * arguments would be rejected. Static string; no HIP call is made.
+ */
+const char* simplicial_attn_path_name(int32_t which, int64_t B, int64_t N, int64_t H, int64_t D,
+                                      int32_t w1, int32_t w2, int32_t dtype);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SIMPLICIAL_ATTN_H */

@@ -1,0 +1,19 @@
+"""MI355X (gfx950) causal sliding-window 2-simplicial attention.
+
+The compute lives in libsimplicial_attn.so (hand-written HIP, C ABI in
+include/simplicial_attn.h); this package is its thin Python binding plus the
+seeded synthetic workloads used by the tests and the benchmark.
+"""
+
+from .binding import (  # noqa: F401
+    DTYPE_BF16,
+    DTYPE_F32,
+    SimplicialAttnError,
+    load_library,
+    simplicial_attn_abi_version,
+    simplicial_attn_bwd,
+    simplicial_attn_bwd_workspace_size,
+    simplicial_attn_error_string,
+    simplicial_attn_fwd,
+    simplicial_attn_path_name,
+)

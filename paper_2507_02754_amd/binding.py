@@ -1,0 +1,165 @@
+"""ctypes binding of libsimplicial_attn.so (argument marshalling only).
+
+Every function here has the name of the C entry point it calls and does no
+arithmetic of its own: tensors are checked for device, dtype, layout and shape,
+outputs/workspace are allocated with torch (device memory only), and the raw
+pointers plus torch's current HIP stream are handed to the library. If the
+library has not been built the import of the first call raises; there is no
+fallback implementation.
+"""
+
+import ctypes
+import os
+
+import torch
+
+__all__ = [
+    "SimplicialAttnError",
+    "load_library",
+    "simplicial_attn_fwd",
+    "simplicial_attn_bwd",
+    "simplicial_attn_bwd_workspace_size",
+    "simplicial_attn_error_string",
+    "simplicial_attn_abi_version",
+    "simplicial_attn_path_name",
+    "DTYPE_F32",
+    "DTYPE_BF16",
+]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsimplicial_attn.so")
+DTYPE_F32 = 0
+DTYPE_BF16 = 1
+_DTYPES = {torch.float32: DTYPE_F32, torch.bfloat16: DTYPE_BF16}
+
+_lib = None
+
+
+class SimplicialAttnError(RuntimeError):
+    def __init__(self, code, where):
+        self.code = code
+        super().__init__(f"{where} failed with status {code}: {simplicial_attn_error_string(code)}")
+
+
+def load_library():
+    """Load (once) and return the ctypes handle; raise if the library is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(
+            f"{LIB_PATH} is not built; run `python -m paper_2507_02754_amd.build` "
+            "(the HIP library is required; there is no CPU fallback)")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i64, i32, f32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_float
+    lib.simplicial_attn_fwd.argtypes = [vp] * 7 + [i64] * 4 + [i32, i32, f32, i32, vp]
+    lib.simplicial_attn_fwd.restype = ctypes.c_int
+    lib.simplicial_attn_bwd.argtypes = [vp] * 14 + [ctypes.c_size_t] + [i64] * 4 + [i32, i32, f32, i32, vp]
+    lib.simplicial_attn_bwd.restype = ctypes.c_int
+    lib.simplicial_attn_bwd_workspace_size.argtypes = [i64] * 4 + [i32, i32, i32]
+    lib.simplicial_attn_bwd_workspace_size.restype = ctypes.c_size_t
+    lib.simplicial_attn_error_string.argtypes = [ctypes.c_int]
+    lib.simplicial_attn_error_string.restype = ctypes.c_char_p
+    lib.simplicial_attn_abi_version.argtypes = []
+    lib.simplicial_attn_abi_version.restype = ctypes.c_int
+    lib.simplicial_attn_path_name.argtypes = [i32] + [i64] * 4 + [i32, i32, i32]
+    lib.simplicial_attn_path_name.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def simplicial_attn_error_string(code):
+    return load_library().simplicial_attn_error_string(int(code)).decode()
+
+
+def simplicial_attn_abi_version():
+    return int(load_library().simplicial_attn_abi_version())
+
+
+def simplicial_attn_path_name(which, B, N, H, D, w1, w2, dtype):
+    """Kernel path for forward (which=0) or backward (which=1); dtype is a torch dtype or int."""
+    dt = _DTYPES.get(dtype, dtype)
+    return load_library().simplicial_attn_path_name(int(which), B, N, H, D, int(w1), int(w2), int(dt)).decode()
+
+
+def simplicial_attn_bwd_workspace_size(B, N, H, D, w1, w2, dtype):
+    dt = _DTYPES.get(dtype, dtype)
+    return int(load_library().simplicial_attn_bwd_workspace_size(B, N, H, D, int(w1), int(w2), int(dt)))
+
+
+def _check_inputs(tensors, names):
+    t0 = tensors[0]
+    if t0.dim() != 4:
+        raise ValueError(f"{names[0]} must be [B, N, H, D], got shape {tuple(t0.shape)}")
+    if t0.dtype not in _DTYPES:
+        raise ValueError(f"unsupported dtype {t0.dtype}; expected float32 or bfloat16")
+    for t, n in zip(tensors, names):
+        if not t.is_cuda:
+            raise ValueError(f"{n} must be a GPU tensor")
+        if t.device != t0.device:
+            raise ValueError(f"{n} is on {t.device}, expected {t0.device}")
+        if t.dtype != t0.dtype:
+            raise ValueError(f"{n} has dtype {t.dtype}, expected {t0.dtype}")
+        if t.shape != t0.shape:
+            raise ValueError(f"{n} has shape {tuple(t.shape)}, expected {tuple(t0.shape)}")
+        if not t.is_contiguous():
+            raise ValueError(f"{n} must be contiguous [B, N, H, D]")
+    return t0.shape, _DTYPES[t0.dtype]
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def simplicial_attn_fwd(q, k, kp, v, vp, w1, w2, scale=None, out=None, lse=None):
+    """O, LSE = forward(Q, K, K', V, V'); tensors [B, N, H, D] on one GPU.
+
+    `scale` defaults to 1/sqrt(D). Returns (out [B, N, H, D], lse [B, H, N] fp32).
+    """
+    (B, N, H, D), dt = _check_inputs((q, k, kp, v, vp), ("q", "k", "kp", "v", "vp"))
+    if scale is None:
+        scale = D ** -0.5
+    if out is None:
+        out = torch.empty_like(q)
+    else:
+        _check_inputs((q, out), ("q", "out"))
+    if lse is None:
+        lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+    elif lse.shape != (B, H, N) or lse.dtype != torch.float32 or not lse.is_contiguous() \
+            or lse.device != q.device:
+        raise ValueError("lse must be a contiguous float32 [B, H, N] tensor on the inputs' device")
+    rc = load_library().simplicial_attn_fwd(
+        _ptr(q), _ptr(k), _ptr(kp), _ptr(v), _ptr(vp), _ptr(out), _ptr(lse),
+        B, N, H, D, int(w1), int(w2), float(scale), dt, _stream(q.device))
+    if rc != 0:
+        raise SimplicialAttnError(rc, "simplicial_attn_fwd")
+    return out, lse
+
+
+def simplicial_attn_bwd(q, k, kp, v, vp, out, dout, lse, w1, w2, scale=None, grads=None,
+                        workspace=None):
+    """(dQ, dK, dK', dV, dV') = backward(...); `out`/`lse` come from the forward."""
+    (B, N, H, D), dt = _check_inputs((q, k, kp, v, vp, out, dout),
+                                     ("q", "k", "kp", "v", "vp", "out", "dout"))
+    if scale is None:
+        scale = D ** -0.5
+    if lse.shape != (B, H, N) or lse.dtype != torch.float32 or not lse.is_contiguous() \
+            or lse.device != q.device:
+        raise ValueError("lse must be a contiguous float32 [B, H, N] tensor on the inputs' device")
+    if grads is None:
+        grads = tuple(torch.empty_like(q) for _ in range(5))
+    else:
+        _check_inputs((q, *grads), ("q", "dq", "dk", "dkp", "dv", "dvp"))
+    ws = simplicial_attn_bwd_workspace_size(B, N, H, D, w1, w2, dt)
+    if workspace is None:
+        workspace = torch.empty(max(ws, 16), dtype=torch.uint8, device=q.device)
+    rc = load_library().simplicial_attn_bwd(
+        _ptr(q), _ptr(k), _ptr(kp), _ptr(v), _ptr(vp), _ptr(out), _ptr(dout), _ptr(lse),
+        *(_ptr(g) for g in grads), _ptr(workspace), ctypes.c_size_t(workspace.numel()),
+        B, N, H, D, int(w1), int(w2), float(scale), dt, _stream(q.device))
+    if rc != 0:
+        raise SimplicialAttnError(rc, "simplicial_attn_bwd")
+    return grads

@@ -1,0 +1,139 @@
+// C-ABI entry points of libsimplicial_attn.so: argument validation (host only,
+// before any HIP call), kernel-path selection and error mapping. The
+// operation and the conventions are documented in include/simplicial_attn.h.
+#include "simplicial_attn.h"
+
+#include <limits.h>
+#include <math.h>
+
+#include "sa_internal.h"
+
+namespace {
+
+using sa::Shape;
+
+enum class Path { Invalid, Generic, Mfma };
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Size checks shared by every entry point. Returns SA_OK or an error code.
+int check_sizes(int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1, int32_t w2,
+                int32_t dtype) {
+  if (B <= 0 || N <= 0 || H <= 0 || D <= 0 || w1 < 1 || w2 < 1) return SA_ERR_INVALID;
+  // Every grid index and per-head row count must fit in 32 bits, and byte
+  // offsets in 63 bits.
+  if (N > INT_MAX || B > INT_MAX || H > INT_MAX || D > INT_MAX) return SA_ERR_INVALID;
+  const int64_t rows = B * H;
+  if (rows > INT_MAX || N > INT_MAX / rows) return SA_ERR_INVALID;
+  if (D > (int64_t(1) << 40) / (N * rows)) return SA_ERR_INVALID;
+  if (dtype != SA_DTYPE_F32 && dtype != SA_DTYPE_BF16) return SA_ERR_UNSUPPORTED;
+  if (D != 16 && D != 32 && D != 64 && D != 128) return SA_ERR_UNSUPPORTED;
+  return SA_OK;
+}
+
+Shape make_shape(int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1, int32_t w2, float scale,
+                 int32_t dtype) {
+  Shape s;
+  s.B = static_cast<int>(B);
+  s.N = static_cast<int>(N);
+  s.H = static_cast<int>(H);
+  s.D = static_cast<int>(D);
+  // Windows longer than the sequence behave exactly like the sequence length.
+  s.w1 = static_cast<int>(w1 > N ? N : w1);
+  s.w2 = static_cast<int>(w2 > N ? N : w2);
+  s.scale = scale;
+  s.dtype = dtype;
+  return s;
+}
+
+Path choose_path(int which, int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1, int32_t w2,
+                 int32_t dtype) {
+  if (check_sizes(B, N, H, D, w1, w2, dtype) != SA_OK) return Path::Invalid;
+  const Shape s = make_shape(B, N, H, D, w1, w2, 1.0f, dtype);
+  if (which == 0 && sa::mfma_fwd_supported(s)) return Path::Mfma;
+  return Path::Generic;
+}
+
+int to_status(hipError_t e) { return e == hipSuccess ? SA_OK : SA_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+int simplicial_attn_abi_version(void) { return SIMPLICIAL_ATTN_ABI_VERSION; }
+
+const char* simplicial_attn_error_string(int code) {
+  switch (code) {
+    case SA_OK: return "success";
+    case SA_ERR_INVALID: return "invalid argument (null/misaligned pointer, bad size or window)";
+    case SA_ERR_UNSUPPORTED: return "unsupported head_dim or dtype";
+    case SA_ERR_WORKSPACE: return "workspace smaller than simplicial_attn_bwd_workspace_size()";
+    case SA_ERR_HIP: return "HIP runtime error while launching kernels";
+    default: return "unknown status";
+  }
+}
+
+const char* simplicial_attn_path_name(int32_t which, int64_t B, int64_t N, int64_t H, int64_t D,
+                                      int32_t w1, int32_t w2, int32_t dtype) {
+  if (which != 0 && which != 1) return "invalid";
+  switch (choose_path(which, B, N, H, D, w1, w2, dtype)) {
+    case Path::Generic: return "generic";
+    case Path::Mfma: return "mfma_bf16";
+    default: return "invalid";
+  }
+}
+
+int simplicial_attn_fwd(const void* q, const void* k, const void* kp, const void* v, const void* vp,
+                        void* out, float* lse, int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1,
+                        int32_t w2, float scale, int32_t dtype, void* stream) {
+  if (!q || !k || !kp || !v || !vp || !out || !lse) return SA_ERR_INVALID;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(kp) || !aligned16(v) || !aligned16(vp) ||
+      !aligned16(out) || !aligned16(lse))
+    return SA_ERR_INVALID;
+  if (!isfinite(scale)) return SA_ERR_INVALID;
+  const int rc = check_sizes(B, N, H, D, w1, w2, dtype);
+  if (rc != SA_OK) return rc;
+  const Shape s = make_shape(B, N, H, D, w1, w2, scale, dtype);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  switch (choose_path(0, B, N, H, D, w1, w2, dtype)) {
+    case Path::Generic: return to_status(sa::generic_fwd(s, q, k, kp, v, vp, out, lse, st));
+    case Path::Mfma: return to_status(sa::mfma_fwd(s, q, k, kp, v, vp, out, lse, st));
+    default: return SA_ERR_UNSUPPORTED;
+  }
+}
+
+size_t simplicial_attn_bwd_workspace_size(int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1,
+                                          int32_t w2, int32_t dtype) {
+  if (check_sizes(B, N, H, D, w1, w2, dtype) != SA_OK) return 0;
+  // Delta: one float per (b, h, query), rounded up to 256 bytes.
+  const size_t delta = ((static_cast<size_t>(B * H * N) * sizeof(float)) + 255) & ~size_t(255);
+  return delta;
+}
+
+int simplicial_attn_bwd(const void* q, const void* k, const void* kp, const void* v, const void* vp,
+                        const void* out, const void* dout, const float* lse, void* dq, void* dk,
+                        void* dkp, void* dv, void* dvp, void* workspace, size_t workspace_bytes,
+                        int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1, int32_t w2,
+                        float scale, int32_t dtype, void* stream) {
+  const void* ptrs[] = {q, k, kp, v, vp, out, dout, lse, dq, dk, dkp, dv, dvp, workspace};
+  for (const void* p : ptrs) {
+    if (!p) return SA_ERR_INVALID;
+    if (!aligned16(p)) return SA_ERR_INVALID;
+  }
+  if (!isfinite(scale)) return SA_ERR_INVALID;
+  const int rc = check_sizes(B, N, H, D, w1, w2, dtype);
+  if (rc != SA_OK) return rc;
+  if (workspace_bytes < simplicial_attn_bwd_workspace_size(B, N, H, D, w1, w2, dtype))
+    return SA_ERR_WORKSPACE;
+  const Shape s = make_shape(B, N, H, D, w1, w2, scale, dtype);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  float* delta = static_cast<float*>(workspace);
+  switch (choose_path(1, B, N, H, D, w1, w2, dtype)) {
+    case Path::Generic:
+      return to_status(sa::generic_bwd(s, q, k, kp, v, vp, out, dout, lse, dq, dk, dkp, dv, dvp,
+                                       delta, st));
+    default: return SA_ERR_UNSUPPORTED;
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,363 @@
+// Generic HIP path: correct for every supported dtype, head_dim and window
+// pair, written for clarity rather than speed. It serves shapes the MFMA
+// kernels do not specialise (fp32 data, w2 not a multiple of 32, small
+// head_dim) and is the fallback the fast paths are tested against.
+//
+// One workgroup of 256 threads owns one output row. Threads stride over the
+// (j, k) pairs of that row, each keeping a private D-vector accumulator in
+// registers; a wavefront shuffle reduction plus a small LDS pass combines
+// them. All arithmetic is fp32; exponentials use expf.
+//
+// Forward (Section 4, Eqs. (3d-attention), (softmax), (attenval)): two passes
+// over the pairs -- the first finds the row maximum of the logits, the second
+// sums exp(logit - max) and the exp-weighted v_j o v'_k.
+// Backward (Section 7): dQ per query row; dK/dV per K-row j and dK'/dV' per
+// K'-row k, each gathering its own pairs, so no atomics are needed and the
+// result is deterministic.
+#include "sa_internal.h"
+
+#include <math.h>
+
+namespace sa {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+
+template <typename T>
+__device__ __forceinline__ float ld(const T* p);
+template <>
+__device__ __forceinline__ float ld<float>(const float* p) {
+  return *p;
+}
+template <>
+__device__ __forceinline__ float ld<uint16_t>(const uint16_t* p) {
+  return bf16_to_f32(*p);
+}
+
+template <typename T>
+__device__ __forceinline__ void st(T* p, float x);
+template <>
+__device__ __forceinline__ void st<float>(float* p, float x) {
+  *p = x;
+}
+template <>
+__device__ __forceinline__ void st<uint16_t>(uint16_t* p, float x) {
+  *p = f32_to_bf16(x);
+}
+
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x = fmaxf(x, __shfl_xor(x, off));
+  return x;
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off);
+  return x;
+}
+
+// Block-wide max/sum of one scalar; every thread gets the result.
+__device__ float block_max(float x, float* red) {
+  x = wave_max(x);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) red[w] = x;
+  __syncthreads();
+  float r = red[0];
+  for (int i = 1; i < kWaves; ++i) r = fmaxf(r, red[i]);
+  __syncthreads();
+  return r;
+}
+
+__device__ float block_sum(float x, float* red) {
+  x = wave_sum(x);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) red[w] = x;
+  __syncthreads();
+  float r = 0.f;
+  for (int i = 0; i < kWaves; ++i) r += red[i];
+  __syncthreads();
+  return r;
+}
+
+// Sums acc[D] over the block; thread t < D receives component t (others 0).
+template <int D>
+__device__ float block_sum_vec(float (&acc)[D], float* red /* [kWaves * D] */) {
+#pragma unroll
+  for (int d = 0; d < D; ++d) acc[d] = wave_sum(acc[d]);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+#pragma unroll
+    for (int d = 0; d < D; ++d) red[w * D + d] = acc[d];
+  }
+  __syncthreads();
+  float r = 0.f;
+  if (threadIdx.x < D) {
+    for (int i = 0; i < kWaves; ++i) r += red[i * D + threadIdx.x];
+  }
+  __syncthreads();
+  return r;
+}
+
+// Row pointer helper for [B, N, H, D] tensors: base of (b, 0, h, 0), stride H*D.
+struct Rows {
+  size_t base, stride;
+  __device__ Rows(int b, int h, const Shape& s)
+      : base((static_cast<size_t>(b) * s.N * s.H + h) * s.D),
+        stride(static_cast<size_t>(s.H) * s.D) {}
+  __device__ size_t at(int n) const { return base + static_cast<size_t>(n) * stride; }
+};
+
+template <typename T, int D>
+__device__ __forceinline__ float tri(const float* a, const T* x, const T* y) {
+  float s = 0.f;
+#pragma unroll 8
+  for (int d = 0; d < D; ++d) s += a[d] * ld(x + d) * ld(y + d);
+  return s;
+}
+
+// ---------------------------------------------------------------- forward ---
+template <typename T, int D>
+__global__ __launch_bounds__(kThreads) void fwd_kernel(Shape s, const T* __restrict__ q,
+                                                       const T* __restrict__ k,
+                                                       const T* __restrict__ kp,
+                                                       const T* __restrict__ v,
+                                                       const T* __restrict__ vp, T* __restrict__ out,
+                                                       float* __restrict__ lse) {
+  const int i = blockIdx.x % s.N;
+  const int bh = blockIdx.x / s.N;
+  const int b = bh / s.H, h = bh % s.H;
+  const Rows rows(b, h, s);
+  __shared__ float qs[D];
+  __shared__ float red[kWaves * D];
+  __shared__ float sred[kWaves];
+  if (threadIdx.x < D) qs[threadIdx.x] = ld(q + rows.at(i) + threadIdx.x) * s.scale;
+  __syncthreads();
+
+  const int j0 = max(0, i - s.w1 + 1), nj = i - j0 + 1;
+  const int k0 = max(0, i - s.w2 + 1), nk = i - k0 + 1;
+  const int np = nj * nk;
+
+  float m = -INFINITY;
+  for (int p = threadIdx.x; p < np; p += kThreads) {
+    const int j = j0 + p / nk, kk = k0 + p % nk;
+    m = fmaxf(m, tri<T, D>(qs, k + rows.at(j), kp + rows.at(kk)));
+  }
+  m = block_max(m, sred);
+
+  float l = 0.f;
+  float acc[D];
+#pragma unroll
+  for (int d = 0; d < D; ++d) acc[d] = 0.f;
+  for (int p = threadIdx.x; p < np; p += kThreads) {
+    const int j = j0 + p / nk, kk = k0 + p % nk;
+    const float e = expf(tri<T, D>(qs, k + rows.at(j), kp + rows.at(kk)) - m);
+    l += e;
+    const T* vj = v + rows.at(j);
+    const T* vk = vp + rows.at(kk);
+#pragma unroll
+    for (int d = 0; d < D; ++d) acc[d] += e * ld(vj + d) * ld(vk + d);
+  }
+  l = block_sum(l, sred);
+  const float o = block_sum_vec<D>(acc, red);
+  if (threadIdx.x < D) st(out + rows.at(i) + threadIdx.x, o / l);
+  if (threadIdx.x == 0) lse[static_cast<size_t>(bh) * s.N + i] = m + logf(l);
+}
+
+// ------------------------------------------------------------------ delta ---
+template <typename T>
+__global__ void delta_kernel(Shape s, const T* __restrict__ out, const T* __restrict__ dout,
+                             float* __restrict__ delta) {
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int64_t total = static_cast<int64_t>(s.B) * s.H * s.N;
+  if (idx >= total) return;
+  const int i = static_cast<int>(idx % s.N);
+  const int bh = static_cast<int>(idx / s.N);
+  const size_t off = ((static_cast<size_t>(bh / s.H) * s.N + i) * s.H + bh % s.H) * s.D;
+  float acc = 0.f;
+  for (int d = 0; d < s.D; ++d) acc += ld(out + off + d) * ld(dout + off + d);
+  delta[idx] = acc;
+}
+
+// --------------------------------------------------------------------- dQ ---
+template <typename T, int D>
+__global__ __launch_bounds__(kThreads) void dq_kernel(Shape s, const T* __restrict__ q,
+                                                      const T* __restrict__ k,
+                                                      const T* __restrict__ kp,
+                                                      const T* __restrict__ v,
+                                                      const T* __restrict__ vp,
+                                                      const T* __restrict__ dout,
+                                                      const float* __restrict__ lse,
+                                                      const float* __restrict__ delta,
+                                                      T* __restrict__ dq) {
+  const int i = blockIdx.x % s.N;
+  const int bh = blockIdx.x / s.N;
+  const int b = bh / s.H, h = bh % s.H;
+  const Rows rows(b, h, s);
+  __shared__ float qs[D];
+  __shared__ float ds_[D];
+  __shared__ float red[kWaves * D];
+  if (threadIdx.x < D) {
+    qs[threadIdx.x] = ld(q + rows.at(i) + threadIdx.x) * s.scale;
+    ds_[threadIdx.x] = ld(dout + rows.at(i) + threadIdx.x);
+  }
+  __syncthreads();
+  const float lse_i = lse[static_cast<size_t>(bh) * s.N + i];
+  const float delta_i = delta[static_cast<size_t>(bh) * s.N + i];
+  const int j0 = max(0, i - s.w1 + 1), nj = i - j0 + 1;
+  const int k0 = max(0, i - s.w2 + 1), nk = i - k0 + 1;
+  const int np = nj * nk;
+
+  float acc[D];
+#pragma unroll
+  for (int d = 0; d < D; ++d) acc[d] = 0.f;
+  for (int p = threadIdx.x; p < np; p += kThreads) {
+    const int j = j0 + p / nk, kk = k0 + p % nk;
+    const T* kj = k + rows.at(j);
+    const T* kk_ = kp + rows.at(kk);
+    const float pr = expf(tri<T, D>(qs, kj, kk_) - lse_i);
+    const float dp = tri<T, D>(ds_, v + rows.at(j), vp + rows.at(kk));
+    const float dsv = pr * (dp - delta_i);
+#pragma unroll
+    for (int d = 0; d < D; ++d) acc[d] += dsv * ld(kj + d) * ld(kk_ + d);
+  }
+  const float g = block_sum_vec<D>(acc, red);
+  if (threadIdx.x < D) st(dq + rows.at(i) + threadIdx.x, g * s.scale);
+}
+
+// ------------------------------------------------------- dK / dV / dK' / dV' ---
+// One workgroup per key row r of the K/V side (SIDE 0: window w1, partner
+// window w2) or of the K'/V' side (SIDE 1: window w2, partner window w1). The
+// pairs touching r are (i, o) with i in [r, r + w_self) and o in (i - w_other, i].
+// MODE 0 produces the key gradient, MODE 1 the value gradient.
+template <typename T, int D, int SIDE, int MODE>
+__global__ __launch_bounds__(kThreads) void keyside_kernel(
+    Shape s, const T* __restrict__ q, const T* __restrict__ kself, const T* __restrict__ kother,
+    const T* __restrict__ vself, const T* __restrict__ vother, const T* __restrict__ dout,
+    const float* __restrict__ lse, const float* __restrict__ delta, T* __restrict__ grad) {
+  const int r = blockIdx.x % s.N;
+  const int bh = blockIdx.x / s.N;
+  const int b = bh / s.H, h = bh % s.H;
+  const Rows rows(b, h, s);
+  const int wself = SIDE == 0 ? s.w1 : s.w2;
+  const int wother = SIDE == 0 ? s.w2 : s.w1;
+  __shared__ float kr[D];
+  __shared__ float vr[D];
+  __shared__ float red[kWaves * D];
+  if (threadIdx.x < D) {
+    kr[threadIdx.x] = ld(kself + rows.at(r) + threadIdx.x) * s.scale;
+    vr[threadIdx.x] = ld(vself + rows.at(r) + threadIdx.x);
+  }
+  __syncthreads();
+  const int na = min(wself, s.N - r);
+  const int np = na * wother;
+  const size_t stat = static_cast<size_t>(bh) * s.N;
+
+  float acc[D];
+#pragma unroll
+  for (int d = 0; d < D; ++d) acc[d] = 0.f;
+  for (int p = threadIdx.x; p < np; p += kThreads) {
+    const int i = r + p / wother;
+    const int o = i - p % wother;
+    if (o < 0) continue;
+    const T* qi = q + rows.at(i);
+    const T* ko = kother + rows.at(o);
+    const T* doi = dout + rows.at(i);
+    const T* vo = vother + rows.at(o);
+    const float pr = expf(tri<T, D>(kr, qi, ko) - lse[stat + i]);
+    if (MODE == 0) {
+      const float dp = tri<T, D>(vr, doi, vo);
+      const float dsv = pr * (dp - delta[stat + i]);
+#pragma unroll
+      for (int d = 0; d < D; ++d) acc[d] += dsv * ld(qi + d) * ld(ko + d);
+    } else {
+#pragma unroll
+      for (int d = 0; d < D; ++d) acc[d] += pr * ld(doi + d) * ld(vo + d);
+    }
+  }
+  const float g = block_sum_vec<D>(acc, red);
+  if (threadIdx.x < D) st(grad + rows.at(r) + threadIdx.x, MODE == 0 ? g * s.scale : g);
+}
+
+template <typename T, int D>
+hipError_t fwd_t(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
+                 const void* vp, void* out, float* lse, hipStream_t st) {
+  const unsigned grid = static_cast<unsigned>(s.N) * s.B * s.H;
+  hipLaunchKernelGGL((fwd_kernel<T, D>), dim3(grid), dim3(kThreads), 0, st, s,
+                     static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(kp),
+                     static_cast<const T*>(v), static_cast<const T*>(vp), static_cast<T*>(out),
+                     lse);
+  return hipGetLastError();
+}
+
+template <typename T, int D>
+hipError_t bwd_t(const Shape& s, const void* q_, const void* k_, const void* kp_, const void* v_,
+                 const void* vp_, const void* dout_, const float* lse, const float* delta,
+                 void* dq, void* dk, void* dkp, void* dv, void* dvp, hipStream_t st) {
+  const T* q = static_cast<const T*>(q_);
+  const T* k = static_cast<const T*>(k_);
+  const T* kp = static_cast<const T*>(kp_);
+  const T* v = static_cast<const T*>(v_);
+  const T* vp = static_cast<const T*>(vp_);
+  const T* dout = static_cast<const T*>(dout_);
+  const unsigned grid = static_cast<unsigned>(s.N) * s.B * s.H;
+  hipLaunchKernelGGL((dq_kernel<T, D>), dim3(grid), dim3(kThreads), 0, st, s, q, k, kp, v, vp,
+                     dout, lse, delta, static_cast<T*>(dq));
+  hipLaunchKernelGGL((keyside_kernel<T, D, 0, 0>), dim3(grid), dim3(kThreads), 0, st, s, q, k, kp,
+                     v, vp, dout, lse, delta, static_cast<T*>(dk));
+  hipLaunchKernelGGL((keyside_kernel<T, D, 0, 1>), dim3(grid), dim3(kThreads), 0, st, s, q, k, kp,
+                     v, vp, dout, lse, delta, static_cast<T*>(dv));
+  hipLaunchKernelGGL((keyside_kernel<T, D, 1, 0>), dim3(grid), dim3(kThreads), 0, st, s, q, kp, k,
+                     vp, v, dout, lse, delta, static_cast<T*>(dkp));
+  hipLaunchKernelGGL((keyside_kernel<T, D, 1, 1>), dim3(grid), dim3(kThreads), 0, st, s, q, kp, k,
+                     vp, v, dout, lse, delta, static_cast<T*>(dvp));
+  return hipGetLastError();
+}
+
+}  // namespace
+
+#define SA_DISPATCH_D(T, FN, ...)              \
+  switch (s.D) {                              \
+    case 16: return FN<T, 16>(__VA_ARGS__);   \
+    case 32: return FN<T, 32>(__VA_ARGS__);   \
+    case 64: return FN<T, 64>(__VA_ARGS__);   \
+    case 128: return FN<T, 128>(__VA_ARGS__); \
+    default: return hipErrorInvalidValue;     \
+  }
+
+hipError_t generic_fwd(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
+                       const void* vp, void* out, float* lse, hipStream_t st) {
+  if (s.dtype == 0) {
+    SA_DISPATCH_D(float, fwd_t, s, q, k, kp, v, vp, out, lse, st);
+  }
+  SA_DISPATCH_D(uint16_t, fwd_t, s, q, k, kp, v, vp, out, lse, st);
+}
+
+hipError_t launch_delta(const Shape& s, const void* out, const void* dout, float* delta,
+                        hipStream_t st) {
+  const int64_t total = static_cast<int64_t>(s.B) * s.H * s.N;
+  const unsigned grid = static_cast<unsigned>((total + 255) / 256);
+  if (s.dtype == 0) {
+    hipLaunchKernelGGL(delta_kernel<float>, dim3(grid), dim3(256), 0, st, s,
+                       static_cast<const float*>(out), static_cast<const float*>(dout), delta);
+  } else {
+    hipLaunchKernelGGL(delta_kernel<uint16_t>, dim3(grid), dim3(256), 0, st, s,
+                       static_cast<const uint16_t*>(out), static_cast<const uint16_t*>(dout),
+                       delta);
+  }
+  return hipGetLastError();
+}
+
+hipError_t generic_bwd(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
+                       const void* vp, const void* out, const void* dout, const float* lse, void* dq,
+                       void* dk, void* dkp, void* dv, void* dvp, float* delta, hipStream_t st) {
+  hipError_t e = launch_delta(s, out, dout, delta, st);
+  if (e != hipSuccess) return e;
+  if (s.dtype == 0) {
+    SA_DISPATCH_D(float, bwd_t, s, q, k, kp, v, vp, dout, lse, delta, dq, dk, dkp, dv, dvp, st);
+  }
+  SA_DISPATCH_D(uint16_t, bwd_t, s, q, k, kp, v, vp, dout, lse, delta, dq, dk, dkp, dv, dvp, st);
+}
+
+}  // namespace sa

@@ -1,0 +1,50 @@
+// Internal declarations shared by the library's translation units (not part of
+// the public ABI). Host launchers return hipError_t; the C-ABI layer in api.hip
+// maps errors to SA_* status codes.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace sa {
+
+// Problem description after host validation. Tensors are [B, N, H, D]
+// contiguous; per-query statistics are [B, H, N].
+struct Shape {
+  int B, N, H, D;
+  int w1, w2;
+  float scale;
+  int dtype;  // SA_DTYPE_*
+};
+
+// bf16 is carried as raw 16-bit patterns (uint16_t) in every kernel.
+__device__ __forceinline__ float bf16_to_f32(uint16_t x) {
+  return __uint_as_float(static_cast<uint32_t>(x) << 16);
+}
+
+// float -> bf16, round to nearest even; NaN stays NaN (quiet bit forced).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+// ---- generic path (any supported dtype / head_dim / windows) --------------
+hipError_t generic_fwd(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
+                       const void* vp, void* out, float* lse, hipStream_t st);
+hipError_t generic_bwd(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
+                       const void* vp, const void* out, const void* dout, const float* lse, void* dq,
+                       void* dk, void* dkp, void* dv, void* dvp, float* delta, hipStream_t st);
+
+// ---- gfx950 MFMA path (bf16, head_dim 64/128, w2 <= 64) --------------------
+bool mfma_fwd_supported(const Shape& s);
+hipError_t mfma_fwd(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
+                    const void* vp, void* out, float* lse, hipStream_t st);
+
+// Delta_i = <dO_i, O_i> for every query, [B, H, N] float32.
+hipError_t launch_delta(const Shape& s, const void* out, const void* dout, float* delta,
+                        hipStream_t st);
+
+}  // namespace sa

@@ -1,0 +1,186 @@
+"""Shared helpers of the GPU parity tests: run the HIP path through the C ABI,
+run the oracle on the same seeded inputs (whole tensors or sampled rows), and
+measure the differences.
+
+Tolerances (the bar each parity test asserts), with the arithmetic behind them:
+
+* fp32 data: max |x - ref| / max |ref| <= 1e-5 per tensor. The GPU computes in
+  fp32 with fp32 products; with D <= 128 terms per logit and <= w1*w2 pairs per
+  query, the relative rounding error stays near 1e-6.
+* bf16 data, forward: max |O - O_ref| <= 2e-2 (absolute) and, because |O| is
+  itself only ~1e-2 at the benchmark shapes, also the normwise
+  ||O - O_ref|| / ||O_ref|| <= 1e-2. The kernels round the modulated query
+  q_i o k'_k, the probabilities P and the output to bf16 (unit roundoff
+  2^-9 = 2e-3 each), which gives a normwise error of a few 1e-3.
+  LSE (fp32 output): |LSE - ref| <= 2e-2; the bf16 rounding of the modulated
+  query perturbs each logit by ~2^-9 |logit|.
+* bf16 data, backward: per gradient max |g - ref| / max |ref| <= 5e-2 and
+  normwise <= 2e-2 (P, dS and the modulated operands are rounded to bf16
+  before each matrix product, and the result is rounded to bf16).
+  Delta_i = <dO_i, O_i> is formed from the stored bf16 output, so a gradient
+  that vanishes exactly (dQ, dK, dK' with unit windows or unit values) comes
+  out at ~2^-9 of the call's gradient scale instead of 0. A gradient whose
+  reference is that small (max |ref| below 10% of the largest gradient of the
+  call) is therefore measured against 10% of the largest gradient instead of
+  its own maximum, and its normwise error is not asserted.
+"""
+
+import json
+import os
+
+import numpy as np
+import torch
+
+import oracle as orc
+from paper_2507_02754_amd import simplicial_attn_bwd, simplicial_attn_fwd
+
+TOL = {
+    "fp32": dict(o_maxrel=1e-5, lse_abs=1e-5, g_maxrel=1e-5, o_norm=1e-5, g_norm=1e-5),
+    "bf16": dict(o_abs=2e-2, o_norm=1e-2, lse_abs=2e-2, g_maxrel=5e-2, g_norm=2e-2),
+}
+
+GRAD_NAMES = ("dq", "dk", "dkp", "dv", "dvp")
+
+
+def to64(t):
+    return t.detach().to("cpu", torch.float64).numpy()
+
+
+def gpu_forward(inputs, w1, w2, scale, device="cuda"):
+    q, k, kp, v, vp = (x.to(device) for x in inputs[:5])
+    out, lse = simplicial_attn_fwd(q, k, kp, v, vp, w1, w2, scale)
+    torch.cuda.synchronize()
+    return out, lse
+
+
+def gpu_backward(inputs, out, lse, w1, w2, scale, device="cuda"):
+    q, k, kp, v, vp, do = (x.to(device) for x in inputs)
+    grads = simplicial_attn_bwd(q, k, kp, v, vp, out, do, lse, w1, w2, scale)
+    torch.cuda.synchronize()
+    return grads
+
+
+def head_arrays(inputs, b, h):
+    """fp64 [N, D] arrays of head (b, h) from [B, N, H, D] tensors."""
+    return [x[b, :, h, :].to(torch.float64).numpy() for x in inputs]
+
+
+def err(x, ref):
+    x = np.asarray(x, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    diff = np.abs(x - ref)
+    mref = float(np.max(np.abs(ref))) if ref.size else 0.0
+    nref = float(np.linalg.norm(ref))
+    return dict(
+        max_abs=float(diff.max()) if diff.size else 0.0,
+        max_rel=float(diff.max()) / mref if mref > 0 else float(diff.max() if diff.size else 0.0),
+        norm_rel=float(np.linalg.norm(x - ref)) / nref if nref > 0 else float(np.linalg.norm(x - ref)),
+        finite=bool(np.all(np.isfinite(x))),
+    )
+
+
+def report(kind, label, metrics):
+    """Append one JSON line per check to $PARITY_REPORT (if set)."""
+    path = os.environ.get("PARITY_REPORT")
+    if path:
+        with open(path, "a") as f:
+            f.write(json.dumps({"kind": kind, "case": label, **metrics}) + "\n")
+
+
+def check_forward(o, lse, o_ref, lse_ref, dtype, label=""):
+    t = TOL[dtype]
+    eo, el = err(o, o_ref), err(lse, lse_ref)
+    report("fwd", label, {"o": eo, "lse": el})
+    assert eo["finite"] and el["finite"], f"{label}: non-finite output"
+    if dtype == "fp32":
+        assert eo["max_rel"] <= t["o_maxrel"], f"{label}: O {eo}"
+    else:
+        assert eo["max_abs"] <= t["o_abs"], f"{label}: O {eo}"
+        assert eo["norm_rel"] <= t["o_norm"], f"{label}: O {eo}"
+    assert el["max_abs"] <= t["lse_abs"], f"{label}: LSE {el}"
+    return eo, el
+
+
+def check_grads(grads, refs, dtype, label="", rows=None):
+    """grads/refs: sequences of 5 arrays; rows: optional per-gradient row index lists."""
+    t = TOL[dtype]
+    out = {}
+    pairs = []
+    for idx, (name, g, r) in enumerate(zip(GRAD_NAMES, grads, refs)):
+        if rows is not None:
+            sel = rows[idx]
+            if len(sel) == 0:
+                continue
+            g, r = g[sel], r[sel]
+        pairs.append((name, np.asarray(g, np.float64), np.asarray(r, np.float64)))
+    gscale = max(float(np.max(np.abs(r))) if r.size else 0.0 for _, _, r in pairs)
+    for name, g, r in pairs:
+        e = err(g, r)
+        mref = float(np.max(np.abs(r))) if r.size else 0.0
+        degenerate = dtype == "bf16" and mref < 0.1 * gscale
+        if degenerate:
+            e["max_rel"] = e["max_abs"] / (0.1 * gscale)
+            e["degenerate"] = True
+        out[name] = e
+        assert e["finite"], f"{label}: {name} non-finite"
+        assert e["max_rel"] <= t["g_maxrel"], f"{label}: {name} {e}"
+        if not degenerate:
+            assert e["norm_rel"] <= t["g_norm"], f"{label}: {name} {e}"
+    report("bwd", label, out)
+    return out
+
+
+def full_oracle(inputs, w1, w2, scale, backward=True):
+    """Oracle on whole tensors (small shapes only)."""
+    arrs = [x.to(torch.float64).numpy() for x in inputs]
+    o, lse = orc.forward_batched(*arrs[:5], w1, w2, scale)
+    grads = orc.backward_batched(*arrs, w1, w2, scale) if backward else None
+    return o, lse, grads
+
+
+def sample_rows(n, w1, w2, extra=4, seed=0):
+    """Query rows spanning the clipped start, window edges, tile edges, middle and end."""
+    cand = {0, 1, 2, w2 - 1, w2, w1 - 2, w1 - 1, w1, w1 + 1, 63, 64, 255, 256,
+            n // 2, n // 2 + 1, n - 2, n - 1}
+    rng = np.random.default_rng(seed)
+    cand.update(int(x) for x in rng.integers(0, n, size=extra))
+    return sorted(c for c in cand if 0 <= c < n)
+
+
+def sampled_forward_check(inputs, o_gpu, lse_gpu, w1, w2, scale, dtype, heads, rows, label=""):
+    o_gpu = to64(o_gpu)
+    lse_gpu = to64(lse_gpu)
+    os_, ors, ls, lrs = [], [], [], []
+    for (b, h) in heads:
+        q, k, kp, v, vp = head_arrays(inputs[:5], b, h)
+        o_ref, lse_ref = orc.forward(q, k, kp, v, vp, w1, w2, scale, queries=rows)
+        os_.append(o_gpu[b, rows, h, :])
+        ors.append(o_ref[rows])
+        ls.append(lse_gpu[b, h, rows])
+        lrs.append(lse_ref[rows])
+    return check_forward(np.concatenate(os_), np.concatenate(ls), np.concatenate(ors),
+                         np.concatenate(lrs), dtype, label)
+
+
+def sampled_backward_check(inputs, grads_gpu, w1, w2, scale, dtype, heads, q_rows, key_rows,
+                           label=""):
+    """dQ at q_rows; dK/dV and dK'/dV' at key_rows (the oracle runs every query
+    touching those rows, so the sampled rows are exact)."""
+    n = inputs[0].shape[1]
+    w1c, w2c = min(w1, n), min(w2, n)
+    queries = set(q_rows)
+    for r in key_rows:
+        queries.update(range(r, min(n, r + max(w1c, w2c))))
+    queries = sorted(queries)
+    g_gpu = [to64(g) for g in grads_gpu]
+    got = [[] for _ in range(5)]
+    ref = [[] for _ in range(5)]
+    for (b, h) in heads:
+        arrs = head_arrays(inputs, b, h)
+        g_ref = orc.backward(*arrs, w1, w2, scale, queries=queries)
+        for t in range(5):
+            rows = q_rows if t == 0 else key_rows
+            got[t].append(g_gpu[t][b, rows, h, :])
+            ref[t].append(g_ref[t][rows])
+    return check_grads([np.concatenate(x) for x in got], [np.concatenate(x) for x in ref],
+                       dtype, label)

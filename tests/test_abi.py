@@ -1,0 +1,145 @@
+"""The C-ABI library: it builds, loads, exports every declared symbol, and rejects
+invalid arguments on the host before any HIP call (so these run without a GPU).
+"""
+
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2507_02754_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "simplicial_attn.h")
+
+# Fake device addresses for calls that must be rejected before any launch. They
+# are only used where the validation must fail; on a machine with a GPU these
+# tests are skipped so a validation bug can never launch on them.
+A = 0x10000  # 16-byte aligned
+MISALIGNED = 0x10008
+
+
+def _no_gpu():
+    import torch
+    return torch.cuda.device_count() == 0
+
+
+only_without_gpu = pytest.mark.skipif(not _no_gpu(), reason="fake-pointer checks run only where no GPU is visible")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(binding.LIB_PATH):
+        from paper_2507_02754_amd import build
+        build.build()
+    return binding.load_library()
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(simplicial_attn_\w+)\s*\(", src)))
+
+
+def test_header_declares_the_expected_entry_points():
+    assert declared_functions() == sorted([
+        "simplicial_attn_fwd", "simplicial_attn_bwd", "simplicial_attn_bwd_workspace_size",
+        "simplicial_attn_error_string", "simplicial_attn_abi_version", "simplicial_attn_path_name",
+    ])
+
+
+def test_library_exports_every_declared_symbol(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", binding.LIB_PATH],
+                         capture_output=True, text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (simplicial_attn_\w+)", out))
+    for name in declared_functions():
+        assert name in exported, name
+        assert hasattr(lib, name)
+
+
+def test_abi_version_matches_header(lib):
+    m = re.search(r"#define SIMPLICIAL_ATTN_ABI_VERSION (\d+)", open(HEADER).read())
+    assert binding.simplicial_attn_abi_version() == int(m.group(1))
+
+
+def test_error_strings(lib):
+    for code in range(5):
+        s = binding.simplicial_attn_error_string(code)
+        assert s and s != "unknown status"
+    assert binding.simplicial_attn_error_string(99) == "unknown status"
+
+
+def _fwd(lib, ptrs=None, B=1, N=64, H=2, D=128, w1=16, w2=8, scale=0.1, dtype=1):
+    ptrs = ptrs or [A] * 7
+    return lib.simplicial_attn_fwd(*[ctypes.c_void_p(p) for p in ptrs], B, N, H, D, w1, w2,
+                                   ctypes.c_float(scale), dtype, None)
+
+
+def _bwd(lib, ptrs=None, ws_bytes=1 << 30, B=1, N=64, H=2, D=128, w1=16, w2=8, scale=0.1, dtype=1):
+    ptrs = ptrs or [A] * 14
+    return lib.simplicial_attn_bwd(*[ctypes.c_void_p(p) for p in ptrs], ctypes.c_size_t(ws_bytes),
+                                   B, N, H, D, w1, w2, ctypes.c_float(scale), dtype, None)
+
+
+@only_without_gpu
+def test_forward_rejects_invalid_arguments(lib):
+    for i in range(7):
+        ptrs = [A] * 7
+        ptrs[i] = 0
+        assert _fwd(lib, ptrs) == 1, f"null pointer {i}"
+        ptrs[i] = MISALIGNED
+        assert _fwd(lib, ptrs) == 1, f"misaligned pointer {i}"
+    assert _fwd(lib, B=0) == 1
+    assert _fwd(lib, N=0) == 1
+    assert _fwd(lib, H=-1) == 1
+    assert _fwd(lib, D=0) == 1
+    assert _fwd(lib, w1=0) == 1
+    assert _fwd(lib, w2=-3) == 1
+    assert _fwd(lib, scale=float("nan")) == 1
+    assert _fwd(lib, scale=float("inf")) == 1
+    assert _fwd(lib, N=1 << 31) == 1          # does not fit a 32-bit index
+    assert _fwd(lib, B=1 << 20, N=1 << 20, H=1 << 10) == 1  # overflow
+    assert _fwd(lib, D=48) == 2
+    assert _fwd(lib, D=256) == 2
+    assert _fwd(lib, dtype=2) == 2
+    assert _fwd(lib, dtype=-1) == 2
+
+
+@only_without_gpu
+def test_backward_rejects_invalid_arguments(lib):
+    for i in range(14):
+        ptrs = [A] * 14
+        ptrs[i] = 0
+        assert _bwd(lib, ptrs) == 1, f"null pointer {i}"
+        ptrs[i] = MISALIGNED
+        assert _bwd(lib, ptrs) == 1, f"misaligned pointer {i}"
+    assert _bwd(lib, w1=0) == 1
+    assert _bwd(lib, D=40) == 2
+    need = binding.simplicial_attn_bwd_workspace_size(1, 64, 2, 128, 16, 8, 1)
+    assert need > 0
+    assert _bwd(lib, ws_bytes=need - 1) == 3
+    assert _bwd(lib, ws_bytes=0) == 3
+
+
+def test_workspace_size(lib):
+    f = binding.simplicial_attn_bwd_workspace_size
+    assert f(0, 64, 2, 128, 16, 8, 1) == 0
+    assert f(1, 64, 2, 128, 16, 8, 7) == 0
+    assert f(1, 64, 2, 128, 0, 8, 1) == 0
+    # at least one float of Delta per (b, h, query), 256-byte granular
+    for shape in [(1, 64, 2, 128, 16, 8, 1), (2, 8192, 8, 128, 512, 32, 1), (1, 128, 1, 64, 16, 8, 0)]:
+        ws = f(*shape)
+        b, n, h = shape[0], shape[1], shape[2]
+        assert ws >= 4 * b * h * n and ws % 256 == 0
+
+
+def test_path_names(lib):
+    f = binding.simplicial_attn_path_name
+    assert f(0, 1, 128, 1, 64, 16, 8, 0) == "generic"
+    assert f(1, 1, 128, 1, 64, 16, 8, 0) == "generic"
+    assert f(0, 1, 128, 1, 48, 16, 8, 0) == "invalid"
+    assert f(2, 1, 128, 1, 64, 16, 8, 0) == "invalid"
+    for which in (0, 1):
+        assert f(which, 1, 32768, 16, 128, 512, 32, 1) in ("generic", "mfma_bf16")

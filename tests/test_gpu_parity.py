@@ -1,0 +1,157 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle on the
+same seeded inputs. Small shapes compare every element; the full workload
+shapes compare sampled rows that the oracle computes exactly."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as orc
+from paper_2507_02754_amd import (load_library, simplicial_attn_bwd, simplicial_attn_fwd,
+                                  simplicial_attn_path_name)
+from paper_2507_02754_amd.workloads import WORKLOADS, draw, make_inputs
+
+import parity as P
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    load_library()
+
+
+def _announce(label):
+    print(f"\n[parity] {label}", flush=True)
+
+
+def test_tiny_fp32_workload_full():
+    w = WORKLOADS["tiny_fp32"]
+    _announce(f"{w.name} {w.shape()} w1={w.w1} w2={w.w2}")
+    inputs = make_inputs(w)
+    o, lse = P.gpu_forward(inputs, w.w1, w.w2, w.scale)
+    grads = P.gpu_backward(inputs, o, lse, w.w1, w.w2, w.scale)
+    o_ref, lse_ref, g_ref = P.full_oracle(inputs, w.w1, w.w2, w.scale)
+    P.check_forward(P.to64(o), P.to64(lse), o_ref, lse_ref, "fp32", w.name)
+    P.check_grads([P.to64(g) for g in grads], g_ref, "fp32", w.name)
+
+
+SMALL = [
+    # (B, H, N, D, w1, w2, dtype)
+    (1, 2, 300, 128, 64, 32, "bf16"),    # several query tiles and a ragged tail
+    (2, 1, 200, 64, 40, 32, "bf16"),     # head_dim 64
+    (1, 1, 333, 128, 96, 64, "bf16"),    # w2 = 64
+    (1, 1, 150, 128, 16, 32, "bf16"),    # w1 < w2
+    (1, 1, 20, 128, 512, 32, "bf16"),    # both windows longer than the sequence
+    (1, 3, 1, 128, 512, 32, "bf16"),     # a single query
+    (1, 1, 100, 128, 1, 1, "bf16"),      # unit windows
+    (1, 1, 129, 128, 33, 7, "bf16"),     # w2 not a multiple of 32
+    (1, 1, 100, 64, 7, 5, "fp32"),
+    (2, 2, 70, 32, 9, 3, "fp32"),
+    (1, 1, 70, 16, 9, 3, "bf16"),
+]
+
+
+@pytest.mark.parametrize("shape", SMALL, ids=[str(s) for s in SMALL])
+def test_small_shapes_full(shape):
+    b, h, n, d, w1, w2, dt = shape
+    _announce(f"small {shape} fwd={simplicial_attn_path_name(0, b, n, h, d, w1, w2, 1 if dt == 'bf16' else 0)}")
+    inputs = draw((b, n, h, d), seed=100 + n, dtype=torch.float32 if dt == "fp32" else torch.bfloat16)
+    scale = d ** -0.5
+    o, lse = P.gpu_forward(inputs, w1, w2, scale)
+    grads = P.gpu_backward(inputs, o, lse, w1, w2, scale)
+    o_ref, lse_ref, g_ref = P.full_oracle(inputs, w1, w2, scale)
+    P.check_forward(P.to64(o), P.to64(lse), o_ref, lse_ref, dt, str(shape))
+    P.check_grads([P.to64(g) for g in grads], g_ref, dt, str(shape))
+
+
+def _is_fast(w, which):
+    return simplicial_attn_path_name(which, w.B, w.N, w.H, w.D, w.w1, w.w2, 1) != "generic"
+
+
+@pytest.mark.parametrize("name", ["fwd_bf16_n4k", "fb_bf16_n8k", "long_bf16_n32k", "wide_bf16_n16k"])
+def test_full_size_workloads_sampled(name):
+    w = WORKLOADS[name]
+    if not _is_fast(w, 0):
+        pytest.skip("full-size shapes are only run on the MFMA path")
+    _announce(f"{w.name} {w.shape()} w1={w.w1} w2={w.w2}")
+    inputs = make_inputs(w)
+    o, lse = P.gpu_forward(inputs, w.w1, w.w2, w.scale)
+    heads = [(0, 0), (w.B - 1, w.H - 1)]
+    rows = P.sample_rows(w.N, w.w1, w.w2, seed=w.seed)
+    P.sampled_forward_check(inputs, o, lse, w.w1, w.w2, w.scale, w.dtype, heads, rows, w.name)
+    if not w.backward or not _is_fast(w, 1):
+        return
+    grads = P.gpu_backward(inputs, o, lse, w.w1, w.w2, w.scale)
+    key_rows = [0, 1, w.N // 2, w.N - 2, w.N - 1]
+    q_rows = rows
+    bw_heads = heads if w.w1 * w.w2 <= 512 * 32 else heads[:1]
+    P.sampled_backward_check(inputs, grads, w.w1, w.w2, w.scale, w.dtype, bw_heads, q_rows,
+                             key_rows, w.name)
+
+
+def test_backward_is_deterministic():
+    shape = (1, 2, 400, 128, 128, 32)
+    b, h, n, d, w1, w2 = shape
+    _announce(f"determinism {shape}")
+    inputs = [x.cuda() for x in draw((b, n, h, d), seed=7)]
+    o, lse = simplicial_attn_fwd(*inputs[:5], w1, w2)
+    runs = []
+    for _ in range(3):
+        g = simplicial_attn_bwd(*inputs[:5], o, inputs[5], lse, w1, w2)
+        torch.cuda.synchronize()
+        runs.append([x.clone() for x in g])
+    for r in runs[1:]:
+        for a, c in zip(runs[0], r):
+            assert torch.equal(a.view(torch.int16), c.view(torch.int16))
+
+
+def test_unit_values_through_gpu():
+    """V = V' = 1 gives O = 1 and zero key/query gradients (exact identities)."""
+    b, h, n, d, w1, w2 = 1, 2, 260, 128, 64, 32
+    _announce("unit values")
+    q, k, kp, _, _, do = draw((b, n, h, d), seed=8)
+    ones = torch.ones_like(q)
+    dev = [x.cuda() for x in (q, k, kp, ones, ones, do)]
+    o, lse = simplicial_attn_fwd(*dev[:5], w1, w2)
+    dq, dk, dkp, dv, dvp = simplicial_attn_bwd(*dev[:5], o, dev[5], lse, w1, w2)
+    torch.cuda.synchronize()
+    assert torch.allclose(o.float(), torch.ones_like(o, dtype=torch.float32), atol=8e-3)
+    # dv_j = sum_{i,k} P_ijk dO_i: compare with the oracle; dq, dk, dkp vanish.
+    for g in (dq, dk, dkp):
+        assert g.float().abs().max().item() <= 5e-3 * max(1.0, dv.float().abs().max().item())
+
+
+def test_guard_bands_untouched_and_no_stray_reads():
+    """Tensors live inside NaN-filled allocations; outputs must be finite and the
+    guard regions around every output must still be NaN afterwards."""
+    b, h, n, d, w1, w2 = 1, 2, 190, 128, 64, 32
+    _announce("guard bands")
+    inputs = draw((b, n, h, d), seed=9)
+    numel = b * n * h * d
+    pad = 4096
+
+    def guarded(x=None, dtype=torch.bfloat16, count=numel):
+        buf = torch.full((count + 2 * pad,), float("nan"), dtype=dtype, device="cuda")
+        view = buf[pad:pad + count]
+        if x is not None:
+            view.copy_(x.reshape(-1))
+        return buf, view
+
+    bufs = [guarded(x) for x in inputs]
+    t = [v.view(b, n, h, d) for _, v in bufs]
+    ob, ov = guarded()
+    lb, lv = guarded(dtype=torch.float32, count=b * h * n)
+    o, lse = simplicial_attn_fwd(*t[:5], w1, w2, out=ov.view(b, n, h, d), lse=lv.view(b, h, n))
+    gbufs = [guarded() for _ in range(5)]
+    grads = tuple(v.view(b, n, h, d) for _, v in gbufs)
+    simplicial_attn_bwd(*t[:5], o, t[5], lse, w1, w2, grads=grads)
+    torch.cuda.synchronize()
+    for buf, view in [(ob, ov), (lb, lv), *gbufs]:
+        assert torch.isfinite(view.float()).all()
+        assert torch.isnan(buf[:pad].float()).all() and torch.isnan(buf[-pad:].float()).all()
+    o_ref, lse_ref, g_ref = P.full_oracle(inputs, w1, w2, d ** -0.5)
+    P.check_forward(P.to64(o), P.to64(lse), o_ref, lse_ref, "bf16", "guard")
+    P.check_grads([P.to64(g) for g in grads], g_ref, "bf16", "guard")
