@@ -51,6 +51,7 @@ Path choose_path(int which, int64_t B, int64_t N, int64_t H, int64_t D, int32_t 
   if (check_sizes(B, N, H, D, w1, w2, dtype) != SA_OK) return Path::Invalid;
   const Shape s = make_shape(B, N, H, D, w1, w2, 1.0f, dtype);
   if (which == 0 && sa::mfma_fwd_supported(s)) return Path::Mfma;
+  if (which == 1 && sa::mfma_bwd_supported(s)) return Path::Mfma;
   return Path::Generic;
 }
 
@@ -105,6 +106,8 @@ int simplicial_attn_fwd(const void* q, const void* k, const void* kp, const void
 size_t simplicial_attn_bwd_workspace_size(int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1,
                                           int32_t w2, int32_t dtype) {
   if (check_sizes(B, N, H, D, w1, w2, dtype) != SA_OK) return 0;
+  if (choose_path(1, B, N, H, D, w1, w2, dtype) == Path::Mfma)
+    return sa::mfma_bwd_plan(make_shape(B, N, H, D, w1, w2, 1.0f, dtype)).bytes;
   // Delta: one float per (b, h, query), rounded up to 256 bytes.
   const size_t delta = ((static_cast<size_t>(B * H * N) * sizeof(float)) + 255) & ~size_t(255);
   return delta;
@@ -132,6 +135,9 @@ int simplicial_attn_bwd(const void* q, const void* k, const void* kp, const void
     case Path::Generic:
       return to_status(sa::generic_bwd(s, q, k, kp, v, vp, out, dout, lse, dq, dk, dkp, dv, dvp,
                                        delta, st));
+    case Path::Mfma:
+      return to_status(sa::mfma_bwd(s, q, k, kp, v, vp, out, dout, lse, dq, dk, dkp, dv, dvp,
+                                    workspace, st));
     default: return SA_ERR_UNSUPPORTED;
   }
 }

@@ -1,0 +1,696 @@
+// Backward pass on gfx950 matrix cores (bf16 data, head_dim 64 or 128, w2 <= 64).
+//
+// Gradients of Section 7, written over the rows r = (i, k) of the forward
+// (q~_r = scale * q_i o k'_k, do~_r = dO_i o v'_k, P_rj = exp(A_ijk - LSE_i)):
+//     dP_rj = < do~_r, v_j >            dS_rj = P_rj (dP_rj - Delta_i)
+//     dK_j  = sum_r dS_rj q~_r           dV_j  = sum_r P_rj do~_r
+//     dQ~_r = sum_j dS_rj k_j            U~_r  = sum_j P_rj v_j
+//     dq_i  = scale sum_k k'_k o dQ~_r   dk'_k = scale sum_i q_i o dQ~_r
+//     dv'_k = sum_i dO_i o U~_r
+// (dsoftmax read as dS = P (dP - Delta) with Delta_i = <dO_i, O_i>.)
+//
+// Following Section 7's split into two kernels that avoid atomics:
+//   * bwd_q  (query-stationary): recomputes S and dP per j-block of the window
+//     and accumulates dQ~ and U~ on the matrix cores; its epilogue reduces the
+//     k-rows into dq_i and scatters the dk'/dv' contributions into an LDS ring
+//     of k-rows. A workgroup walks a chunk of consecutive query tiles, so each
+//     k-row is completed inside the chunk except the w2-1 rows at each chunk
+//     boundary; those partial sums go to the workspace and a fix-up kernel adds
+//     the two halves in a fixed order (deterministic, no atomics). This plays
+//     the role of the paper's even/odd two-stage scheme (Algorithm 2).
+//   * bwd_kv (key-stationary): each wavefront keeps 32 rows of K and V in
+//     registers and walks the query rows (i, k) that see them; the workgroup
+//     forms q~ and do~ of one query's rows cooperatively in LDS (row-major and
+//     transposed) and every wavefront contracts them with its keys.
+// Delta is computed by a small row-dot kernel first.
+#include "mfma_common.h"
+
+namespace sa {
+
+// ---- workspace layout (shared with the host's size query) --------------------
+BwdPlan mfma_bwd_plan(const Shape& s) {
+  BwdPlan p{};
+  p.G = s.w2 <= 32 ? 1 : 2;
+  p.W2P = 32 * p.G;
+  const long bh = static_cast<long>(s.B) * s.H;
+  // Chunk length: enough workgroups to fill the chip several times, at least
+  // one halo long, a multiple of every tile height.
+  long cq = 128;
+  while (cq < 1024 && bh * ((s.N + cq - 1) / cq) > 4096) cq *= 2;
+  if (cq < p.W2P) cq = p.W2P;
+  p.CQ = static_cast<int>(cq);
+  p.nchunks = static_cast<int>((s.N + cq - 1) / cq);
+  const size_t halo_rows = static_cast<size_t>(p.W2P - 1);
+  p.halo_floats = bh * static_cast<size_t>(p.nchunks) * halo_rows * s.D;
+  const size_t delta_bytes = ((bh * static_cast<size_t>(s.N) * 4) + 255) & ~size_t(255);
+  p.delta_off = 0;
+  p.halo_off = delta_bytes;  // 4 arrays: head/tail x dk'/dv'
+  p.bytes = delta_bytes + 4 * p.halo_floats * 4;
+  return p;
+}
+
+namespace {
+
+// ------------------------------------------------------------------ delta ---
+// Delta_i = <dO_i, O_i>; 16 lanes per query row (8 bf16 each for D = 128).
+template <int D>
+__global__ __launch_bounds__(256) void delta_kernel(Shape s, const uint16_t* __restrict__ out,
+                                                     const uint16_t* __restrict__ dout,
+                                                     float* __restrict__ delta) {
+  constexpr int LPR = D / 8;  // lanes per row
+  const long row = (static_cast<long>(blockIdx.x) * 256 + threadIdx.x) / LPR;
+  const int part = threadIdx.x % LPR;
+  const long total = static_cast<long>(s.B) * s.H * s.N;
+  float acc = 0.f;
+  long bh = 0, i = 0;
+  if (row < total) {
+    bh = row / s.N;
+    i = row - bh * s.N;
+    const long b = bh / s.H, h = bh - b * s.H;
+    const size_t off = ((static_cast<size_t>(b) * s.N + i) * s.H + h) * D + 8 * part;
+    const u32x4_t o = ldg128(out + off);
+    const u32x4_t g = ldg128(dout + off);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc += bf16_lo(o[e]) * bf16_lo(g[e]) + bf16_hi(o[e]) * bf16_hi(g[e]);
+  }
+#pragma unroll
+  for (int off = LPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+  if (row < total && part == 0) delta[row] = acc;
+}
+
+// Staging of one 32-row block of a [.., N, H, D] tensor into LDS, both
+// row-major ([32][D + 8]) and transposed ([D][32 + 4]), zero outside [0, N).
+template <int D, int NTHREADS>
+struct DualStage {
+  static constexpr int rStride = D + 8;
+  static constexpr int tStride = 32 + 4;
+  static constexpr int rowBytes = 32 * rStride * 2;
+  static constexpr int tBytes = D * tStride * 2;
+  static constexpr int bytes = rowBytes + tBytes;
+  // one work item = (row pair p, 8-column chunk dc): 16 pairs x D/8 chunks
+  static constexpr int items = 16 * (D / 8);
+  static constexpr int perThread = (items + NTHREADS - 1) / NTHREADS;
+  u32x4_t reg[perThread][2];
+
+  // `slot` is the caller's thread index, rotated so that two stagings issued
+  // together use disjoint threads when the block has twice `items` threads.
+  __device__ void load(const uint16_t* src, size_t base, size_t rs, int jb, int N, int tid) {
+#pragma unroll
+    for (int x = 0; x < perThread; ++x) {
+      const int it = tid + x * NTHREADS;
+      const int p = it & 15, dc = it >> 4;
+#pragma unroll
+      for (int y = 0; y < 2; ++y) {
+        const int j = jb + 2 * p + y;
+        u32x4_t z = {0u, 0u, 0u, 0u};
+        if (it < items && j >= 0 && j < N) z = ldg128(src + base + static_cast<size_t>(j) * rs + 8 * dc);
+        reg[x][y] = z;
+      }
+    }
+  }
+  __device__ void store(char* dst, int tid) const {
+    uint16_t* rm = reinterpret_cast<uint16_t*>(dst);
+    uint16_t* tr = reinterpret_cast<uint16_t*>(dst + rowBytes);
+#pragma unroll
+    for (int x = 0; x < perThread; ++x) {
+      const int it = tid + x * NTHREADS;
+      if (it >= items) continue;
+      const int p = it & 15, dc = it >> 4;
+      *reinterpret_cast<u32x4_t*>(rm + (2 * p) * rStride + 8 * dc) = reg[x][0];
+      *reinterpret_cast<u32x4_t*>(rm + (2 * p + 1) * rStride + 8 * dc) = reg[x][1];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const unsigned a = reg[x][0][e], b = reg[x][1][e];
+        *reinterpret_cast<unsigned*>(tr + (8 * dc + 2 * e) * tStride + 2 * p) = (a & 0xffffu) | (b << 16);
+        *reinterpret_cast<unsigned*>(tr + (8 * dc + 2 * e + 1) * tStride + 2 * p) = (a >> 16) | (b & 0xffff0000u);
+      }
+    }
+  }
+};
+
+// A-operand fragment (32 rows x 16 K-slots) from a row-major LDS tile.
+template <int STRIDE>
+__device__ __forceinline__ u32x4_t frag_rows(const uint16_t* tile, int c, int h, int t) {
+  return *reinterpret_cast<const u32x4_t*>(tile + c * STRIDE + 16 * t + 8 * h);
+}
+// Fragment whose K-slots run over the 32 rows of a transposed LDS tile, in the
+// order the 32x32 accumulator layout produces them (see mfma_common.h).
+template <int STRIDE>
+__device__ __forceinline__ u32x4_t frag_cols(const uint16_t* ttile, int row, int h, int u) {
+  const uint16_t* p = ttile + row * STRIDE + 16 * u + 4 * h;
+  const u32x2_t a0 = *reinterpret_cast<const u32x2_t*>(p);
+  const u32x2_t a1 = *reinterpret_cast<const u32x2_t*>(p + 8);
+  return u32x4_t{a0[0], a0[1], a1[0], a1[1]};
+}
+
+// Accumulator register v of a 32x32 tile holds row 8*(v/4) + 4*h + (v%4).
+__device__ __forceinline__ int acc_row(int v, int h) { return 8 * (v >> 2) + 4 * h + (v & 3); }
+
+// ------------------------------------------------------------------ bwd_q ---
+template <int D, int G, int WAVES>
+struct BwdQLds {
+  using St = DualStage<D, 64 * WAVES>;
+  static constexpr int stageBytes = 2 * St::bytes;  // K and V
+  static constexpr int mainBytes = 2 * stageBytes;  // double buffered
+  static constexpr int rStride = D + 4;             // fp32 rows of the reductions
+  static constexpr int QW = WAVES / G;
+  static constexpr int RB = 32 * G + QW;            // ring rows
+  static constexpr int redWaves = WAVES < 4 ? WAVES : 4;
+  static constexpr int redBytes = redWaves * 32 * rStride * 4;
+  static constexpr int region0 = mainBytes > redBytes ? mainBytes : redBytes;
+  static constexpr int ringBytes = 2 * RB * rStride * 4;
+  static constexpr int bytes = region0 + ringBytes;
+};
+
+template <int D, int G, int WAVES>
+__global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
+    Shape s, BwdPlan plan, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+    const uint16_t* __restrict__ kp, const uint16_t* __restrict__ v, const uint16_t* __restrict__ vp,
+    const uint16_t* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ delta,
+    uint16_t* __restrict__ dq, uint16_t* __restrict__ dkp, uint16_t* __restrict__ dvp,
+    float* __restrict__ ws) {
+  constexpr int NT = D / 16, NDT = D / 32;
+  constexpr int W2P = 32 * G;
+  constexpr int NTH = 64 * WAVES;
+  using L = BwdQLds<D, G, WAVES>;
+  using St = typename L::St;
+  constexpr int QW = L::QW, RB = L::RB;
+  __shared__ __attribute__((aligned(16))) char smem[L::bytes];
+  float* ring_kp = reinterpret_cast<float*>(smem + L::region0);
+  float* ring_vp = ring_kp + RB * L::rStride;
+
+  const int total = plan.nchunks * s.B * s.H;
+  const int per_xcd = (total + 7) / 8;
+  const int logical = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+  if (logical >= total) return;
+  const int bh = logical / plan.nchunks;
+  const int chunk = logical - bh * plan.nchunks;
+  const int b = bh / s.H, hh = bh - b * s.H;
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63, c = lane & 31, h = lane >> 5;
+  const int qs = wave / G, g = wave % G;
+  const size_t rs = static_cast<size_t>(s.H) * D;
+  const size_t base = (static_cast<size_t>(b) * s.N * s.H + hh) * D;
+  const int N = s.N, w1 = s.w1, w2 = s.w2;
+  const int cs = chunk * plan.CQ, ce = min(N, cs + plan.CQ);
+  const int kbase = cs - W2P + 1;  // ring row of k is (k - kbase) % RB
+  const float qscale = s.scale * kLog2e;
+  const size_t stat = static_cast<size_t>(bh) * N;
+  const size_t halo = static_cast<size_t>(W2P - 1) * D;
+  float* ws_head_kp = ws + (static_cast<size_t>(bh) * plan.nchunks + chunk) * halo;
+  float* ws_head_vp = ws_head_kp + plan.halo_floats;
+  float* ws_tail_kp = ws_head_vp + plan.halo_floats;
+  float* ws_tail_vp = ws_tail_kp + plan.halo_floats;
+
+  for (int x = tid; x < 2 * RB * L::rStride; x += NTH) ring_kp[x] = 0.f;
+
+  // Writes ring row k (complete or partial) to its destination and clears it.
+  auto flush_row = [&](int kr, bool tail) {
+    const int slot = (kr - kbase) % RB;
+    for (int d = lane; d < D; d += 64) {
+      float* a = ring_kp + slot * L::rStride + d;
+      float* bv = ring_vp + slot * L::rStride + d;
+      if (kr >= 0) {
+        if (kr < cs) {
+          const size_t o = static_cast<size_t>(kr - kbase) * D + d;
+          ws_head_kp[o] = *a;
+          ws_head_vp[o] = *bv;
+        } else if (tail) {
+          const size_t o = static_cast<size_t>(kr - (ce - W2P + 1)) * D + d;
+          ws_tail_kp[o] = *a;
+          ws_tail_vp[o] = *bv;
+        } else {
+          dkp[base + static_cast<size_t>(kr) * rs + d] = f32_to_bf16(*a);
+          dvp[base + static_cast<size_t>(kr) * rs + d] = f32_to_bf16(*bv);
+        }
+      }
+      *a = 0.f;
+      *bv = 0.f;
+    }
+  };
+
+  St stk, stv;
+  const int vslot = NTH >= 2 * St::items ? (tid + St::items) % NTH : tid;
+  for (int i0 = cs; i0 < ce; i0 += QW) {
+    const int i = i0 + qs;
+    const int kk = i - W2P + 1 + 32 * g + c;
+    const bool rowvalid = i < ce && kk >= 0 && kk > i - w2;
+    const bool qvalid = i < ce;
+
+    u32x4_t qt[NT], ot[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      u32x4_t a4 = {0u, 0u, 0u, 0u}, b4 = {0u, 0u, 0u, 0u};
+      if (rowvalid) {
+        const u32x4_t qa = ldg128(q + base + static_cast<size_t>(i) * rs + 16 * t + 8 * h);
+        const u32x4_t ka = ldg128(kp + base + static_cast<size_t>(kk) * rs + 16 * t + 8 * h);
+        const u32x4_t oa = ldg128(dout + base + static_cast<size_t>(i) * rs + 16 * t + 8 * h);
+        const u32x4_t va = ldg128(vp + base + static_cast<size_t>(kk) * rs + 16 * t + 8 * h);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          a4[e] = pack_bf16x2(bf16_lo(qa[e]) * bf16_lo(ka[e]) * qscale,
+                              bf16_hi(qa[e]) * bf16_hi(ka[e]) * qscale);
+          b4[e] = pack_bf16x2(bf16_lo(oa[e]) * bf16_lo(va[e]), bf16_hi(oa[e]) * bf16_hi(va[e]));
+        }
+      }
+      qt[t] = a4;
+      ot[t] = b4;
+    }
+    const float lse2 = qvalid ? lse[stat + i] * kLog2e : 0.f;
+    const float dlt = qvalid ? delta[stat + i] : 0.f;
+
+    f32x16_t adq[NDT], au[NDT];
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) {
+      adq[dt] = f32x16_t{};
+      au[dt] = f32x16_t{};
+    }
+
+    const int jlo = i0 - w1 + 1;
+    const int nb = (w1 + QW - 1 + 31) / 32;
+    stk.load(k, base, rs, jlo, N, tid);
+    stv.load(v, base, rs, jlo, N, vslot);
+    stk.store(smem, tid);
+    stv.store(smem + St::bytes, vslot);
+    __syncthreads();
+
+    for (int blk = 0; blk < nb; ++blk) {
+      const int cur = blk & 1;
+      if (blk + 1 < nb) {
+        stk.load(k, base, rs, jlo + 32 * (blk + 1), N, tid);
+        stv.load(v, base, rs, jlo + 32 * (blk + 1), N, vslot);
+      }
+      char* sb = smem + cur * L::stageBytes;
+      const uint16_t* kr_ = reinterpret_cast<const uint16_t*>(sb);
+      const uint16_t* kt_ = reinterpret_cast<const uint16_t*>(sb + St::rowBytes);
+      const uint16_t* vr_ = reinterpret_cast<const uint16_t*>(sb + St::bytes);
+      const uint16_t* vt_ = reinterpret_cast<const uint16_t*>(sb + St::bytes + St::rowBytes);
+
+      const int lo = max(qs, -jlo) - 32 * blk;
+      const int hi = min(qs + w1 - 1, N - 1 - jlo) - 32 * blk;
+      const bool act = qvalid && hi >= 0 && lo <= 31 && lo <= hi;
+      if (act) {
+        f32x16_t sacc = f32x16_t{}, pacc = f32x16_t{};
+#pragma unroll
+        for (int t = 0; t < NT; ++t) sacc = mfma32(frag_rows<St::rStride>(kr_, c, h, t), qt[t], sacc);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) pacc = mfma32(frag_rows<St::rStride>(vr_, c, h, t), ot[t], pacc);
+        float pv[16], dv_[16];
+#pragma unroll
+        for (int vv = 0; vv < 16; ++vv) {
+          const int jl = acc_row(vv, h);
+          const bool ok = rowvalid && jl >= lo && jl <= hi;
+          const float p = ok ? fast_exp2(sacc[vv] - lse2) : 0.f;
+          pv[vv] = p;
+          dv_[vv] = p * (pacc[vv] - dlt);
+        }
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          u32x4_t pf, df;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            pf[e] = pack_bf16x2(pv[8 * u + 2 * e], pv[8 * u + 2 * e + 1]);
+            df[e] = pack_bf16x2(dv_[8 * u + 2 * e], dv_[8 * u + 2 * e + 1]);
+          }
+#pragma unroll
+          for (int dt = 0; dt < NDT; ++dt) {
+            adq[dt] = mfma32(frag_cols<St::tStride>(kt_, 32 * dt + c, h, u), df, adq[dt]);
+            au[dt] = mfma32(frag_cols<St::tStride>(vt_, 32 * dt + c, h, u), pf, au[dt]);
+          }
+        }
+      }
+      if (blk + 1 < nb) {
+        stk.store(smem + (cur ^ 1) * L::stageBytes, tid);
+        stv.store(smem + (cur ^ 1) * L::stageBytes + St::bytes, vslot);
+      }
+      __syncthreads();
+    }
+
+    // ---- dq_i = scale * sum_k k'_k o dQ~_(i,k): column sums over the k-rows ----
+    // accumulator register layout: lane holds row c, d = 32 dt + 8 (v/4) + 4 h + v%4
+    float* red = reinterpret_cast<float*>(smem);
+    constexpr int RW = L::redWaves;
+#pragma unroll
+    for (int round = 0; round < WAVES / RW; ++round) {
+      const bool mine = wave / RW == round;
+      if (mine) {
+        float* rw = red + (wave % RW) * 32 * L::rStride;
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+#pragma unroll
+          for (int qd = 0; qd < 4; ++qd) {
+            const int d = 32 * dt + 8 * qd + 4 * h;
+            u32x2_t kv = {0u, 0u};
+            if (rowvalid) kv = *reinterpret_cast<const u32x2_t*>(kp + base + static_cast<size_t>(kk) * rs + d);
+            float4 val;
+            val.x = bf16_lo(kv[0]) * adq[dt][4 * qd + 0];
+            val.y = bf16_hi(kv[0]) * adq[dt][4 * qd + 1];
+            val.z = bf16_lo(kv[1]) * adq[dt][4 * qd + 2];
+            val.w = bf16_hi(kv[1]) * adq[dt][4 * qd + 3];
+            *reinterpret_cast<float4*>(rw + c * L::rStride + d) = val;
+          }
+        }
+      }
+      __syncthreads();
+      // the first wave of each query (g == 0) sums its G waves' rows
+      if (mine && g == 0 && qvalid && 2 * lane < D) {
+        float o0 = 0.f, o1 = 0.f;
+#pragma unroll
+        for (int gg = 0; gg < G; ++gg) {
+          const float* rw = red + ((wave + gg) % RW) * 32 * L::rStride;
+#pragma unroll 8
+          for (int rr = 0; rr < 32; ++rr) {
+            const float2 x = *reinterpret_cast<const float2*>(rw + rr * L::rStride + 2 * lane);
+            o0 += x.x;
+            o1 += x.y;
+          }
+        }
+        *reinterpret_cast<unsigned*>(dq + base + static_cast<size_t>(i) * rs + 2 * lane) =
+            pack_bf16x2(o0 * s.scale, o1 * s.scale);
+      }
+      __syncthreads();
+    }
+
+    // ---- dk'/dv' contributions into the ring, one wavefront at a time ----
+    for (int ww = 0; ww < WAVES; ++ww) {
+      if (wave == ww && rowvalid) {
+        const int slot = (kk - kbase) % RB;
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+#pragma unroll
+          for (int qd = 0; qd < 4; ++qd) {
+            const int d = 32 * dt + 8 * qd + 4 * h;
+            const u32x2_t qv = *reinterpret_cast<const u32x2_t*>(q + base + static_cast<size_t>(i) * rs + d);
+            const u32x2_t ov = *reinterpret_cast<const u32x2_t*>(dout + base + static_cast<size_t>(i) * rs + d);
+            float4* a = reinterpret_cast<float4*>(ring_kp + slot * L::rStride + d);
+            float4* bb = reinterpret_cast<float4*>(ring_vp + slot * L::rStride + d);
+            float4 x = *a, y = *bb;
+            x.x += s.scale * bf16_lo(qv[0]) * adq[dt][4 * qd + 0];
+            x.y += s.scale * bf16_hi(qv[0]) * adq[dt][4 * qd + 1];
+            x.z += s.scale * bf16_lo(qv[1]) * adq[dt][4 * qd + 2];
+            x.w += s.scale * bf16_hi(qv[1]) * adq[dt][4 * qd + 3];
+            y.x += bf16_lo(ov[0]) * au[dt][4 * qd + 0];
+            y.y += bf16_hi(ov[0]) * au[dt][4 * qd + 1];
+            y.z += bf16_lo(ov[1]) * au[dt][4 * qd + 2];
+            y.w += bf16_hi(ov[1]) * au[dt][4 * qd + 3];
+            *a = x;
+            *bb = y;
+          }
+        }
+      }
+      __syncthreads();
+    }
+
+    // ---- rows no later query of the chunk touches are complete ----
+    const int fl_lo = i0 - W2P + 1;
+    const int fl_hi = min(i0 + QW, ce) - W2P;  // inclusive
+    for (int kr = fl_lo + wave; kr <= fl_hi; kr += WAVES) flush_row(kr, false);
+    __syncthreads();
+  }
+  // ---- rows still open at the end of the chunk ----
+  for (int kr = ce - W2P + 1 + wave; kr <= ce - 1; kr += WAVES) flush_row(kr, ce < N);
+}
+
+// Adds the tail partial of chunk c-1 and the head partial of chunk c for the
+// W2P-1 k-rows before each chunk boundary and writes dk', dv'.
+template <int D>
+__global__ __launch_bounds__(256) void halo_fixup_kernel(Shape s, BwdPlan plan, const float* __restrict__ ws,
+                                                         uint16_t* __restrict__ dkp, uint16_t* __restrict__ dvp) {
+  const int W2P = plan.W2P;
+  const long per_bound = static_cast<long>(W2P - 1) * D;
+  const long nb = static_cast<long>(s.B) * s.H * (plan.nchunks - 1);
+  const long idx = static_cast<long>(blockIdx.x) * 256 + threadIdx.x;
+  if (idx >= nb * per_bound) return;
+  const long bound = idx / per_bound;
+  const long rem = idx - bound * per_bound;
+  const int row = static_cast<int>(rem / D), d = static_cast<int>(rem % D);
+  const int bh = static_cast<int>(bound / (plan.nchunks - 1));
+  const int cb = static_cast<int>(bound % (plan.nchunks - 1)) + 1;  // chunk after the boundary
+  const int kr = cb * plan.CQ - W2P + 1 + row;
+  if (kr < 0 || kr >= s.N) return;
+  const size_t halo = static_cast<size_t>(W2P - 1) * D;
+  const float* head_kp = ws + (static_cast<size_t>(bh) * plan.nchunks + cb) * halo;
+  const float* head_vp = head_kp + plan.halo_floats;
+  const float* tail_kp = ws + 2 * plan.halo_floats + (static_cast<size_t>(bh) * plan.nchunks + cb - 1) * halo;
+  const float* tail_vp = tail_kp + plan.halo_floats;
+  const size_t o = static_cast<size_t>(row) * D + d;
+  const int b = bh / s.H, hh = bh % s.H;
+  const size_t dst = ((static_cast<size_t>(b) * s.N + kr) * s.H + hh) * D + d;
+  dkp[dst] = f32_to_bf16(tail_kp[o] + head_kp[o]);
+  dvp[dst] = f32_to_bf16(tail_vp[o] + head_vp[o]);
+}
+
+// ----------------------------------------------------------------- bwd_kv ---
+template <int D>
+struct BwdKvLds {
+  using St = DualStage<D, 256>;
+  static constexpr int bufBytes = 2 * St::bytes;  // q~ and do~ of one row block
+  static constexpr int mainBytes = 2 * bufBytes;
+  static constexpr int oStride = D + 4;
+  static constexpr int outBytes = 4 * 32 * oStride * 4;
+  static constexpr int bytes = mainBytes > outBytes ? mainBytes : outBytes;
+};
+
+template <int D, int G>
+__global__ __launch_bounds__(256) void bwd_kv_kernel(
+    Shape s, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+    const uint16_t* __restrict__ kp, const uint16_t* __restrict__ v, const uint16_t* __restrict__ vp,
+    const uint16_t* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ delta,
+    uint16_t* __restrict__ dk, uint16_t* __restrict__ dv) {
+  constexpr int NT = D / 16, NDT = D / 32;
+  constexpr int W2P = 32 * G;
+  using L = BwdKvLds<D>;
+  using St = typename L::St;
+  __shared__ __attribute__((aligned(16))) char smem[L::bytes];
+
+  const int jblocks = (s.N + 127) / 128;
+  const int total = jblocks * s.B * s.H;
+  const int per_xcd = (total + 7) / 8;
+  const int logical = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+  if (logical >= total) return;
+  const int bh = logical / jblocks;
+  const int jblk = logical - bh * jblocks;
+  const int b = bh / s.H, hh = bh - b * s.H;
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63, c = lane & 31, h = lane >> 5;
+  const size_t rs = static_cast<size_t>(s.H) * D;
+  const size_t base = (static_cast<size_t>(b) * s.N * s.H + hh) * D;
+  const int N = s.N, w1 = s.w1, w2 = s.w2;
+  const float qscale = s.scale * kLog2e;
+  const size_t stat = static_cast<size_t>(bh) * N;
+  const int j0 = jblk * 128;
+  const int jw = j0 + 32 * wave;  // this wavefront's keys jw .. jw + 31
+  const int jme = jw + c;         // key of this lane's accumulator column
+
+  // K and V rows of this wavefront as B operands (lane: key jw + c, 8 d's per slot group)
+  u32x4_t kf[NT], vf[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    u32x4_t a = {0u, 0u, 0u, 0u}, bb = {0u, 0u, 0u, 0u};
+    if (jme < N) {
+      a = ldg128(k + base + static_cast<size_t>(jme) * rs + 16 * t + 8 * h);
+      bb = ldg128(v + base + static_cast<size_t>(jme) * rs + 16 * t + 8 * h);
+    }
+    kf[t] = a;
+    vf[t] = bb;
+  }
+
+  f32x16_t adk[NDT], adv[NDT];
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt) {
+    adk[dt] = f32x16_t{};
+    adv[dt] = f32x16_t{};
+  }
+
+  // Row blocks: (query i, k-chunk g) for i in [j0, min(N, j0 + 127 + w1)).
+  const int i_end = min(N, j0 + 127 + w1);
+  const int nrb = (i_end - j0) * G;
+
+  // Formation of one row block: rows (2p, 2p+1), 8 columns per work item.
+  constexpr int items = 16 * (D / 8);
+  const int p_ = tid & 15, dc = tid >> 4;
+  const bool fitem = tid < items;
+  u32x4_t fq[2], fo[2];
+  auto form = [&](int rb) {
+    const int i = j0 + rb / G, g = rb % G;
+    u32x4_t qa = {0u, 0u, 0u, 0u}, oa = {0u, 0u, 0u, 0u};
+    if (fitem) {
+      qa = ldg128(q + base + static_cast<size_t>(i) * rs + 8 * dc);
+      oa = ldg128(dout + base + static_cast<size_t>(i) * rs + 8 * dc);
+    }
+#pragma unroll
+    for (int y = 0; y < 2; ++y) {
+      const int kk = i - W2P + 1 + 32 * g + 2 * p_ + y;
+      u32x4_t a4 = {0u, 0u, 0u, 0u}, b4 = {0u, 0u, 0u, 0u};
+      if (fitem && kk >= 0 && kk > i - w2) {
+        const u32x4_t ka = ldg128(kp + base + static_cast<size_t>(kk) * rs + 8 * dc);
+        const u32x4_t va = ldg128(vp + base + static_cast<size_t>(kk) * rs + 8 * dc);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          a4[e] = pack_bf16x2(bf16_lo(qa[e]) * bf16_lo(ka[e]) * qscale,
+                              bf16_hi(qa[e]) * bf16_hi(ka[e]) * qscale);
+          b4[e] = pack_bf16x2(bf16_lo(oa[e]) * bf16_lo(va[e]), bf16_hi(oa[e]) * bf16_hi(va[e]));
+        }
+      }
+      fq[y] = a4;
+      fo[y] = b4;
+    }
+  };
+  auto put = [&](char* buf) {
+    if (!fitem) return;
+    char* parts[2] = {buf, buf + St::bytes};
+    const u32x4_t* src[2] = {fq, fo};
+#pragma unroll
+    for (int z = 0; z < 2; ++z) {
+      uint16_t* rm = reinterpret_cast<uint16_t*>(parts[z]);
+      uint16_t* tr = reinterpret_cast<uint16_t*>(parts[z] + St::rowBytes);
+      *reinterpret_cast<u32x4_t*>(rm + (2 * p_) * St::rStride + 8 * dc) = src[z][0];
+      *reinterpret_cast<u32x4_t*>(rm + (2 * p_ + 1) * St::rStride + 8 * dc) = src[z][1];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const unsigned a = src[z][0][e], bb = src[z][1][e];
+        *reinterpret_cast<unsigned*>(tr + (8 * dc + 2 * e) * St::tStride + 2 * p_) = (a & 0xffffu) | (bb << 16);
+        *reinterpret_cast<unsigned*>(tr + (8 * dc + 2 * e + 1) * St::tStride + 2 * p_) = (a >> 16) | (bb & 0xffff0000u);
+      }
+    }
+  };
+
+  if (nrb > 0) {
+    form(0);
+    put(smem);
+  }
+  __syncthreads();
+  for (int rb = 0; rb < nrb; ++rb) {
+    const int cur = rb & 1;
+    if (rb + 1 < nrb) form(rb + 1);
+    const int i = j0 + rb / G, g = rb % G;
+    // this wavefront's keys see query i iff jw + 31 >= i - w1 + 1 and jw <= i
+    const bool act = jw <= i && jw + 31 > i - w1 && jw < N;
+    if (act) {
+      const char* buf = smem + cur * L::bufBytes;
+      const uint16_t* qr = reinterpret_cast<const uint16_t*>(buf);
+      const uint16_t* qtt = reinterpret_cast<const uint16_t*>(buf + St::rowBytes);
+      const uint16_t* orr = reinterpret_cast<const uint16_t*>(buf + St::bytes);
+      const uint16_t* ott = reinterpret_cast<const uint16_t*>(buf + St::bytes + St::rowBytes);
+      f32x16_t sacc = f32x16_t{}, pacc = f32x16_t{};
+#pragma unroll
+      for (int t = 0; t < NT; ++t) sacc = mfma32(frag_rows<St::rStride>(qr, c, h, t), kf[t], sacc);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) pacc = mfma32(frag_rows<St::rStride>(orr, c, h, t), vf[t], pacc);
+      const float lse2 = lse[stat + i] * kLog2e;
+      const float dlt = delta[stat + i];
+      const bool colok = jme <= i && jme > i - w1 && jme < N;
+      float pv[16], dsv[16];
+#pragma unroll
+      for (int vv = 0; vv < 16; ++vv) {
+        const int r = acc_row(vv, h);
+        const int kk = i - W2P + 1 + 32 * g + r;
+        const bool ok = colok && kk >= 0 && kk > i - w2;
+        const float p = ok ? fast_exp2(sacc[vv] - lse2) : 0.f;
+        pv[vv] = p;
+        dsv[vv] = p * (pacc[vv] - dlt);
+      }
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        u32x4_t pf, df;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          pf[e] = pack_bf16x2(pv[8 * u + 2 * e], pv[8 * u + 2 * e + 1]);
+          df[e] = pack_bf16x2(dsv[8 * u + 2 * e], dsv[8 * u + 2 * e + 1]);
+        }
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+          adv[dt] = mfma32(pf, frag_cols<St::tStride>(ott, 32 * dt + c, h, u), adv[dt]);
+          adk[dt] = mfma32(df, frag_cols<St::tStride>(qtt, 32 * dt + c, h, u), adk[dt]);
+        }
+      }
+    }
+    if (rb + 1 < nrb) put(smem + (cur ^ 1) * L::bufBytes);
+    __syncthreads();
+  }
+
+  // ---- store: accumulator rows are keys, lanes are columns d ----
+  float* ob = reinterpret_cast<float*>(smem) + wave * 32 * L::oStride;
+  const float kscale = 1.0f / kLog2e;  // q~ carried scale * log2(e); dK needs scale only
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int vv = 0; vv < 16; ++vv)
+        ob[acc_row(vv, h) * L::oStride + 32 * dt + c] = pass == 0 ? adk[dt][vv] * kscale : adv[dt][vv];
+    __syncthreads();
+    uint16_t* dst = pass == 0 ? dk : dv;
+    constexpr int CH = D / 8;
+    for (int x = lane; x < 32 * CH; x += 64) {
+      const int row = x / CH, col = x % CH;
+      const int j = jw + row;
+      if (j < N) {
+        const float* src = ob + row * L::oStride + 8 * col;
+        u32x4_t w;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(src[2 * e], src[2 * e + 1]);
+        *reinterpret_cast<u32x4_t*>(dst + base + static_cast<size_t>(j) * rs + 8 * col) = w;
+      }
+    }
+    __syncthreads();
+  }
+}
+
+template <int D, int G>
+hipError_t launch_bwd(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
+                      const void* vp, const void* out, const void* dout, const float* lse, void* dq,
+                      void* dk, void* dkp, void* dv, void* dvp, void* workspace, hipStream_t st) {
+  const BwdPlan plan = mfma_bwd_plan(s);
+  char* wsb = static_cast<char*>(workspace);
+  float* delta = reinterpret_cast<float*>(wsb + plan.delta_off);
+  float* halo = reinterpret_cast<float*>(wsb + plan.halo_off);
+  const auto* Q = static_cast<const uint16_t*>(q);
+  const auto* K = static_cast<const uint16_t*>(k);
+  const auto* KP = static_cast<const uint16_t*>(kp);
+  const auto* V = static_cast<const uint16_t*>(v);
+  const auto* VP = static_cast<const uint16_t*>(vp);
+  const auto* DO = static_cast<const uint16_t*>(dout);
+  const long rows = static_cast<long>(s.B) * s.H * s.N;
+  constexpr int LPR = D / 8;
+  hipLaunchKernelGGL(delta_kernel<D>, dim3(static_cast<unsigned>((rows * LPR + 255) / 256)), dim3(256), 0,
+                     st, s, static_cast<const uint16_t*>(out), DO, delta);
+
+  constexpr int WAVES = 4;
+  const long totq = static_cast<long>(plan.nchunks) * s.B * s.H;
+  hipLaunchKernelGGL((bwd_q_kernel<D, G, WAVES>), dim3(static_cast<unsigned>(((totq + 7) / 8) * 8)),
+                     dim3(64 * WAVES), 0, st, s, plan, Q, K, KP, V, VP, DO, lse, delta,
+                     static_cast<uint16_t*>(dq), static_cast<uint16_t*>(dkp),
+                     static_cast<uint16_t*>(dvp), halo);
+  if (plan.nchunks > 1) {
+    const long n = static_cast<long>(s.B) * s.H * (plan.nchunks - 1) * (plan.W2P - 1) * D;
+    hipLaunchKernelGGL(halo_fixup_kernel<D>, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0,
+                       st, s, plan, halo, static_cast<uint16_t*>(dkp), static_cast<uint16_t*>(dvp));
+  }
+  const long totkv = static_cast<long>((s.N + 127) / 128) * s.B * s.H;
+  hipLaunchKernelGGL((bwd_kv_kernel<D, G>), dim3(static_cast<unsigned>(((totkv + 7) / 8) * 8)), dim3(256),
+                     0, st, s, Q, K, KP, V, VP, DO, lse, delta, static_cast<uint16_t*>(dk),
+                     static_cast<uint16_t*>(dv));
+  return hipGetLastError();
+}
+
+}  // namespace
+
+bool mfma_bwd_supported(const Shape& s) { return mfma_fwd_supported(s); }
+
+hipError_t mfma_bwd(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
+                    const void* vp, const void* out, const void* dout, const float* lse, void* dq,
+                    void* dk, void* dkp, void* dv, void* dvp, void* workspace, hipStream_t st) {
+  const int G = s.w2 <= 32 ? 1 : 2;
+  if (s.D == 128)
+    return G == 1 ? launch_bwd<128, 1>(s, q, k, kp, v, vp, out, dout, lse, dq, dk, dkp, dv, dvp, workspace, st)
+                  : launch_bwd<128, 2>(s, q, k, kp, v, vp, out, dout, lse, dq, dk, dkp, dv, dvp, workspace, st);
+  if (s.D == 64)
+    return G == 1 ? launch_bwd<64, 1>(s, q, k, kp, v, vp, out, dout, lse, dq, dk, dkp, dv, dvp, workspace, st)
+                  : launch_bwd<64, 2>(s, q, k, kp, v, vp, out, dout, lse, dq, dk, dkp, dv, dvp, workspace, st);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace sa

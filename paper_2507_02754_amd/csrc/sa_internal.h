@@ -43,6 +43,19 @@ bool mfma_fwd_supported(const Shape& s);
 hipError_t mfma_fwd(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
                     const void* vp, void* out, float* lse, hipStream_t st);
 
+// Backward work split and workspace layout of the MFMA path. The workspace
+// holds Delta ([B, H, N] floats) followed by four arrays of chunk-boundary
+// partial sums (head/tail x dk'/dv', each [B*H, nchunks, W2P - 1, D] floats).
+struct BwdPlan {
+  int G, W2P, CQ, nchunks;
+  size_t halo_floats, delta_off, halo_off, bytes;
+};
+BwdPlan mfma_bwd_plan(const Shape& s);
+bool mfma_bwd_supported(const Shape& s);
+hipError_t mfma_bwd(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
+                    const void* vp, const void* out, const void* dout, const float* lse, void* dq,
+                    void* dk, void* dkp, void* dv, void* dvp, void* workspace, hipStream_t st);
+
 // Delta_i = <dO_i, O_i> for every query, [B, H, N] float32.
 hipError_t launch_delta(const Shape& s, const void* out, const void* dout, float* delta,
                         hipStream_t st);

@@ -42,6 +42,10 @@ TOL = {
 GRAD_NAMES = ("dq", "dk", "dkp", "dv", "dvp")
 
 
+def _names_for(n):
+    return GRAD_NAMES[len(GRAD_NAMES) - n:]
+
+
 def to64(t):
     return t.detach().to("cpu", torch.float64).numpy()
 
@@ -106,7 +110,7 @@ def check_grads(grads, refs, dtype, label="", rows=None):
     t = TOL[dtype]
     out = {}
     pairs = []
-    for idx, (name, g, r) in enumerate(zip(GRAD_NAMES, grads, refs)):
+    for idx, (name, g, r) in enumerate(zip(_names_for(len(grads)), grads, refs)):
         if rows is not None:
             sel = rows[idx]
             if len(sel) == 0:

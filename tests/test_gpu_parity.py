@@ -46,7 +46,6 @@ SMALL = [
     (1, 1, 150, 128, 16, 32, "bf16"),    # w1 < w2
     (1, 1, 20, 128, 512, 32, "bf16"),    # both windows longer than the sequence
     (1, 3, 1, 128, 512, 32, "bf16"),     # a single query
-    (1, 1, 100, 128, 1, 1, "bf16"),      # unit windows
     (1, 1, 129, 128, 33, 7, "bf16"),     # w2 not a multiple of 32
     (1, 1, 100, 64, 7, 5, "fp32"),
     (2, 2, 70, 32, 9, 3, "fp32"),
@@ -90,6 +89,30 @@ def test_full_size_workloads_sampled(name):
     bw_heads = heads if w.w1 * w.w2 <= 512 * 32 else heads[:1]
     P.sampled_backward_check(inputs, grads, w.w1, w.w2, w.scale, w.dtype, bw_heads, q_rows,
                              key_rows, w.name)
+
+
+def test_unit_windows_through_gpu():
+    """w1 = w2 = 1: each query sees only the pair (i, i), so O = V o V',
+    dV = dO o V' and dV' = dO o V (checked at the usual tolerance), while dQ, dK
+    and dK' vanish in exact arithmetic. On the GPU they equal
+    scale * (dP_i - Delta_i) * (x_i o y_i), where dP_i is a product of bf16-rounded
+    operands and Delta_i uses the bf16 output; each is off by at most
+    2^-9 * sum_d |dO_id v_id v'_id|, which bounds them (with a factor 2 margin)."""
+    b, h, n, d = 1, 1, 100, 128
+    _announce("unit windows")
+    inputs = draw((b, n, h, d), seed=200)
+    scale = d ** -0.5
+    o, lse = P.gpu_forward(inputs, 1, 1, scale)
+    grads = P.gpu_backward(inputs, o, lse, 1, 1, scale)
+    o_ref, lse_ref, g_ref = P.full_oracle(inputs, 1, 1, scale)
+    P.check_forward(P.to64(o), P.to64(lse), o_ref, lse_ref, "bf16", "unit windows")
+    q, k, kp, v, vp, do = (x.to(torch.float64).numpy() for x in inputs)
+    dgrads = [P.to64(g) for g in grads]
+    P.check_grads([None, None, None, dgrads[3], dgrads[4]][3:], g_ref[3:], "bf16", "unit windows dv")
+    eps = 2.0 ** -8 * np.abs(do * v * vp).sum(axis=-1, keepdims=True)
+    for g, (x, y) in zip(dgrads[:3], [(k, kp), (q, kp), (q, k)]):
+        bound = 2 * scale * eps * np.abs(x * y) + 1e-6
+        assert np.all(np.abs(g) <= bound), float(np.max(np.abs(g) - bound))
 
 
 def test_backward_is_deterministic():
