@@ -1,0 +1,232 @@
+"""Benchmark of the MI355X 2-simplicial attention hot path (one GPU).
+
+One step = the whole hot path over one batch of synthetic input already
+resident in HBM: the forward (O, LSE) and the full backward (Delta, the
+query-side kernel for dQ/dK'/dV', the key-side kernel for dK/dV).
+
+Workload (default): B=1, H=16, N=32768, D=128, w1=512, w2=32, bf16, Q and K
+rows L2-normalised and scaled by sqrt(D), seed 4 -- the long-context training
+shape the headline metric is quoted on.
+
+FLOP convention: forward 4*B*H*N*w1*w2*D, backward 12*B*H*N*w1*w2*D (the six
+window contractions S, dP, dV, dK, dQ~, U~, counting the S recompute once);
+the masked start of the sequence is not discounted.
+
+Prints one JSON line. Multi-GPU runs are not part of this build: the path runs
+on one GPU (sharding would split (batch, head) pairs or the sequence with a
+w1-row halo exchange), so --gpus other than 1 exits with a message.
+"""
+
+import argparse
+import hashlib
+import glob
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6  # MI355X dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 FLOP/clk
+METRIC = "2-simplicial attn fwd/bwd TFLOP/s and % bf16 MFMA peak at N=32k, w1=512, w2=32"
+
+
+def source_hash():
+    files = sorted(glob.glob(os.path.join(ROOT, "paper_2507_02754_amd", "csrc", "*")))
+    h = hashlib.sha256()
+    for f in files:
+        with open(f, "rb") as fh:
+            h.update(os.path.basename(f).encode())
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(kernel, workload):
+    """Per-launch HBM bytes of `kernel` from the committed counter summary, or None
+    if there is none or it was taken on different kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    for line in open(path):
+        if ":" in line:
+            key, val = line.split(":", 1)
+            vals[key.strip()] = val.strip()
+    if vals.get("source_sha256") != source_hash():
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(w, inputs, target_s):
+    """The CPU oracle, as it is, on a bounded sample of the same workload: head
+    (0, 0), consecutive queries from the middle of the sequence (full windows),
+    forward + backward, until about `target_s` seconds have elapsed."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    import oracle as orc
+
+    start = w.N // 2
+    lo = start - (w.w1 - 1)
+    arrs = [x[0, lo:, 0, :].to("cpu").double().numpy() for x in inputs]
+    q0 = w.w1 - 1
+    done = 0
+    chunk = 64
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < target_s and q0 + done + chunk <= arrs[0].shape[0]:
+        qs = range(q0 + done, q0 + done + chunk)
+        orc.forward(*arrs[:5], w.w1, w.w2, w.scale, queries=qs)
+        orc.backward(*arrs, w.w1, w.w2, w.scale, queries=qs)
+        done += chunk
+    el = time.perf_counter() - t0
+    flops = 16.0 * done * w.w1 * w.w2 * w.D
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {
+        "value": flops / el / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+        "sample": f"fwd+bwd of {done} queries (head 0, queries {start}..{start + done - 1}) "
+                  f"of {w.name}; {el:.1f} s; nominal 16*w1*w2*D FLOPs per query",
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="long_bf16_n32k")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="run one 1 GiB device-to-device copy first (HBM counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build runs the hot path on one GPU only; multi-GPU sharding "
+              "(over (batch, head) or the sequence with a w1-row halo) is not built. "
+              "Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2507_02754_amd import (load_library, simplicial_attn_bwd_key_side,
+                                      simplicial_attn_bwd_preprocess, simplicial_attn_bwd_query_side,
+                                      simplicial_attn_bwd_workspace_size, simplicial_attn_fwd,
+                                      simplicial_attn_path_name)
+    from paper_2507_02754_amd.workloads import WORKLOADS, make_inputs
+
+    load_library()
+    w = WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    print(f"[bench] {w.name} B={w.B} H={w.H} N={w.N} D={w.D} w1={w.w1} w2={w.w2} "
+          f"fwd={simplicial_attn_path_name(0, w.B, w.N, w.H, w.D, w.w1, w.w2, w.torch_dtype)} "
+          f"bwd={simplicial_attn_path_name(1, w.B, w.N, w.H, w.D, w.w1, w.w2, w.torch_dtype)}",
+          file=sys.stderr, flush=True)
+    inputs_cpu = make_inputs(w)
+    q, k, kp, v, vp, do = (x.to(dev) for x in inputs_cpu)
+    out = torch.empty_like(q)
+    lse = torch.empty((w.B, w.H, w.N), dtype=torch.float32, device=dev)
+    dq, dk, dkp, dv, dvp = (torch.empty_like(q) for _ in range(5))
+    ws = torch.empty(simplicial_attn_bwd_workspace_size(w.B, w.N, w.H, w.D, w.w1, w.w2, w.torch_dtype),
+                     dtype=torch.uint8, device=dev)
+    if args.calibrate_copy:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    phases = ["fwd", "bwd_preprocess", "bwd_query_side", "bwd_key_side"]
+
+    def step(ev=None):
+        if ev:
+            ev[0].record()
+        simplicial_attn_fwd(q, k, kp, v, vp, w.w1, w.w2, w.scale, out=out, lse=lse)
+        if ev:
+            ev[1].record()
+        simplicial_attn_bwd_preprocess(out, do, w.w1, w.w2, ws)
+        if ev:
+            ev[2].record()
+        simplicial_attn_bwd_query_side(q, k, kp, v, vp, do, lse, w.w1, w.w2, ws, w.scale,
+                                       grads=(dq, dkp, dvp))
+        if ev:
+            ev[3].record()
+        simplicial_attn_bwd_key_side(q, k, kp, v, vp, do, lse, w.w1, w.w2, ws, w.scale,
+                                     grads=(dk, dv))
+        if ev:
+            ev[4].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    start.record()
+    for i in range(args.steps):
+        step(evs[i])
+    end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = start.elapsed_time(end)
+    ms = {p: sum(e[j].elapsed_time(e[j + 1]) for e in evs) / args.steps for j, p in enumerate(phases)}
+    ms_step = total_ms / args.steps
+
+    unit = float(w.B) * w.H * w.N * w.w1 * w.w2 * w.D
+    fwd_flops, bwd_flops = 4 * unit, 12 * unit
+    bwd_ms = ms["bwd_preprocess"] + ms["bwd_query_side"] + ms["bwd_key_side"]
+    value = (fwd_flops + bwd_flops) / (ms_step * 1e-3) / 1e12
+    fwd_tf = fwd_flops / (ms["fwd"] * 1e-3) / 1e12
+    bwd_tf = bwd_flops / (bwd_ms * 1e-3) / 1e12
+
+    # Roofline of the dominant kernel: algorithmic FLOPs per launch / its time.
+    algo = {
+        "fwd": ("fwd_mfma_kernel", 4 * unit),
+        "bwd_query_side": ("bwd_q_kernel", 8 * unit),   # S recompute, dP, dQ~, U~
+        "bwd_key_side": ("bwd_kv_kernel", 4 * unit),    # dV, dK (its S/dP recompute is not counted)
+    }
+    dom = max(algo, key=lambda p: ms[p])
+    kname, kflops = algo[dom]
+    achieved = kflops / (ms[dom] * 1e-3) / 1e12
+    roofline = {"bound": "mfma", "kernel": kname, "achieved": round(achieved, 2),
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                "traffic": read_traffic(kname, w.name)}
+
+    result = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "H": w.H, "N": w.N, "D": w.D, "w1": w.w1,
+                   "w2": w.w2, "seed": w.seed, "inputs": w.note},
+        "fwd_ms": round(ms["fwd"], 4),
+        "bwd_ms": round(bwd_ms, 4),
+        "fwd_tflops": round(fwd_tf, 2),
+        "bwd_tflops": round(bwd_tf, 2),
+        "fwd_pct_peak": round(100 * fwd_tf / PEAK_BF16_TFLOPS, 2),
+        "bwd_pct_peak": round(100 * bwd_tf / PEAK_BF16_TFLOPS, 2),
+        "phase_ms": {p: round(ms[p], 4) for p in phases},
+        "wall_s_timed": round(wall, 3),
+        "roofline": roofline,
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline(w, inputs_cpu, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -94,6 +94,32 @@ int simplicial_attn_bwd(const void* q, const void* k, const void* kp, const void
                         int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1, int32_t w2,
                         float scale, int32_t dtype, void* stream);
 
+/*
+ * The backward in three stages, for callers that schedule them themselves.
+ * simplicial_attn_bwd is exactly preprocess, then query side, then key side
+ * on one stream. Both sides read what preprocess wrote into `workspace` (the
+ * per-query Delta); once it has run they are independent of each other.
+ *   preprocess  Delta_i = <dO_i, O_i> into the workspace.
+ *   query side  dQ, dK', dV' (the query-stationary kernel, Section 7's second
+ *               kernel, with the k-halo reduction of Algorithm 2's role).
+ *   key side    dK, dV (the key-stationary kernel, Section 7's first kernel).
+ * Arguments mean what they mean for simplicial_attn_bwd; the same workspace
+ * (same size rule) must be passed to all three.
+ */
+int simplicial_attn_bwd_preprocess(const void* out, const void* dout, void* workspace,
+                                   size_t workspace_bytes, int64_t B, int64_t N, int64_t H,
+                                   int64_t D, int32_t w1, int32_t w2, int32_t dtype, void* stream);
+int simplicial_attn_bwd_query_side(const void* q, const void* k, const void* kp, const void* v,
+                                   const void* vp, const void* dout, const float* lse, void* dq,
+                                   void* dkp, void* dvp, void* workspace, size_t workspace_bytes,
+                                   int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1,
+                                   int32_t w2, float scale, int32_t dtype, void* stream);
+int simplicial_attn_bwd_key_side(const void* q, const void* k, const void* kp, const void* v,
+                                 const void* vp, const void* dout, const float* lse, void* dk,
+                                 void* dv, void* workspace, size_t workspace_bytes, int64_t B,
+                                 int64_t N, int64_t H, int64_t D, int32_t w1, int32_t w2,
+                                 float scale, int32_t dtype, void* stream);
+
 /* Static, NUL-terminated description of a status code ("unknown status" otherwise). */
 const char* simplicial_attn_error_string(int code);
 

@@ -18,6 +18,9 @@ __all__ = [
     "load_library",
     "simplicial_attn_fwd",
     "simplicial_attn_bwd",
+    "simplicial_attn_bwd_preprocess",
+    "simplicial_attn_bwd_query_side",
+    "simplicial_attn_bwd_key_side",
     "simplicial_attn_bwd_workspace_size",
     "simplicial_attn_error_string",
     "simplicial_attn_abi_version",
@@ -55,6 +58,12 @@ def load_library():
     lib.simplicial_attn_fwd.restype = ctypes.c_int
     lib.simplicial_attn_bwd.argtypes = [vp] * 14 + [ctypes.c_size_t] + [i64] * 4 + [i32, i32, f32, i32, vp]
     lib.simplicial_attn_bwd.restype = ctypes.c_int
+    lib.simplicial_attn_bwd_preprocess.argtypes = [vp] * 3 + [ctypes.c_size_t] + [i64] * 4 + [i32, i32, i32, vp]
+    lib.simplicial_attn_bwd_preprocess.restype = ctypes.c_int
+    lib.simplicial_attn_bwd_query_side.argtypes = [vp] * 11 + [ctypes.c_size_t] + [i64] * 4 + [i32, i32, f32, i32, vp]
+    lib.simplicial_attn_bwd_query_side.restype = ctypes.c_int
+    lib.simplicial_attn_bwd_key_side.argtypes = [vp] * 10 + [ctypes.c_size_t] + [i64] * 4 + [i32, i32, f32, i32, vp]
+    lib.simplicial_attn_bwd_key_side.restype = ctypes.c_int
     lib.simplicial_attn_bwd_workspace_size.argtypes = [i64] * 4 + [i32, i32, i32]
     lib.simplicial_attn_bwd_workspace_size.restype = ctypes.c_size_t
     lib.simplicial_attn_error_string.argtypes = [ctypes.c_int]
@@ -139,6 +148,65 @@ def simplicial_attn_fwd(q, k, kp, v, vp, w1, w2, scale=None, out=None, lse=None)
     return out, lse
 
 
+def _bwd_common(q, k, kp, v, vp, dout, lse, w1, w2, extra=(), extra_names=()):
+    (B, N, H, D), dt = _check_inputs((q, k, kp, v, vp, dout, *extra),
+                                     ("q", "k", "kp", "v", "vp", "dout", *extra_names))
+    if lse.shape != (B, H, N) or lse.dtype != torch.float32 or not lse.is_contiguous() \
+            or lse.device != q.device:
+        raise ValueError("lse must be a contiguous float32 [B, H, N] tensor on the inputs' device")
+    return (B, N, H, D), dt
+
+
+def _workspace(workspace, B, N, H, D, w1, w2, dt, device):
+    ws = simplicial_attn_bwd_workspace_size(B, N, H, D, w1, w2, dt)
+    if workspace is None:
+        workspace = torch.empty(max(ws, 16), dtype=torch.uint8, device=device)
+    return workspace
+
+
+def simplicial_attn_bwd_preprocess(out, dout, w1, w2, workspace):
+    """Delta_i = <dO_i, O_i> into `workspace` (a uint8 GPU tensor of the backward's size)."""
+    (B, N, H, D), dt = _check_inputs((out, dout), ("out", "dout"))
+    rc = load_library().simplicial_attn_bwd_preprocess(
+        _ptr(out), _ptr(dout), _ptr(workspace), ctypes.c_size_t(workspace.numel()),
+        B, N, H, D, int(w1), int(w2), dt, _stream(out.device))
+    if rc != 0:
+        raise SimplicialAttnError(rc, "simplicial_attn_bwd_preprocess")
+    return workspace
+
+
+def simplicial_attn_bwd_query_side(q, k, kp, v, vp, dout, lse, w1, w2, workspace, scale=None,
+                                   grads=None):
+    """(dQ, dK', dV') after simplicial_attn_bwd_preprocess filled `workspace`."""
+    (B, N, H, D), dt = _bwd_common(q, k, kp, v, vp, dout, lse, w1, w2)
+    scale = D ** -0.5 if scale is None else scale
+    grads = grads if grads is not None else tuple(torch.empty_like(q) for _ in range(3))
+    _check_inputs((q, *grads), ("q", "dq", "dkp", "dvp"))
+    rc = load_library().simplicial_attn_bwd_query_side(
+        _ptr(q), _ptr(k), _ptr(kp), _ptr(v), _ptr(vp), _ptr(dout), _ptr(lse),
+        *(_ptr(g) for g in grads), _ptr(workspace), ctypes.c_size_t(workspace.numel()),
+        B, N, H, D, int(w1), int(w2), float(scale), dt, _stream(q.device))
+    if rc != 0:
+        raise SimplicialAttnError(rc, "simplicial_attn_bwd_query_side")
+    return grads
+
+
+def simplicial_attn_bwd_key_side(q, k, kp, v, vp, dout, lse, w1, w2, workspace, scale=None,
+                                 grads=None):
+    """(dK, dV) after simplicial_attn_bwd_preprocess filled `workspace`."""
+    (B, N, H, D), dt = _bwd_common(q, k, kp, v, vp, dout, lse, w1, w2)
+    scale = D ** -0.5 if scale is None else scale
+    grads = grads if grads is not None else tuple(torch.empty_like(q) for _ in range(2))
+    _check_inputs((q, *grads), ("q", "dk", "dv"))
+    rc = load_library().simplicial_attn_bwd_key_side(
+        _ptr(q), _ptr(k), _ptr(kp), _ptr(v), _ptr(vp), _ptr(dout), _ptr(lse),
+        *(_ptr(g) for g in grads), _ptr(workspace), ctypes.c_size_t(workspace.numel()),
+        B, N, H, D, int(w1), int(w2), float(scale), dt, _stream(q.device))
+    if rc != 0:
+        raise SimplicialAttnError(rc, "simplicial_attn_bwd_key_side")
+    return grads
+
+
 def simplicial_attn_bwd(q, k, kp, v, vp, out, dout, lse, w1, w2, scale=None, grads=None,
                         workspace=None):
     """(dQ, dK, dK', dV, dV') = backward(...); `out`/`lse` come from the forward."""
@@ -153,9 +221,7 @@ def simplicial_attn_bwd(q, k, kp, v, vp, out, dout, lse, w1, w2, scale=None, gra
         grads = tuple(torch.empty_like(q) for _ in range(5))
     else:
         _check_inputs((q, *grads), ("q", "dq", "dk", "dkp", "dv", "dvp"))
-    ws = simplicial_attn_bwd_workspace_size(B, N, H, D, w1, w2, dt)
-    if workspace is None:
-        workspace = torch.empty(max(ws, 16), dtype=torch.uint8, device=q.device)
+    workspace = _workspace(workspace, B, N, H, D, w1, w2, dt, q.device)
     rc = load_library().simplicial_attn_bwd(
         _ptr(q), _ptr(k), _ptr(kp), _ptr(v), _ptr(vp), _ptr(out), _ptr(dout), _ptr(lse),
         *(_ptr(g) for g in grads), _ptr(workspace), ctypes.c_size_t(workspace.numel()),

@@ -6,22 +6,32 @@
 #include <limits.h>
 #include <math.h>
 
+#include <initializer_list>
+
 #include "sa_internal.h"
 
 namespace {
 
+using sa::BwdStage;
 using sa::Shape;
 
 enum class Path { Invalid, Generic, Mfma };
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+int check_ptrs(std::initializer_list<const void*> ptrs) {
+  for (const void* p : ptrs) {
+    if (!p || !aligned16(p)) return SA_ERR_INVALID;
+  }
+  return SA_OK;
+}
+
 // Size checks shared by every entry point. Returns SA_OK or an error code.
 int check_sizes(int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1, int32_t w2,
                 int32_t dtype) {
   if (B <= 0 || N <= 0 || H <= 0 || D <= 0 || w1 < 1 || w2 < 1) return SA_ERR_INVALID;
-  // Every grid index and per-head row count must fit in 32 bits, and byte
-  // offsets in 63 bits.
+  // Every grid index and per-head row count must fit in 32 bits, and element
+  // offsets comfortably in 64 bits.
   if (N > INT_MAX || B > INT_MAX || H > INT_MAX || D > INT_MAX) return SA_ERR_INVALID;
   const int64_t rows = B * H;
   if (rows > INT_MAX || N > INT_MAX / rows) return SA_ERR_INVALID;
@@ -55,7 +65,42 @@ Path choose_path(int which, int64_t B, int64_t N, int64_t H, int64_t D, int32_t 
   return Path::Generic;
 }
 
+size_t workspace_bytes_for(int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1, int32_t w2,
+                           int32_t dtype) {
+  if (check_sizes(B, N, H, D, w1, w2, dtype) != SA_OK) return 0;
+  if (choose_path(1, B, N, H, D, w1, w2, dtype) == Path::Mfma)
+    return sa::mfma_bwd_plan(make_shape(B, N, H, D, w1, w2, 1.0f, dtype)).bytes;
+  // Delta: one float per (b, h, query), rounded up to 256 bytes.
+  return ((static_cast<size_t>(B * H * N) * sizeof(float)) + 255) & ~size_t(255);
+}
+
 int to_status(hipError_t e) { return e == hipSuccess ? SA_OK : SA_ERR_HIP; }
+
+// Common validation of the backward entry points (pointers checked by callers).
+int check_bwd(int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1, int32_t w2, float scale,
+              int32_t dtype, size_t workspace_bytes) {
+  if (!isfinite(scale)) return SA_ERR_INVALID;
+  const int rc = check_sizes(B, N, H, D, w1, w2, dtype);
+  if (rc != SA_OK) return rc;
+  if (workspace_bytes < workspace_bytes_for(B, N, H, D, w1, w2, dtype)) return SA_ERR_WORKSPACE;
+  return SA_OK;
+}
+
+int run_delta(const Shape& s, Path path, const void* out, const void* dout, void* workspace,
+              hipStream_t st) {
+  if (path == Path::Mfma) return to_status(sa::mfma_bwd_delta(s, out, dout, workspace, st));
+  return to_status(sa::launch_delta(s, out, dout, static_cast<float*>(workspace), st));
+}
+
+int run_stage(const Shape& s, Path path, BwdStage stage, const void* q, const void* k,
+              const void* kp, const void* v, const void* vp, const void* dout, const float* lse,
+              void* g0, void* g1, void* g2, void* workspace, hipStream_t st) {
+  if (path == Path::Mfma)
+    return to_status(
+        sa::mfma_bwd_stage(s, stage, q, k, kp, v, vp, dout, lse, g0, g1, g2, workspace, st));
+  return to_status(sa::generic_bwd_stage(s, stage, q, k, kp, v, vp, dout, lse,
+                                         static_cast<const float*>(workspace), g0, g1, g2, st));
+}
 
 }  // namespace
 
@@ -87,10 +132,7 @@ const char* simplicial_attn_path_name(int32_t which, int64_t B, int64_t N, int64
 int simplicial_attn_fwd(const void* q, const void* k, const void* kp, const void* v, const void* vp,
                         void* out, float* lse, int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1,
                         int32_t w2, float scale, int32_t dtype, void* stream) {
-  if (!q || !k || !kp || !v || !vp || !out || !lse) return SA_ERR_INVALID;
-  if (!aligned16(q) || !aligned16(k) || !aligned16(kp) || !aligned16(v) || !aligned16(vp) ||
-      !aligned16(out) || !aligned16(lse))
-    return SA_ERR_INVALID;
+  if (check_ptrs({q, k, kp, v, vp, out, lse}) != SA_OK) return SA_ERR_INVALID;
   if (!isfinite(scale)) return SA_ERR_INVALID;
   const int rc = check_sizes(B, N, H, D, w1, w2, dtype);
   if (rc != SA_OK) return rc;
@@ -105,12 +147,45 @@ int simplicial_attn_fwd(const void* q, const void* k, const void* kp, const void
 
 size_t simplicial_attn_bwd_workspace_size(int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1,
                                           int32_t w2, int32_t dtype) {
-  if (check_sizes(B, N, H, D, w1, w2, dtype) != SA_OK) return 0;
-  if (choose_path(1, B, N, H, D, w1, w2, dtype) == Path::Mfma)
-    return sa::mfma_bwd_plan(make_shape(B, N, H, D, w1, w2, 1.0f, dtype)).bytes;
-  // Delta: one float per (b, h, query), rounded up to 256 bytes.
-  const size_t delta = ((static_cast<size_t>(B * H * N) * sizeof(float)) + 255) & ~size_t(255);
-  return delta;
+  return workspace_bytes_for(B, N, H, D, w1, w2, dtype);
+}
+
+int simplicial_attn_bwd_preprocess(const void* out, const void* dout, void* workspace,
+                                   size_t workspace_bytes, int64_t B, int64_t N, int64_t H,
+                                   int64_t D, int32_t w1, int32_t w2, int32_t dtype, void* stream) {
+  if (check_ptrs({out, dout, workspace}) != SA_OK) return SA_ERR_INVALID;
+  const int rc = check_bwd(B, N, H, D, w1, w2, 1.0f, dtype, workspace_bytes);
+  if (rc != SA_OK) return rc;
+  const Shape s = make_shape(B, N, H, D, w1, w2, 1.0f, dtype);
+  return run_delta(s, choose_path(1, B, N, H, D, w1, w2, dtype), out, dout, workspace,
+                   static_cast<hipStream_t>(stream));
+}
+
+int simplicial_attn_bwd_query_side(const void* q, const void* k, const void* kp, const void* v,
+                                   const void* vp, const void* dout, const float* lse, void* dq,
+                                   void* dkp, void* dvp, void* workspace, size_t workspace_bytes,
+                                   int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1,
+                                   int32_t w2, float scale, int32_t dtype, void* stream) {
+  if (check_ptrs({q, k, kp, v, vp, dout, lse, dq, dkp, dvp, workspace}) != SA_OK)
+    return SA_ERR_INVALID;
+  const int rc = check_bwd(B, N, H, D, w1, w2, scale, dtype, workspace_bytes);
+  if (rc != SA_OK) return rc;
+  const Shape s = make_shape(B, N, H, D, w1, w2, scale, dtype);
+  return run_stage(s, choose_path(1, B, N, H, D, w1, w2, dtype), BwdStage::Query, q, k, kp, v, vp,
+                   dout, lse, dq, dkp, dvp, workspace, static_cast<hipStream_t>(stream));
+}
+
+int simplicial_attn_bwd_key_side(const void* q, const void* k, const void* kp, const void* v,
+                                 const void* vp, const void* dout, const float* lse, void* dk,
+                                 void* dv, void* workspace, size_t workspace_bytes, int64_t B,
+                                 int64_t N, int64_t H, int64_t D, int32_t w1, int32_t w2,
+                                 float scale, int32_t dtype, void* stream) {
+  if (check_ptrs({q, k, kp, v, vp, dout, lse, dk, dv, workspace}) != SA_OK) return SA_ERR_INVALID;
+  const int rc = check_bwd(B, N, H, D, w1, w2, scale, dtype, workspace_bytes);
+  if (rc != SA_OK) return rc;
+  const Shape s = make_shape(B, N, H, D, w1, w2, scale, dtype);
+  return run_stage(s, choose_path(1, B, N, H, D, w1, w2, dtype), BwdStage::Key, q, k, kp, v, vp,
+                   dout, lse, dk, dv, nullptr, workspace, static_cast<hipStream_t>(stream));
 }
 
 int simplicial_attn_bwd(const void* q, const void* k, const void* kp, const void* v, const void* vp,
@@ -118,28 +193,19 @@ int simplicial_attn_bwd(const void* q, const void* k, const void* kp, const void
                         void* dkp, void* dv, void* dvp, void* workspace, size_t workspace_bytes,
                         int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1, int32_t w2,
                         float scale, int32_t dtype, void* stream) {
-  const void* ptrs[] = {q, k, kp, v, vp, out, dout, lse, dq, dk, dkp, dv, dvp, workspace};
-  for (const void* p : ptrs) {
-    if (!p) return SA_ERR_INVALID;
-    if (!aligned16(p)) return SA_ERR_INVALID;
-  }
-  if (!isfinite(scale)) return SA_ERR_INVALID;
-  const int rc = check_sizes(B, N, H, D, w1, w2, dtype);
+  if (check_ptrs({q, k, kp, v, vp, out, dout, lse, dq, dk, dkp, dv, dvp, workspace}) != SA_OK)
+    return SA_ERR_INVALID;
+  const int rc = check_bwd(B, N, H, D, w1, w2, scale, dtype, workspace_bytes);
   if (rc != SA_OK) return rc;
-  if (workspace_bytes < simplicial_attn_bwd_workspace_size(B, N, H, D, w1, w2, dtype))
-    return SA_ERR_WORKSPACE;
   const Shape s = make_shape(B, N, H, D, w1, w2, scale, dtype);
+  const Path path = choose_path(1, B, N, H, D, w1, w2, dtype);
   hipStream_t st = static_cast<hipStream_t>(stream);
-  float* delta = static_cast<float*>(workspace);
-  switch (choose_path(1, B, N, H, D, w1, w2, dtype)) {
-    case Path::Generic:
-      return to_status(sa::generic_bwd(s, q, k, kp, v, vp, out, dout, lse, dq, dk, dkp, dv, dvp,
-                                       delta, st));
-    case Path::Mfma:
-      return to_status(sa::mfma_bwd(s, q, k, kp, v, vp, out, dout, lse, dq, dk, dkp, dv, dvp,
-                                    workspace, st));
-    default: return SA_ERR_UNSUPPORTED;
-  }
+  int r = run_delta(s, path, out, dout, workspace, st);
+  if (r != SA_OK) return r;
+  r = run_stage(s, path, BwdStage::Query, q, k, kp, v, vp, dout, lse, dq, dkp, dvp, workspace, st);
+  if (r != SA_OK) return r;
+  return run_stage(s, path, BwdStage::Key, q, k, kp, v, vp, dout, lse, dk, dv, nullptr, workspace,
+                   st);
 }
 
 }  // extern "C"

@@ -640,12 +640,12 @@ __global__ __launch_bounds__(256) void bwd_kv_kernel(
 }
 
 template <int D, int G>
-hipError_t launch_bwd(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
-                      const void* vp, const void* out, const void* dout, const float* lse, void* dq,
-                      void* dk, void* dkp, void* dv, void* dvp, void* workspace, hipStream_t st) {
+hipError_t launch_stage(const Shape& s, BwdStage stage, const void* q, const void* k, const void* kp,
+                        const void* v, const void* vp, const void* dout, const float* lse, void* g0,
+                        void* g1, void* g2, void* workspace, hipStream_t st) {
   const BwdPlan plan = mfma_bwd_plan(s);
   char* wsb = static_cast<char*>(workspace);
-  float* delta = reinterpret_cast<float*>(wsb + plan.delta_off);
+  const float* delta = reinterpret_cast<const float*>(wsb + plan.delta_off);
   float* halo = reinterpret_cast<float*>(wsb + plan.halo_off);
   const auto* Q = static_cast<const uint16_t*>(q);
   const auto* K = static_cast<const uint16_t*>(k);
@@ -653,26 +653,24 @@ hipError_t launch_bwd(const Shape& s, const void* q, const void* k, const void* 
   const auto* V = static_cast<const uint16_t*>(v);
   const auto* VP = static_cast<const uint16_t*>(vp);
   const auto* DO = static_cast<const uint16_t*>(dout);
-  const long rows = static_cast<long>(s.B) * s.H * s.N;
-  constexpr int LPR = D / 8;
-  hipLaunchKernelGGL(delta_kernel<D>, dim3(static_cast<unsigned>((rows * LPR + 255) / 256)), dim3(256), 0,
-                     st, s, static_cast<const uint16_t*>(out), DO, delta);
-
-  constexpr int WAVES = 4;
-  const long totq = static_cast<long>(plan.nchunks) * s.B * s.H;
-  hipLaunchKernelGGL((bwd_q_kernel<D, G, WAVES>), dim3(static_cast<unsigned>(((totq + 7) / 8) * 8)),
-                     dim3(64 * WAVES), 0, st, s, plan, Q, K, KP, V, VP, DO, lse, delta,
-                     static_cast<uint16_t*>(dq), static_cast<uint16_t*>(dkp),
-                     static_cast<uint16_t*>(dvp), halo);
-  if (plan.nchunks > 1) {
-    const long n = static_cast<long>(s.B) * s.H * (plan.nchunks - 1) * (plan.W2P - 1) * D;
-    hipLaunchKernelGGL(halo_fixup_kernel<D>, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0,
-                       st, s, plan, halo, static_cast<uint16_t*>(dkp), static_cast<uint16_t*>(dvp));
+  if (stage == BwdStage::Query) {
+    constexpr int WAVES = 4;
+    const long totq = static_cast<long>(plan.nchunks) * s.B * s.H;
+    hipLaunchKernelGGL((bwd_q_kernel<D, G, WAVES>), dim3(static_cast<unsigned>(((totq + 7) / 8) * 8)),
+                       dim3(64 * WAVES), 0, st, s, plan, Q, K, KP, V, VP, DO, lse, delta,
+                       static_cast<uint16_t*>(g0), static_cast<uint16_t*>(g1),
+                       static_cast<uint16_t*>(g2), halo);
+    if (plan.nchunks > 1) {
+      const long n = static_cast<long>(s.B) * s.H * (plan.nchunks - 1) * (plan.W2P - 1) * D;
+      hipLaunchKernelGGL(halo_fixup_kernel<D>, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256),
+                         0, st, s, plan, halo, static_cast<uint16_t*>(g1), static_cast<uint16_t*>(g2));
+    }
+  } else {
+    const long totkv = static_cast<long>((s.N + 127) / 128) * s.B * s.H;
+    hipLaunchKernelGGL((bwd_kv_kernel<D, G>), dim3(static_cast<unsigned>(((totkv + 7) / 8) * 8)),
+                       dim3(256), 0, st, s, Q, K, KP, V, VP, DO, lse, delta,
+                       static_cast<uint16_t*>(g0), static_cast<uint16_t*>(g1));
   }
-  const long totkv = static_cast<long>((s.N + 127) / 128) * s.B * s.H;
-  hipLaunchKernelGGL((bwd_kv_kernel<D, G>), dim3(static_cast<unsigned>(((totkv + 7) / 8) * 8)), dim3(256),
-                     0, st, s, Q, K, KP, V, VP, DO, lse, delta, static_cast<uint16_t*>(dk),
-                     static_cast<uint16_t*>(dv));
   return hipGetLastError();
 }
 
@@ -680,16 +678,36 @@ hipError_t launch_bwd(const Shape& s, const void* q, const void* k, const void* 
 
 bool mfma_bwd_supported(const Shape& s) { return mfma_fwd_supported(s); }
 
-hipError_t mfma_bwd(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
-                    const void* vp, const void* out, const void* dout, const float* lse, void* dq,
-                    void* dk, void* dkp, void* dv, void* dvp, void* workspace, hipStream_t st) {
+hipError_t mfma_bwd_delta(const Shape& s, const void* out, const void* dout, void* workspace,
+                          hipStream_t st) {
+  const BwdPlan plan = mfma_bwd_plan(s);
+  float* delta = reinterpret_cast<float*>(static_cast<char*>(workspace) + plan.delta_off);
+  const long rows = static_cast<long>(s.B) * s.H * s.N;
+  const auto* O = static_cast<const uint16_t*>(out);
+  const auto* DO = static_cast<const uint16_t*>(dout);
+  if (s.D == 128) {
+    hipLaunchKernelGGL(delta_kernel<128>, dim3(static_cast<unsigned>((rows * 16 + 255) / 256)),
+                       dim3(256), 0, st, s, O, DO, delta);
+  } else if (s.D == 64) {
+    hipLaunchKernelGGL(delta_kernel<64>, dim3(static_cast<unsigned>((rows * 8 + 255) / 256)),
+                       dim3(256), 0, st, s, O, DO, delta);
+  } else {
+    return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t mfma_bwd_stage(const Shape& s, BwdStage stage, const void* q, const void* k,
+                          const void* kp, const void* v, const void* vp, const void* dout,
+                          const float* lse, void* g0, void* g1, void* g2, void* workspace,
+                          hipStream_t st) {
   const int G = s.w2 <= 32 ? 1 : 2;
   if (s.D == 128)
-    return G == 1 ? launch_bwd<128, 1>(s, q, k, kp, v, vp, out, dout, lse, dq, dk, dkp, dv, dvp, workspace, st)
-                  : launch_bwd<128, 2>(s, q, k, kp, v, vp, out, dout, lse, dq, dk, dkp, dv, dvp, workspace, st);
+    return G == 1 ? launch_stage<128, 1>(s, stage, q, k, kp, v, vp, dout, lse, g0, g1, g2, workspace, st)
+                  : launch_stage<128, 2>(s, stage, q, k, kp, v, vp, dout, lse, g0, g1, g2, workspace, st);
   if (s.D == 64)
-    return G == 1 ? launch_bwd<64, 1>(s, q, k, kp, v, vp, out, dout, lse, dq, dk, dkp, dv, dvp, workspace, st)
-                  : launch_bwd<64, 2>(s, q, k, kp, v, vp, out, dout, lse, dq, dk, dkp, dv, dvp, workspace, st);
+    return G == 1 ? launch_stage<64, 1>(s, stage, q, k, kp, v, vp, dout, lse, g0, g1, g2, workspace, st)
+                  : launch_stage<64, 2>(s, stage, q, k, kp, v, vp, dout, lse, g0, g1, g2, workspace, st);
   return hipErrorInvalidValue;
 }
 

@@ -292,9 +292,9 @@ hipError_t fwd_t(const Shape& s, const void* q, const void* k, const void* kp, c
 }
 
 template <typename T, int D>
-hipError_t bwd_t(const Shape& s, const void* q_, const void* k_, const void* kp_, const void* v_,
-                 const void* vp_, const void* dout_, const float* lse, const float* delta,
-                 void* dq, void* dk, void* dkp, void* dv, void* dvp, hipStream_t st) {
+hipError_t bwd_stage_t(const Shape& s, BwdStage stage, const void* q_, const void* k_, const void* kp_,
+                       const void* v_, const void* vp_, const void* dout_, const float* lse,
+                       const float* delta, void* g0, void* g1, void* g2, hipStream_t st) {
   const T* q = static_cast<const T*>(q_);
   const T* k = static_cast<const T*>(k_);
   const T* kp = static_cast<const T*>(kp_);
@@ -302,16 +302,19 @@ hipError_t bwd_t(const Shape& s, const void* q_, const void* k_, const void* kp_
   const T* vp = static_cast<const T*>(vp_);
   const T* dout = static_cast<const T*>(dout_);
   const unsigned grid = static_cast<unsigned>(s.N) * s.B * s.H;
-  hipLaunchKernelGGL((dq_kernel<T, D>), dim3(grid), dim3(kThreads), 0, st, s, q, k, kp, v, vp,
-                     dout, lse, delta, static_cast<T*>(dq));
-  hipLaunchKernelGGL((keyside_kernel<T, D, 0, 0>), dim3(grid), dim3(kThreads), 0, st, s, q, k, kp,
-                     v, vp, dout, lse, delta, static_cast<T*>(dk));
-  hipLaunchKernelGGL((keyside_kernel<T, D, 0, 1>), dim3(grid), dim3(kThreads), 0, st, s, q, k, kp,
-                     v, vp, dout, lse, delta, static_cast<T*>(dv));
-  hipLaunchKernelGGL((keyside_kernel<T, D, 1, 0>), dim3(grid), dim3(kThreads), 0, st, s, q, kp, k,
-                     vp, v, dout, lse, delta, static_cast<T*>(dkp));
-  hipLaunchKernelGGL((keyside_kernel<T, D, 1, 1>), dim3(grid), dim3(kThreads), 0, st, s, q, kp, k,
-                     vp, v, dout, lse, delta, static_cast<T*>(dvp));
+  if (stage == BwdStage::Query) {
+    hipLaunchKernelGGL((dq_kernel<T, D>), dim3(grid), dim3(kThreads), 0, st, s, q, k, kp, v, vp,
+                       dout, lse, delta, static_cast<T*>(g0));
+    hipLaunchKernelGGL((keyside_kernel<T, D, 1, 0>), dim3(grid), dim3(kThreads), 0, st, s, q, kp, k,
+                       vp, v, dout, lse, delta, static_cast<T*>(g1));
+    hipLaunchKernelGGL((keyside_kernel<T, D, 1, 1>), dim3(grid), dim3(kThreads), 0, st, s, q, kp, k,
+                       vp, v, dout, lse, delta, static_cast<T*>(g2));
+  } else {
+    hipLaunchKernelGGL((keyside_kernel<T, D, 0, 0>), dim3(grid), dim3(kThreads), 0, st, s, q, k, kp,
+                       v, vp, dout, lse, delta, static_cast<T*>(g0));
+    hipLaunchKernelGGL((keyside_kernel<T, D, 0, 1>), dim3(grid), dim3(kThreads), 0, st, s, q, k, kp,
+                       v, vp, dout, lse, delta, static_cast<T*>(g1));
+  }
   return hipGetLastError();
 }
 
@@ -349,15 +352,14 @@ hipError_t launch_delta(const Shape& s, const void* out, const void* dout, float
   return hipGetLastError();
 }
 
-hipError_t generic_bwd(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
-                       const void* vp, const void* out, const void* dout, const float* lse, void* dq,
-                       void* dk, void* dkp, void* dv, void* dvp, float* delta, hipStream_t st) {
-  hipError_t e = launch_delta(s, out, dout, delta, st);
-  if (e != hipSuccess) return e;
+hipError_t generic_bwd_stage(const Shape& s, BwdStage stage, const void* q, const void* k,
+                             const void* kp, const void* v, const void* vp, const void* dout,
+                             const float* lse, const float* delta, void* g0, void* g1, void* g2,
+                             hipStream_t st) {
   if (s.dtype == 0) {
-    SA_DISPATCH_D(float, bwd_t, s, q, k, kp, v, vp, dout, lse, delta, dq, dk, dkp, dv, dvp, st);
+    SA_DISPATCH_D(float, bwd_stage_t, s, stage, q, k, kp, v, vp, dout, lse, delta, g0, g1, g2, st);
   }
-  SA_DISPATCH_D(uint16_t, bwd_t, s, q, k, kp, v, vp, dout, lse, delta, dq, dk, dkp, dv, dvp, st);
+  SA_DISPATCH_D(uint16_t, bwd_stage_t, s, stage, q, k, kp, v, vp, dout, lse, delta, g0, g1, g2, st);
 }
 
 }  // namespace sa

@@ -34,9 +34,13 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
 // ---- generic path (any supported dtype / head_dim / windows) --------------
 hipError_t generic_fwd(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
                        const void* vp, void* out, float* lse, hipStream_t st);
-hipError_t generic_bwd(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
-                       const void* vp, const void* out, const void* dout, const float* lse, void* dq,
-                       void* dk, void* dkp, void* dv, void* dvp, float* delta, hipStream_t st);
+// The backward is split into a query-side stage (dQ, dK', dV') and a key-side
+// stage (dK, dV); both read Delta, which the preprocessing stage writes.
+enum class BwdStage { Query, Key };
+hipError_t generic_bwd_stage(const Shape& s, BwdStage stage, const void* q, const void* k,
+                             const void* kp, const void* v, const void* vp, const void* dout,
+                             const float* lse, const float* delta, void* g0, void* g1, void* g2,
+                             hipStream_t st);
 
 // ---- gfx950 MFMA path (bf16, head_dim 64/128, w2 <= 64) --------------------
 bool mfma_fwd_supported(const Shape& s);
@@ -52,9 +56,13 @@ struct BwdPlan {
 };
 BwdPlan mfma_bwd_plan(const Shape& s);
 bool mfma_bwd_supported(const Shape& s);
-hipError_t mfma_bwd(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
-                    const void* vp, const void* out, const void* dout, const float* lse, void* dq,
-                    void* dk, void* dkp, void* dv, void* dvp, void* workspace, hipStream_t st);
+hipError_t mfma_bwd_delta(const Shape& s, const void* out, const void* dout, void* workspace,
+                          hipStream_t st);
+// Query side: g0 = dq, g1 = dk', g2 = dv'. Key side: g0 = dk, g1 = dv.
+hipError_t mfma_bwd_stage(const Shape& s, BwdStage stage, const void* q, const void* k,
+                          const void* kp, const void* v, const void* vp, const void* dout,
+                          const float* lse, void* g0, void* g1, void* g2, void* workspace,
+                          hipStream_t st);
 
 // Delta_i = <dO_i, O_i> for every query, [B, H, N] float32.
 hipError_t launch_delta(const Shape& s, const void* out, const void* dout, float* delta,

@@ -47,6 +47,8 @@ def test_header_declares_the_expected_entry_points():
     assert declared_functions() == sorted([
         "simplicial_attn_fwd", "simplicial_attn_bwd", "simplicial_attn_bwd_workspace_size",
         "simplicial_attn_error_string", "simplicial_attn_abi_version", "simplicial_attn_path_name",
+        "simplicial_attn_bwd_preprocess", "simplicial_attn_bwd_query_side",
+        "simplicial_attn_bwd_key_side",
     ])
 
 
@@ -121,6 +123,31 @@ def test_backward_rejects_invalid_arguments(lib):
     assert need > 0
     assert _bwd(lib, ws_bytes=need - 1) == 3
     assert _bwd(lib, ws_bytes=0) == 3
+
+
+@only_without_gpu
+def test_backward_stages_reject_invalid_arguments(lib):
+    size = ctypes.c_size_t
+    args = [1, 64, 2, 128, 16, 8]
+    pre = lambda ptrs, ws=1 << 30, dtype=1, a=args: lib.simplicial_attn_bwd_preprocess(
+        *[ctypes.c_void_p(p) for p in ptrs], size(ws), *a, dtype, None)
+    assert pre([0, A, A]) == 1
+    assert pre([A, MISALIGNED, A]) == 1
+    assert pre([A, A, A], ws=0) == 3
+    assert pre([A, A, A], dtype=3) == 2
+    assert pre([A, A, A], a=[1, 64, 2, 128, 0, 8]) == 1
+    for fn, n in ((lib.simplicial_attn_bwd_query_side, 11), (lib.simplicial_attn_bwd_key_side, 10)):
+        call = lambda ptrs, ws=1 << 30, scale=0.1, a=args, dtype=1: fn(
+            *[ctypes.c_void_p(p) for p in ptrs], size(ws), *a, ctypes.c_float(scale), dtype, None)
+        for i in range(n):
+            ptrs = [A] * n
+            ptrs[i] = 0
+            assert call(ptrs) == 1
+            ptrs[i] = MISALIGNED
+            assert call(ptrs) == 1
+        assert call([A] * n, ws=16) == 3
+        assert call([A] * n, scale=float("nan")) == 1
+        assert call([A] * n, a=[1, 64, 2, 96, 16, 8]) == 2
 
 
 def test_workspace_size(lib):

@@ -7,7 +7,9 @@ import pytest
 import torch
 
 import oracle as orc
-from paper_2507_02754_amd import (load_library, simplicial_attn_bwd, simplicial_attn_fwd,
+from paper_2507_02754_amd import (load_library, simplicial_attn_bwd, simplicial_attn_bwd_key_side,
+                                  simplicial_attn_bwd_preprocess, simplicial_attn_bwd_query_side,
+                                  simplicial_attn_bwd_workspace_size, simplicial_attn_fwd,
                                   simplicial_attn_path_name)
 from paper_2507_02754_amd.workloads import WORKLOADS, draw, make_inputs
 
@@ -129,6 +131,27 @@ def test_backward_is_deterministic():
     for r in runs[1:]:
         for a, c in zip(runs[0], r):
             assert torch.equal(a.view(torch.int16), c.view(torch.int16))
+
+
+@pytest.mark.parametrize("shape", [(1, 2, 700, 128, 256, 32), (1, 1, 300, 64, 40, 64),
+                                   (1, 1, 90, 64, 7, 5)])
+def test_staged_backward_matches_composite(shape):
+    """preprocess + query side + key side (the three stage entry points) give
+    bitwise the same gradients as simplicial_attn_bwd."""
+    b, h, n, d, w1, w2 = shape
+    _announce(f"staged backward {shape}")
+    dt = torch.bfloat16 if (w1, w2) != (7, 5) else torch.float32
+    x = [t.cuda() for t in draw((b, n, h, d), seed=12, dtype=dt)]
+    o, lse = simplicial_attn_fwd(*x[:5], w1, w2)
+    ref = simplicial_attn_bwd(*x[:5], o, x[5], lse, w1, w2)
+    ws = torch.empty(simplicial_attn_bwd_workspace_size(b, n, h, d, w1, w2, dt), dtype=torch.uint8,
+                     device="cuda")
+    simplicial_attn_bwd_preprocess(o, x[5], w1, w2, ws)
+    dq, dkp, dvp = simplicial_attn_bwd_query_side(*x[:5], x[5], lse, w1, w2, ws)
+    dk, dv = simplicial_attn_bwd_key_side(*x[:5], x[5], lse, w1, w2, ws)
+    torch.cuda.synchronize()
+    for a, c in zip(ref, (dq, dk, dkp, dv, dvp)):
+        assert torch.equal(a, c)
 
 
 def test_unit_values_through_gpu():
