@@ -78,73 +78,8 @@ __global__ __launch_bounds__(256) void delta_kernel(Shape s, const uint16_t* __r
   if (row < total && part == 0) delta[row] = acc;
 }
 
-// Staging of one 32-row block of a [.., N, H, D] tensor into LDS, both
-// row-major ([32][D + 8]) and transposed ([D][32 + 4]), zero outside [0, N).
 template <int D, int NTHREADS>
-struct DualStage {
-  static constexpr int rStride = D + 8;
-  static constexpr int tStride = 32 + 4;
-  static constexpr int rowBytes = 32 * rStride * 2;
-  static constexpr int tBytes = D * tStride * 2;
-  static constexpr int bytes = rowBytes + tBytes;
-  // one work item = (row pair p, 8-column chunk dc): 16 pairs x D/8 chunks
-  static constexpr int items = 16 * (D / 8);
-  static constexpr int perThread = (items + NTHREADS - 1) / NTHREADS;
-  u32x4_t reg[perThread][2];
-
-  // `slot` is the caller's thread index, rotated so that two stagings issued
-  // together use disjoint threads when the block has twice `items` threads.
-  __device__ void load(const uint16_t* src, size_t base, size_t rs, int jb, int N, int tid) {
-#pragma unroll
-    for (int x = 0; x < perThread; ++x) {
-      const int it = tid + x * NTHREADS;
-      const int p = it & 15, dc = it >> 4;
-#pragma unroll
-      for (int y = 0; y < 2; ++y) {
-        const int j = jb + 2 * p + y;
-        u32x4_t z = {0u, 0u, 0u, 0u};
-        if (it < items && j >= 0 && j < N) z = ldg128(src + base + static_cast<size_t>(j) * rs + 8 * dc);
-        reg[x][y] = z;
-      }
-    }
-  }
-  __device__ void store(char* dst, int tid) const {
-    uint16_t* rm = reinterpret_cast<uint16_t*>(dst);
-    uint16_t* tr = reinterpret_cast<uint16_t*>(dst + rowBytes);
-#pragma unroll
-    for (int x = 0; x < perThread; ++x) {
-      const int it = tid + x * NTHREADS;
-      if (it >= items) continue;
-      const int p = it & 15, dc = it >> 4;
-      *reinterpret_cast<u32x4_t*>(rm + (2 * p) * rStride + 8 * dc) = reg[x][0];
-      *reinterpret_cast<u32x4_t*>(rm + (2 * p + 1) * rStride + 8 * dc) = reg[x][1];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const unsigned a = reg[x][0][e], b = reg[x][1][e];
-        *reinterpret_cast<unsigned*>(tr + (8 * dc + 2 * e) * tStride + 2 * p) = (a & 0xffffu) | (b << 16);
-        *reinterpret_cast<unsigned*>(tr + (8 * dc + 2 * e + 1) * tStride + 2 * p) = (a >> 16) | (b & 0xffff0000u);
-      }
-    }
-  }
-};
-
-// A-operand fragment (32 rows x 16 K-slots) from a row-major LDS tile.
-template <int STRIDE>
-__device__ __forceinline__ u32x4_t frag_rows(const uint16_t* tile, int c, int h, int t) {
-  return *reinterpret_cast<const u32x4_t*>(tile + c * STRIDE + 16 * t + 8 * h);
-}
-// Fragment whose K-slots run over the 32 rows of a transposed LDS tile, in the
-// order the 32x32 accumulator layout produces them (see mfma_common.h).
-template <int STRIDE>
-__device__ __forceinline__ u32x4_t frag_cols(const uint16_t* ttile, int row, int h, int u) {
-  const uint16_t* p = ttile + row * STRIDE + 16 * u + 4 * h;
-  const u32x2_t a0 = *reinterpret_cast<const u32x2_t*>(p);
-  const u32x2_t a1 = *reinterpret_cast<const u32x2_t*>(p + 8);
-  return u32x4_t{a0[0], a0[1], a1[0], a1[1]};
-}
-
-// Accumulator register v of a 32x32 tile holds row 8*(v/4) + 4*h + (v%4).
-__device__ __forceinline__ int acc_row(int v, int h) { return 8 * (v >> 2) + 4 * h + (v & 3); }
+using DualStage = BlockStage<D, NTHREADS, true, true>;
 
 // ------------------------------------------------------------------ bwd_q ---
 template <int D, int G, int WAVES>
