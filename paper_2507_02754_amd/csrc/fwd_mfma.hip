@@ -18,10 +18,13 @@
 // uses two wavefronts per query). All accumulators live in VGPRs so that two
 // workgroups share a CU (two wavefronts per SIMD): one's exponentials overlap
 // the other's matrix products. The j-window union of the workgroup is walked
-// in 32-column blocks; K (row-major) and V (transposed) blocks are staged in
-// double-buffered LDS with 16-byte coalesced global loads. Within a wavefront
-// all rows share one query, so a block is skipped, fully valid, or masked by
-// column only. The running maximum is rescaled lazily: only when some row's
+// in 32-key blocks. K and V blocks go from HBM straight into a 4-stage ring of
+// swizzled row-major LDS tiles (buffer loads with the LDS destination, no
+// staging registers; the buffer range check zero-fills rows outside [0, N)),
+// issued three blocks ahead. K fragments are read row-wise; V fragments are
+// read with the gfx950 transposing LDS read, so V needs no transposed copy.
+// Within a wavefront all rows share one query, so a block is skipped, fully
+// valid, or masked by column only. The running maximum is rescaled lazily: only when some row's
 // block maximum exceeds it by more than 2^8 (p stays <= 256, exact in fp32 and
 // bf16 range), which after the first blocks is rare.
 // Rows with k < 0 or k <= i - w2 get q~ = 0 and weight 0 in the merge.
@@ -34,19 +37,19 @@ constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 constexpr float kLazyRescale = 8.0f;  // log2 headroom before the running max is raised
 
-template <int D>
+template <int D, int NS>
 struct FwdLds {
-  using SK = BlockStage<D, kThreads, true, false>;
-  using SV = BlockStage<D, kThreads, false, true>;
-  static constexpr int bufBytes = SK::bytes + SV::bytes;
-  static constexpr int mainBytes = 2 * bufBytes;
-  static constexpr int rStride = D + 4;                // epilogue rows (fp32)
+  using T = SwzTile<D>;
+  static constexpr int stageBytes = 2 * T::bytes;  // K tile + V tile of one 32-key block
+  static constexpr int mainBytes = NS * stageBytes;
+  static constexpr int rStride = D + 4;                  // epilogue rows (fp32)
   static constexpr int redBytes = 2 * 32 * rStride * 4;  // two wavefronts per round
   static constexpr int statOff = mainBytes > redBytes ? mainBytes : redBytes;
   static constexpr int bytes = statOff + kWaves * 32 * 4;
 };
 
-template <int D, int G>
+// NS = stages of the ring of 32-key K/V blocks in LDS (prefetch distance NS-1).
+template <int D, int G, int NS>
 __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const uint16_t* __restrict__ q,
                                                                const uint16_t* __restrict__ k,
                                                                const uint16_t* __restrict__ kp,
@@ -58,9 +61,9 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
   constexpr int NDT = D / 32;    // 32-wide d tiles of the output product
   constexpr int QW = kWaves / G; // queries per workgroup
   constexpr int W2P = 32 * G;    // rows per query (w2 padded up to a multiple of 32)
-  using L = FwdLds<D>;
-  using SK = typename L::SK;
-  using SV = typename L::SV;
+  using L = FwdLds<D, NS>;
+  using T = typename L::T;
+  constexpr int LPB = 2 * ((T::instrs + kWaves - 1) / kWaves);  // loads per wavefront per block
   __shared__ __attribute__((aligned(16))) char smem[L::bytes];
   float* stat = reinterpret_cast<float*>(smem + L::statOff);
 
@@ -107,36 +110,46 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
   // ---- main loop over 32-key blocks of the workgroup's window union ----
   const int jlo = i0 - w1 + 1;
   const int nb = (w1 + QW - 1 + 31) / 32;
-  SK stk;
-  SV stv;
+  const int rsb = static_cast<int>(rs) * 2;
+  const __amdgpu_buffer_rsrc_t rk = make_rsrc(k + base, head_bytes(N, rsb, D));
+  const __amdgpu_buffer_rsrc_t rv = make_rsrc(v + base, head_bytes(N, rsb, D));
   f32x16_t acc[NDT];
 #pragma unroll
   for (int dt = 0; dt < NDT; ++dt) acc[dt] = f32x16_t{};
-  float m = -INFINITY, l = 0.f;
+  // Running row maximum m (log2 units). The logit products start from -m_used
+  // in the accumulator, so they come out already shifted; m_used == m except
+  // before the first block and inside a block where m was raised.
+  float m = -INFINITY, l = 0.f, m_used = 0.f;
+  f32x16_t negm = f32x16_t{};
 
-  stk.load(k, base, rs, jlo, N, tid);
-  stv.load(v, base, rs, jlo, N, tid);
-  stk.store(smem, tid);
-  stv.store(smem + SK::bytes, tid);
-  __syncthreads();
+  auto issue = [&](int blk) {
+    char* st = smem + (blk % NS) * L::stageBytes;
+    tile_load_lds<D, kWaves>(rk, rsb, jlo + 32 * blk, st, wave, lane);
+    tile_load_lds<D, kWaves>(rv, rsb, jlo + 32 * blk, st + T::bytes, wave, lane);
+  };
+#pragma unroll
+  for (int p = 0; p < NS - 1; ++p)
+    if (p < nb) issue(p);
 
   for (int blk = 0; blk < nb; ++blk) {
-    const int cur = blk & 1;
-    if (blk + 1 < nb) {
-      stk.load(k, base, rs, jlo + 32 * (blk + 1), N, tid);
-      stv.load(v, base, rs, jlo + 32 * (blk + 1), N, tid);
-    }
-    const uint16_t* kb = reinterpret_cast<const uint16_t*>(smem + cur * L::bufBytes);
-    const uint16_t* vb = reinterpret_cast<const uint16_t*>(smem + cur * L::bufBytes + SK::bytes);
+    if (blk + NS - 2 < nb) wait_vmem<LPB * (NS - 2)>();
+    else wait_vmem<0>();
+    lds_barrier();
+    if (blk + NS - 1 < nb) issue(blk + NS - 1);
+    const char* kt = smem + (blk % NS) * L::stageBytes;
+    const char* vt = kt + T::bytes;
 
     // Valid block-local columns of this wavefront's query.
     const int lo = max(qs, -jlo) - 32 * blk;
     const int hi = min(qs + w1 - 1, N - 1 - jlo) - 32 * blk;
-    const bool act = qvalid && hi >= 0 && lo <= 31 && lo <= hi;
-    if (act) {
-      f32x16_t sacc = f32x16_t{};
+    if (qvalid && hi >= 0 && lo <= 31 && lo <= hi) {
+      u32x4_t kf[NT];
 #pragma unroll
-      for (int t = 0; t < NT; ++t) sacc = mfma32(frag_rows<SK::rStride>(kb, c, h, t), qt[t], sacc);
+      for (int t = 0; t < NT; ++t) kf[t] = frag_row_swz<D>(kt, c, h, t);
+      f32x16_t sacc = mfma32(kf[0], qt[0], negm);
+#pragma unroll
+      for (int t = 1; t < NT; ++t) sacc = mfma32(kf[t], qt[t], sacc);
+      const float m_blk = m_used;
       float sv[16];
 #pragma unroll
       for (int vv = 0; vv < 16; ++vv) sv[vv] = sacc[vv];
@@ -147,11 +160,10 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
           if (jl < lo || jl > hi) sv[vv] = -INFINITY;
         }
       }
-      float mx = fmaxf(fmaxf(sv[0], sv[1]), sv[2]);
+      float mx = fmaxf(sv[0], sv[1]);
 #pragma unroll
-      for (int vv = 3; vv < 15; vv += 2) mx = fmaxf(fmaxf(mx, sv[vv]), sv[vv + 1]);
-      mx = fmaxf(mx, sv[15]);
-      mx = fmaxf(mx, swap_halves(mx));
+      for (int vv = 2; vv < 16; vv += 2) mx = fmaxf(fmaxf(mx, sv[vv]), sv[vv + 1]);
+      mx = fmaxf(mx, swap_halves(mx)) + m_blk;
       if (__builtin_amdgcn_ballot_w64(mx > m + kLazyRescale) != 0) {
         const float mnew = fmaxf(m, mx);
         const float alpha = fast_exp2(m - mnew);
@@ -159,27 +171,29 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) acc[dt] *= alpha;
         m = mnew;
+        m_used = mnew;
+        const float off = m_blk - mnew;
+#pragma unroll
+        for (int vv = 0; vv < 16; ++vv) {
+          sv[vv] += off;
+          negm[vv] = -mnew;
+        }
       }
 #pragma unroll
       for (int vv = 0; vv < 16; ++vv) {
-        sv[vv] = fast_exp2(sv[vv] - m);
+        sv[vv] = fast_exp2(sv[vv]);
         l += sv[vv];
       }
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         const u32x4_t pf = pack_frag(sv, u);
 #pragma unroll
-        for (int dt = 0; dt < NDT; ++dt)
-          acc[dt] = mfma32(frag_cols<SV::tStride>(vb, 32 * dt + c, h, u), pf, acc[dt]);
+        for (int dt = 0; dt < NDT; ++dt) acc[dt] = mfma32(frag_tr_swz<D>(vt, lane, dt, u), pf, acc[dt]);
       }
     }
-
-    if (blk + 1 < nb) {
-      stk.store(smem + (cur ^ 1) * L::bufBytes, tid);
-      stv.store(smem + (cur ^ 1) * L::bufBytes + SK::bytes, tid);
-    }
-    __syncthreads();
   }
+  wait_vmem<0>();
+  __syncthreads();
 
   // ---- epilogue: merge the k-rows of each query (log-sum-exp), apply v'_k ----
   const float lsum = l + swap_halves(l);
@@ -255,10 +269,11 @@ template <int D, int G>
 hipError_t launch(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
                   const void* vp, void* out, float* lse, hipStream_t st) {
   constexpr int QW = kWaves / G;
+  constexpr int NS = 4;
   const long tiles = (s.N + QW - 1) / QW;
   const long total = tiles * s.B * s.H;
   const long grid = ((total + 7) / 8) * 8;
-  hipLaunchKernelGGL((fwd_mfma_kernel<D, G>), dim3(static_cast<unsigned>(grid)), dim3(kThreads), 0,
+  hipLaunchKernelGGL((fwd_mfma_kernel<D, G, NS>), dim3(static_cast<unsigned>(grid)), dim3(kThreads), 0,
                      st, s, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                      static_cast<const uint16_t*>(kp), static_cast<const uint16_t*>(v),
                      static_cast<const uint16_t*>(vp), static_cast<uint16_t*>(out), lse);
@@ -268,7 +283,9 @@ hipError_t launch(const Shape& s, const void* q, const void* k, const void* kp, 
 }  // namespace
 
 bool mfma_fwd_supported(const Shape& s) {
-  return s.dtype == 1 && (s.D == 64 || s.D == 128) && s.w2 <= 64;
+  // Per-head byte offsets are 32-bit in the buffer loads.
+  const bool fits = static_cast<long long>(s.N) * s.H * s.D * 2 < (1ll << 31);
+  return s.dtype == 1 && (s.D == 64 || s.D == 128) && s.w2 <= 64 && fits;
 }
 
 hipError_t mfma_fwd(const Shape& s, const void* q, const void* k, const void* kp, const void* v,

@@ -67,6 +67,102 @@ __device__ __forceinline__ u32x4_t ldg128(const uint16_t* p) {
   return *reinterpret_cast<const u32x4_t*>(p);
 }
 
+// Raw buffer resource over `bytes` bytes at `p` (gfx9 descriptor word 3). Loads
+// through it return 0 for any offset at or past `bytes`, including offsets that
+// are negative as 32-bit integers: the hardware range check zero-fills the rows
+// outside [0, N) of a staged block without per-lane bounds arithmetic.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, unsigned bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, static_cast<int>(bytes), 0x00020000);
+}
+__device__ __forceinline__ u32x4_t ldbuf128(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+// Byte-range of one head's rows of a [.., N, H, D] bf16 tensor, from row 0 to
+// the end of row N-1 (rows are rs_bytes apart).
+__device__ __forceinline__ unsigned head_bytes(int N, int rs_bytes, int D) {
+  return static_cast<unsigned>(N - 1) * static_cast<unsigned>(rs_bytes) + 2u * static_cast<unsigned>(D);
+}
+
+// ---- swizzled row-major tiles, filled by the buffer unit straight into LDS ----
+//
+// A tile holds 32 rows of D bf16 with no padding; row r's 16-byte chunk ch is
+// stored at chunk slot ch ^ swz(r), swz(r) = 4*(r%4) + (r/4)%4 (mod D/8). This
+// keeps both reads below free of bank conflicts at D = 128: 16 lanes reading
+// one chunk of 16 different rows (row fragments), and the transposing read of
+// 4 consecutive rows x 16 consecutive columns per 16 lanes.
+template <int D>
+struct SwzTile {
+  static constexpr int CH = D / 8;  // 16-byte chunks per row
+  static constexpr int bytes = 32 * D * 2;
+  static constexpr int instrs = 32 * CH / 64;  // 64-lane x 16-byte loads per tile
+  __device__ static __forceinline__ int swz(int r) { return (4 * (r & 3) + ((r >> 2) & 3)) & (CH - 1); }
+  __device__ static __forceinline__ int off(int r, int ch) { return (r * CH + (ch ^ swz(r))) * 16; }
+};
+
+// Issues this wavefront's share of the direct-to-LDS loads of one tile: rows
+// jb .. jb+31 of the head behind `r` (row j at byte offset j * rsb). Load k of
+// the tile fills LDS bytes [1024 k, 1024 k + 1024) with lane l writing 16 bytes
+// at 1024 k + 16 l, so lane l fetches the global chunk that belongs there.
+// Rows outside the resource (j < 0 or j >= N) are zero-filled by the range check.
+template <int D, int NWAVES>
+__device__ __forceinline__ void tile_load_lds(__amdgpu_buffer_rsrc_t r, int rsb, int jb, char* tile,
+                                              int wave, int lane) {
+  using T = SwzTile<D>;
+#pragma unroll
+  for (int k0 = 0; k0 < T::instrs; k0 += NWAVES) {
+    const int k = k0 + wave;
+    if (k < T::instrs) {
+      const int p = 64 * k + lane;
+      const int row = p / T::CH, slot = p % T::CH;
+      const int ch = slot ^ T::swz(row);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          r, reinterpret_cast<__attribute__((address_space(3))) void*>(
+                 reinterpret_cast<uintptr_t>(tile + 1024 * k)),
+          16, (jb + row) * rsb + 16 * ch, 0, 0, 0);
+    }
+  }
+}
+
+// Row fragment (lane (h, c): row c, K-slots = columns 16t + 8h .. +7).
+template <int D>
+__device__ __forceinline__ u32x4_t frag_row_swz(const char* tile, int c, int h, int t) {
+  return *reinterpret_cast<const u32x4_t*>(tile + SwzTile<D>::off(c, 2 * t + h));
+}
+
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ u32x2_t ds_read_tr16(const char* p) {
+  const s16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      reinterpret_cast<__attribute__((address_space(3))) s16x4_t*>(reinterpret_cast<uintptr_t>(p)));
+  return __builtin_bit_cast(u32x2_t, v);
+}
+
+// Transposed fragment from a row-major swizzled tile: lane (h, c) gets column
+// 32 dt + c, K-slot e of half h = row 16u + 8(e/4) + 4h + e%4 (the order the
+// 32x32 accumulator produces). Two ds_read_b64_tr_b16: within each group of 16
+// lanes, output lane i receives element i%4 of the 8 bytes addressed by lane
+// 4e + i/4, so lane s of a group addresses row (base + s/4), columns 4(s%4)..+3.
+template <int D>
+__device__ __forceinline__ u32x4_t frag_tr_swz(const char* tile, int lane, int dt, int u) {
+  const int grp = lane >> 4, s = lane & 15, h = grp >> 1;
+  const int col = 32 * dt + 16 * (grp & 1) + 4 * (s & 3);
+  const int ch = col >> 3, within = (col & 7) * 2;
+  const int r0 = 16 * u + 4 * h + (s >> 2);
+  const u32x2_t a = ds_read_tr16(tile + SwzTile<D>::off(r0, ch) + within);
+  const u32x2_t b = ds_read_tr16(tile + SwzTile<D>::off(r0 + 8, ch) + within);
+  return u32x4_t{a[0], a[1], b[0], b[1]};
+}
+
+// Waits until at most N of this wavefront's vector-memory operations are
+// outstanding, then (lds_barrier) synchronises the workgroup. Written as
+// volatile asm with a memory clobber so the compiler keeps LDS accesses on
+// their side of it; the direct-to-LDS loads are invisible to its own waitcnt
+// bookkeeping.
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 // Accumulator register v of a 32x32 tile holds row 8*(v/4) + 4*h + (v%4).
 __device__ __forceinline__ int acc_row(int v, int h) { return 8 * (v >> 2) + 4 * h + (v & 3); }
 
@@ -129,6 +225,21 @@ struct BlockStage {
       }
     }
   }
+  // Same as load(), through a raw buffer resource covering the head's rows
+  // (row j at byte offset j * rsb); rows outside the resource read as zero.
+  __device__ __forceinline__ void load_buf(__amdgpu_buffer_rsrc_t r, int rsb, int jb, int slot) {
+#pragma unroll
+    for (int x = 0; x < perThread; ++x) {
+      const int it = slot + x * NTHREADS;
+      const int p = it & 15, dc = it >> 4;
+#pragma unroll
+      for (int y = 0; y < 2; ++y) {
+        u32x4_t z = {0u, 0u, 0u, 0u};
+        if (it < items) z = ldbuf128(r, (jb + 2 * p + y) * rsb + 16 * dc);
+        reg[x][y] = z;
+      }
+    }
+  }
   __device__ __forceinline__ void store(char* dst, int slot) const {
     uint16_t* rm = reinterpret_cast<uint16_t*>(dst);
     uint16_t* tr = reinterpret_cast<uint16_t*>(dst + rowBytes);
@@ -144,10 +255,12 @@ struct BlockStage {
       if (TR) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
+          // (low halves of rows 2p, 2p+1) and (high halves), one v_perm_b32 each
           const unsigned a = reg[x][0][e], b = reg[x][1][e];
-          *reinterpret_cast<unsigned*>(tr + (8 * dc + 2 * e) * tStride + 2 * p) = (a & 0xffffu) | (b << 16);
+          *reinterpret_cast<unsigned*>(tr + (8 * dc + 2 * e) * tStride + 2 * p) =
+              __builtin_amdgcn_perm(b, a, 0x05040100u);
           *reinterpret_cast<unsigned*>(tr + (8 * dc + 2 * e + 1) * tStride + 2 * p) =
-              (a >> 16) | (b & 0xffff0000u);
+              __builtin_amdgcn_perm(b, a, 0x07060302u);
         }
       }
     }
