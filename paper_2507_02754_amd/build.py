@@ -24,10 +24,13 @@ LIB_PATH = os.path.join(PKG, LIB_NAME)
 ARCH = "gfx950"
 
 # Packed-FP32 VALU forms are disabled for all device code (the host pass warns
-# that it does not know the feature; that warning is harmless).
+# that it does not know the feature; that warning is harmless). MFMAs are
+# selected in their VGPR form: with the accumulators in AGPRs the register
+# allocator otherwise copies them across every loop iteration.
 HIP_FLAGS = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
     "-Wall", "-Wno-unused-function", "-Wno-unused-command-line-argument",
 ]
 

@@ -78,26 +78,22 @@ __global__ __launch_bounds__(256) void delta_kernel(Shape s, const uint16_t* __r
   if (row < total && part == 0) delta[row] = acc;
 }
 
-template <int D, int NTHREADS>
-using DualStage = BlockStage<D, NTHREADS, true, true>;
-
 // ------------------------------------------------------------------ bwd_q ---
-template <int D, int G, int WAVES>
+template <int D, int G, int WAVES, int NS>
 struct BwdQLds {
-  using St = DualStage<D, 64 * WAVES>;
-  static constexpr int stageBytes = 2 * St::bytes;  // K and V
-  static constexpr int mainBytes = 2 * stageBytes;  // double buffered
+  using T = SwzTile<D>;
+  static constexpr int stageBytes = 2 * T::bytes;   // K tile + V tile of one 32-key block
+  static constexpr int ringOff = 0;                 // NS stages of the K/V ring
   static constexpr int rStride = D + 4;             // fp32 rows of the reductions
   static constexpr int QW = WAVES / G;
-  static constexpr int RB = 32 * G + QW;            // ring rows
-  static constexpr int redWaves = WAVES < 4 ? WAVES : 4;
-  static constexpr int redBytes = redWaves * 32 * rStride * 4;
-  static constexpr int region0 = mainBytes > redBytes ? mainBytes : redBytes;
-  static constexpr int ringBytes = 2 * RB * rStride * 4;
-  static constexpr int bytes = region0 + ringBytes;
+  static constexpr int RB = 32 * G + QW;            // rows of the dk'/dv' ring
+  static constexpr int redWaves = 2;                // dq column sums, two wavefronts a round
+  static constexpr int redOff = NS * stageBytes;
+  static constexpr int accOff = redOff + redWaves * 32 * rStride * 4;
+  static constexpr int bytes = accOff + 2 * RB * rStride * 4;
 };
 
-template <int D, int G, int WAVES>
+template <int D, int G, int WAVES, int NS>
 __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
     Shape s, BwdPlan plan, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ kp, const uint16_t* __restrict__ v, const uint16_t* __restrict__ vp,
@@ -107,11 +103,14 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
   constexpr int NT = D / 16, NDT = D / 32;
   constexpr int W2P = 32 * G;
   constexpr int NTH = 64 * WAVES;
-  using L = BwdQLds<D, G, WAVES>;
-  using St = typename L::St;
+  using L = BwdQLds<D, G, WAVES, NS>;
+  using T = typename L::T;
   constexpr int QW = L::QW, RB = L::RB;
+  constexpr int LPB = 2 * ((T::instrs + WAVES - 1) / WAVES);  // loads per wavefront per block
+  static_assert(WAVES % L::redWaves == 0 && L::redWaves % G == 0, "reduction rounds");
   __shared__ __attribute__((aligned(16))) char smem[L::bytes];
-  float* ring_kp = reinterpret_cast<float*>(smem + L::region0);
+  float* red = reinterpret_cast<float*>(smem + L::redOff);
+  float* ring_kp = reinterpret_cast<float*>(smem + L::accOff);
   float* ring_vp = ring_kp + RB * L::rStride;
 
   const int total = plan.nchunks * s.B * s.H;
@@ -137,6 +136,9 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
   float* ws_head_vp = ws_head_kp + plan.halo_floats;
   float* ws_tail_kp = ws_head_vp + plan.halo_floats;
   float* ws_tail_vp = ws_tail_kp + plan.halo_floats;
+  const int rsb = static_cast<int>(rs) * 2;
+  const __amdgpu_buffer_rsrc_t rk = make_rsrc(k + base, head_bytes(N, rsb, D));
+  const __amdgpu_buffer_rsrc_t rv = make_rsrc(v + base, head_bytes(N, rsb, D));
 
   for (int x = tid; x < 2 * RB * L::rStride; x += NTH) ring_kp[x] = 0.f;
 
@@ -165,185 +167,191 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
     }
   };
 
-  St stk, stv;
-  const int vslot = NTH >= 2 * St::items ? (tid + St::items) % NTH : tid;
-  for (int i0 = cs; i0 < ce; i0 += QW) {
-    const int i = i0 + qs;
-    const int kk = i - W2P + 1 + 32 * g + c;
-    const bool rowvalid = i < ce && kk >= 0 && kk > i - w2;
-    const bool qvalid = i < ce;
-
-    u32x4_t qt[NT], ot[NT];
+  // One flattened pipeline over (query tile, 32-key block): the K/V ring keeps
+  // NS-1 blocks in flight across tile boundaries.
+  const int nb = (w1 + QW - 1 + 31) / 32;
+  const int ntiles = (ce - cs + QW - 1) / QW;
+  const int total_it = ntiles * nb;
+  auto issue = [&](int it) {
+    const int tile = it / nb, blk = it - tile * nb;
+    const int jb = cs + tile * QW - w1 + 1 + 32 * blk;
+    char* st = smem + (it % NS) * L::stageBytes;
+    tile_load_lds<D, WAVES>(rk, rsb, jb, st, wave, lane);
+    tile_load_lds<D, WAVES>(rv, rsb, jb, st + T::bytes, wave, lane);
+  };
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      u32x4_t a4 = {0u, 0u, 0u, 0u}, b4 = {0u, 0u, 0u, 0u};
-      if (rowvalid) {
-        const u32x4_t qa = ldg128(q + base + static_cast<size_t>(i) * rs + 16 * t + 8 * h);
-        const u32x4_t ka = ldg128(kp + base + static_cast<size_t>(kk) * rs + 16 * t + 8 * h);
-        const u32x4_t oa = ldg128(dout + base + static_cast<size_t>(i) * rs + 16 * t + 8 * h);
-        const u32x4_t va = ldg128(vp + base + static_cast<size_t>(kk) * rs + 16 * t + 8 * h);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          a4[e] = pack_bf16x2(bf16_lo(qa[e]) * bf16_lo(ka[e]) * qscale,
-                              bf16_hi(qa[e]) * bf16_hi(ka[e]) * qscale);
-          b4[e] = pack_bf16x2(bf16_lo(oa[e]) * bf16_lo(va[e]), bf16_hi(oa[e]) * bf16_hi(va[e]));
-        }
-      }
-      qt[t] = a4;
-      ot[t] = b4;
-    }
-    const float lse2 = qvalid ? lse[stat + i] * kLog2e : 0.f;
-    const float dlt = qvalid ? delta[stat + i] : 0.f;
+  for (int p = 0; p < NS - 1; ++p)
+    if (p < total_it) issue(p);
+  lds_barrier();  // ring rows cleared
 
-    f32x16_t adq[NDT], au[NDT];
-#pragma unroll
-    for (int dt = 0; dt < NDT; ++dt) {
-      adq[dt] = f32x16_t{};
-      au[dt] = f32x16_t{};
-    }
+  u32x4_t qt[NT], ot[NT];
+  f32x16_t adq[NDT], au[NDT];
+  float lse2 = 0.f, dlt = 0.f;
+  int i = 0, kk = 0;
+  bool rowvalid = false, qvalid = false;
 
+  for (int it = 0; it < total_it; ++it) {
+    const int tile = it / nb, blk = it - tile * nb;
+    const int i0 = cs + tile * QW;
     const int jlo = i0 - w1 + 1;
-    const int nb = (w1 + QW - 1 + 31) / 32;
-    stk.load(k, base, rs, jlo, N, tid);
-    stv.load(v, base, rs, jlo, N, vslot);
-    stk.store(smem, tid);
-    stv.store(smem + St::bytes, vslot);
-    __syncthreads();
-
-    for (int blk = 0; blk < nb; ++blk) {
-      const int cur = blk & 1;
-      if (blk + 1 < nb) {
-        stk.load(k, base, rs, jlo + 32 * (blk + 1), N, tid);
-        stv.load(v, base, rs, jlo + 32 * (blk + 1), N, vslot);
-      }
-      char* sb = smem + cur * L::stageBytes;
-      const uint16_t* kr_ = reinterpret_cast<const uint16_t*>(sb);
-      const uint16_t* kt_ = reinterpret_cast<const uint16_t*>(sb + St::rowBytes);
-      const uint16_t* vr_ = reinterpret_cast<const uint16_t*>(sb + St::bytes);
-      const uint16_t* vt_ = reinterpret_cast<const uint16_t*>(sb + St::bytes + St::rowBytes);
-
-      const int lo = max(qs, -jlo) - 32 * blk;
-      const int hi = min(qs + w1 - 1, N - 1 - jlo) - 32 * blk;
-      const bool act = qvalid && hi >= 0 && lo <= 31 && lo <= hi;
-      if (act) {
-        f32x16_t sacc = f32x16_t{}, pacc = f32x16_t{};
+    if (blk == 0) {
+      // ---- tile prologue: modulated operands of this wavefront's 32 rows ----
+      i = i0 + qs;
+      kk = i - W2P + 1 + 32 * g + c;
+      qvalid = i < ce;
+      rowvalid = qvalid && kk >= 0 && kk > i - w2;
 #pragma unroll
-        for (int t = 0; t < NT; ++t) sacc = mfma32(frag_rows<St::rStride>(kr_, c, h, t), qt[t], sacc);
-#pragma unroll
-        for (int t = 0; t < NT; ++t) pacc = mfma32(frag_rows<St::rStride>(vr_, c, h, t), ot[t], pacc);
-        float pv[16], dv_[16];
-#pragma unroll
-        for (int vv = 0; vv < 16; ++vv) {
-          const int jl = acc_row(vv, h);
-          const bool ok = rowvalid && jl >= lo && jl <= hi;
-          const float p = ok ? fast_exp2(sacc[vv] - lse2) : 0.f;
-          pv[vv] = p;
-          dv_[vv] = p * (pacc[vv] - dlt);
-        }
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          u32x4_t pf, df;
+      for (int t = 0; t < NT; ++t) {
+        u32x4_t a4 = {0u, 0u, 0u, 0u}, b4 = {0u, 0u, 0u, 0u};
+        if (rowvalid) {
+          const u32x4_t qa = ldg128(q + base + static_cast<size_t>(i) * rs + 16 * t + 8 * h);
+          const u32x4_t ka = ldg128(kp + base + static_cast<size_t>(kk) * rs + 16 * t + 8 * h);
+          const u32x4_t oa = ldg128(dout + base + static_cast<size_t>(i) * rs + 16 * t + 8 * h);
+          const u32x4_t va = ldg128(vp + base + static_cast<size_t>(kk) * rs + 16 * t + 8 * h);
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            pf[e] = pack_bf16x2(pv[8 * u + 2 * e], pv[8 * u + 2 * e + 1]);
-            df[e] = pack_bf16x2(dv_[8 * u + 2 * e], dv_[8 * u + 2 * e + 1]);
+            a4[e] = pack_bf16x2(bf16_lo(qa[e]) * bf16_lo(ka[e]) * qscale,
+                                bf16_hi(qa[e]) * bf16_hi(ka[e]) * qscale);
+            b4[e] = pack_bf16x2(bf16_lo(oa[e]) * bf16_lo(va[e]), bf16_hi(oa[e]) * bf16_hi(va[e]));
           }
+        }
+        qt[t] = a4;
+        ot[t] = b4;
+      }
+      lse2 = qvalid ? lse[stat + i] * kLog2e : 0.f;
+      dlt = qvalid ? delta[stat + i] : 0.f;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) {
+        adq[dt] = f32x16_t{};
+        au[dt] = f32x16_t{};
+      }
+    }
+
+    if (it + NS - 2 < total_it) wait_vmem<LPB * (NS - 2)>();
+    else wait_vmem<0>();
+    lds_barrier();
+    if (it + NS - 1 < total_it) issue(it + NS - 1);
+    const char* kt = smem + (it % NS) * L::stageBytes;
+    const char* vt = kt + T::bytes;
+
+    const int lo = max(qs, -jlo) - 32 * blk;
+    const int hi = min(qs + w1 - 1, N - 1 - jlo) - 32 * blk;
+    if (qvalid && hi >= 0 && lo <= 31 && lo <= hi) {
+      f32x16_t sacc = f32x16_t{}, pacc = f32x16_t{};
+#pragma unroll
+      for (int t = 0; t < NT; ++t) sacc = mfma32(frag_row_swz<D>(kt, c, h, t), qt[t], sacc);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) pacc = mfma32(frag_row_swz<D>(vt, c, h, t), ot[t], pacc);
+      u32x4_t pf[2], df[2];
+#pragma unroll
+      for (int vv = 0; vv < 16; vv += 2) {
+        float p2[2], d2[2];
+#pragma unroll
+        for (int x = 0; x < 2; ++x) {
+          const int jl = acc_row(vv + x, h);
+          const bool ok = rowvalid && jl >= lo && jl <= hi;
+          const float pr = ok ? fast_exp2(sacc[vv + x] - lse2) : 0.f;
+          p2[x] = pr;
+          d2[x] = pr * (pacc[vv + x] - dlt);
+        }
+        pf[vv >> 3][(vv & 7) >> 1] = pack_bf16x2(p2[0], p2[1]);
+        df[vv >> 3][(vv & 7) >> 1] = pack_bf16x2(d2[0], d2[1]);
+      }
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+          adq[dt] = mfma32(frag_tr_swz<D>(kt, lane, dt, u), df[u], adq[dt]);
+          au[dt] = mfma32(frag_tr_swz<D>(vt, lane, dt, u), pf[u], au[dt]);
+        }
+      }
+    }
+
+    if (blk == nb - 1) {
+      // ---- tile epilogue ----
+      // dq_i = scale * sum_k k'_k o dQ~_(i,k): column sums over the k-rows.
+      // accumulator layout: lane holds row c, d = 32 dt + 8 (v/4) + 4 h + v%4
+#pragma unroll
+      for (int round = 0; round < WAVES / L::redWaves; ++round) {
+        const bool mine = wave / L::redWaves == round;
+        if (mine) {
+          float* rw = red + (wave % L::redWaves) * 32 * L::rStride;
 #pragma unroll
           for (int dt = 0; dt < NDT; ++dt) {
-            adq[dt] = mfma32(frag_cols<St::tStride>(kt_, 32 * dt + c, h, u), df, adq[dt]);
-            au[dt] = mfma32(frag_cols<St::tStride>(vt_, 32 * dt + c, h, u), pf, au[dt]);
+#pragma unroll
+            for (int qd = 0; qd < 4; ++qd) {
+              const int d = 32 * dt + 8 * qd + 4 * h;
+              u32x2_t kv = {0u, 0u};
+              if (rowvalid) kv = *reinterpret_cast<const u32x2_t*>(kp + base + static_cast<size_t>(kk) * rs + d);
+              float4 val;
+              val.x = bf16_lo(kv[0]) * adq[dt][4 * qd + 0];
+              val.y = bf16_hi(kv[0]) * adq[dt][4 * qd + 1];
+              val.z = bf16_lo(kv[1]) * adq[dt][4 * qd + 2];
+              val.w = bf16_hi(kv[1]) * adq[dt][4 * qd + 3];
+              *reinterpret_cast<float4*>(rw + c * L::rStride + d) = val;
+            }
           }
         }
-      }
-      if (blk + 1 < nb) {
-        stk.store(smem + (cur ^ 1) * L::stageBytes, tid);
-        stv.store(smem + (cur ^ 1) * L::stageBytes + St::bytes, vslot);
-      }
-      __syncthreads();
-    }
-
-    // ---- dq_i = scale * sum_k k'_k o dQ~_(i,k): column sums over the k-rows ----
-    // accumulator register layout: lane holds row c, d = 32 dt + 8 (v/4) + 4 h + v%4
-    float* red = reinterpret_cast<float*>(smem);
-    constexpr int RW = L::redWaves;
+        lds_barrier();
+        // the G wavefronts of a query split its D columns
+        constexpr int COLS = D / G;
+        if (mine && qvalid && 2 * lane < COLS) {
+          const int c0 = g * COLS;
+          float o0 = 0.f, o1 = 0.f;
 #pragma unroll
-    for (int round = 0; round < WAVES / RW; ++round) {
-      const bool mine = wave / RW == round;
-      if (mine) {
-        float* rw = red + (wave % RW) * 32 * L::rStride;
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) {
-#pragma unroll
-          for (int qd = 0; qd < 4; ++qd) {
-            const int d = 32 * dt + 8 * qd + 4 * h;
-            u32x2_t kv = {0u, 0u};
-            if (rowvalid) kv = *reinterpret_cast<const u32x2_t*>(kp + base + static_cast<size_t>(kk) * rs + d);
-            float4 val;
-            val.x = bf16_lo(kv[0]) * adq[dt][4 * qd + 0];
-            val.y = bf16_hi(kv[0]) * adq[dt][4 * qd + 1];
-            val.z = bf16_lo(kv[1]) * adq[dt][4 * qd + 2];
-            val.w = bf16_hi(kv[1]) * adq[dt][4 * qd + 3];
-            *reinterpret_cast<float4*>(rw + c * L::rStride + d) = val;
-          }
-        }
-      }
-      __syncthreads();
-      // the first wave of each query (g == 0) sums its G waves' rows
-      if (mine && g == 0 && qvalid && 2 * lane < D) {
-        float o0 = 0.f, o1 = 0.f;
-#pragma unroll
-        for (int gg = 0; gg < G; ++gg) {
-          const float* rw = red + ((wave + gg) % RW) * 32 * L::rStride;
+          for (int gg = 0; gg < G; ++gg) {
+            const float* rw = red + ((wave - g + gg) % L::redWaves) * 32 * L::rStride + c0 + 2 * lane;
 #pragma unroll 8
-          for (int rr = 0; rr < 32; ++rr) {
-            const float2 x = *reinterpret_cast<const float2*>(rw + rr * L::rStride + 2 * lane);
-            o0 += x.x;
-            o1 += x.y;
+            for (int rr = 0; rr < 32; ++rr) {
+              const float2 x = *reinterpret_cast<const float2*>(rw + rr * L::rStride);
+              o0 += x.x;
+              o1 += x.y;
+            }
+          }
+          *reinterpret_cast<unsigned*>(dq + base + static_cast<size_t>(i) * rs + c0 + 2 * lane) =
+              pack_bf16x2(o0 * s.scale, o1 * s.scale);
+        }
+        lds_barrier();
+      }
+
+      // dk'/dv' contributions into the ring, one wavefront at a time.
+      for (int ww = 0; ww < WAVES; ++ww) {
+        if (wave == ww && rowvalid) {
+          const int slot = (kk - kbase) % RB;
+#pragma unroll
+          for (int dt = 0; dt < NDT; ++dt) {
+#pragma unroll
+            for (int qd = 0; qd < 4; ++qd) {
+              const int d = 32 * dt + 8 * qd + 4 * h;
+              const u32x2_t qv = *reinterpret_cast<const u32x2_t*>(q + base + static_cast<size_t>(i) * rs + d);
+              const u32x2_t ov = *reinterpret_cast<const u32x2_t*>(dout + base + static_cast<size_t>(i) * rs + d);
+              float4* a = reinterpret_cast<float4*>(ring_kp + slot * L::rStride + d);
+              float4* bb = reinterpret_cast<float4*>(ring_vp + slot * L::rStride + d);
+              float4 x = *a, y = *bb;
+              x.x += s.scale * bf16_lo(qv[0]) * adq[dt][4 * qd + 0];
+              x.y += s.scale * bf16_hi(qv[0]) * adq[dt][4 * qd + 1];
+              x.z += s.scale * bf16_lo(qv[1]) * adq[dt][4 * qd + 2];
+              x.w += s.scale * bf16_hi(qv[1]) * adq[dt][4 * qd + 3];
+              y.x += bf16_lo(ov[0]) * au[dt][4 * qd + 0];
+              y.y += bf16_hi(ov[0]) * au[dt][4 * qd + 1];
+              y.z += bf16_lo(ov[1]) * au[dt][4 * qd + 2];
+              y.w += bf16_hi(ov[1]) * au[dt][4 * qd + 3];
+              *a = x;
+              *bb = y;
+            }
           }
         }
-        *reinterpret_cast<unsigned*>(dq + base + static_cast<size_t>(i) * rs + 2 * lane) =
-            pack_bf16x2(o0 * s.scale, o1 * s.scale);
+        lds_barrier();
       }
-      __syncthreads();
-    }
 
-    // ---- dk'/dv' contributions into the ring, one wavefront at a time ----
-    for (int ww = 0; ww < WAVES; ++ww) {
-      if (wave == ww && rowvalid) {
-        const int slot = (kk - kbase) % RB;
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) {
-#pragma unroll
-          for (int qd = 0; qd < 4; ++qd) {
-            const int d = 32 * dt + 8 * qd + 4 * h;
-            const u32x2_t qv = *reinterpret_cast<const u32x2_t*>(q + base + static_cast<size_t>(i) * rs + d);
-            const u32x2_t ov = *reinterpret_cast<const u32x2_t*>(dout + base + static_cast<size_t>(i) * rs + d);
-            float4* a = reinterpret_cast<float4*>(ring_kp + slot * L::rStride + d);
-            float4* bb = reinterpret_cast<float4*>(ring_vp + slot * L::rStride + d);
-            float4 x = *a, y = *bb;
-            x.x += s.scale * bf16_lo(qv[0]) * adq[dt][4 * qd + 0];
-            x.y += s.scale * bf16_hi(qv[0]) * adq[dt][4 * qd + 1];
-            x.z += s.scale * bf16_lo(qv[1]) * adq[dt][4 * qd + 2];
-            x.w += s.scale * bf16_hi(qv[1]) * adq[dt][4 * qd + 3];
-            y.x += bf16_lo(ov[0]) * au[dt][4 * qd + 0];
-            y.y += bf16_hi(ov[0]) * au[dt][4 * qd + 1];
-            y.z += bf16_lo(ov[1]) * au[dt][4 * qd + 2];
-            y.w += bf16_hi(ov[1]) * au[dt][4 * qd + 3];
-            *a = x;
-            *bb = y;
-          }
-        }
-      }
-      __syncthreads();
+      // Rows no later query of the chunk touches are complete.
+      const int fl_lo = i0 - W2P + 1;
+      const int fl_hi = min(i0 + QW, ce) - W2P;  // inclusive
+      for (int kr = fl_lo + wave; kr <= fl_hi; kr += WAVES) flush_row(kr, false);
+      lds_barrier();
     }
-
-    // ---- rows no later query of the chunk touches are complete ----
-    const int fl_lo = i0 - W2P + 1;
-    const int fl_hi = min(i0 + QW, ce) - W2P;  // inclusive
-    for (int kr = fl_lo + wave; kr <= fl_hi; kr += WAVES) flush_row(kr, false);
-    __syncthreads();
   }
-  // ---- rows still open at the end of the chunk ----
+  // Rows still open at the end of the chunk.
   for (int kr = ce - W2P + 1 + wave; kr <= ce - 1; kr += WAVES) flush_row(kr, ce < N);
 }
 
@@ -379,8 +387,8 @@ __global__ __launch_bounds__(256) void halo_fixup_kernel(Shape s, BwdPlan plan, 
 // ----------------------------------------------------------------- bwd_kv ---
 template <int D>
 struct BwdKvLds {
-  using St = DualStage<D, 256>;
-  static constexpr int bufBytes = 2 * St::bytes;  // q~ and do~ of one row block
+  using T = SwzTile<D>;
+  static constexpr int bufBytes = 2 * T::bytes;  // q~ and do~ tiles of one row block
   static constexpr int mainBytes = 2 * bufBytes;
   static constexpr int oStride = D + 4;
   static constexpr int outBytes = 4 * 32 * oStride * 4;
@@ -396,7 +404,7 @@ __global__ __launch_bounds__(256) void bwd_kv_kernel(
   constexpr int NT = D / 16, NDT = D / 32;
   constexpr int W2P = 32 * G;
   using L = BwdKvLds<D>;
-  using St = typename L::St;
+  using T = typename L::T;
   __shared__ __attribute__((aligned(16))) char smem[L::bytes];
 
   const int jblocks = (s.N + 127) / 128;
@@ -473,23 +481,13 @@ __global__ __launch_bounds__(256) void bwd_kv_kernel(
       fo[y] = b4;
     }
   };
+  // Row-major swizzled tiles: rows (2p, 2p+1), 16-byte chunk dc of each.
   auto put = [&](char* buf) {
     if (!fitem) return;
-    char* parts[2] = {buf, buf + St::bytes};
-    const u32x4_t* src[2] = {fq, fo};
-#pragma unroll
-    for (int z = 0; z < 2; ++z) {
-      uint16_t* rm = reinterpret_cast<uint16_t*>(parts[z]);
-      uint16_t* tr = reinterpret_cast<uint16_t*>(parts[z] + St::rowBytes);
-      *reinterpret_cast<u32x4_t*>(rm + (2 * p_) * St::rStride + 8 * dc) = src[z][0];
-      *reinterpret_cast<u32x4_t*>(rm + (2 * p_ + 1) * St::rStride + 8 * dc) = src[z][1];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const unsigned a = src[z][0][e], bb = src[z][1][e];
-        *reinterpret_cast<unsigned*>(tr + (8 * dc + 2 * e) * St::tStride + 2 * p_) = (a & 0xffffu) | (bb << 16);
-        *reinterpret_cast<unsigned*>(tr + (8 * dc + 2 * e + 1) * St::tStride + 2 * p_) = (a >> 16) | (bb & 0xffff0000u);
-      }
-    }
+    *reinterpret_cast<u32x4_t*>(buf + T::off(2 * p_, dc)) = fq[0];
+    *reinterpret_cast<u32x4_t*>(buf + T::off(2 * p_ + 1, dc)) = fq[1];
+    *reinterpret_cast<u32x4_t*>(buf + T::bytes + T::off(2 * p_, dc)) = fo[0];
+    *reinterpret_cast<u32x4_t*>(buf + T::bytes + T::off(2 * p_ + 1, dc)) = fo[1];
   };
 
   if (nrb > 0) {
@@ -504,41 +502,38 @@ __global__ __launch_bounds__(256) void bwd_kv_kernel(
     // this wavefront's keys see query i iff jw + 31 >= i - w1 + 1 and jw <= i
     const bool act = jw <= i && jw + 31 > i - w1 && jw < N;
     if (act) {
-      const char* buf = smem + cur * L::bufBytes;
-      const uint16_t* qr = reinterpret_cast<const uint16_t*>(buf);
-      const uint16_t* qtt = reinterpret_cast<const uint16_t*>(buf + St::rowBytes);
-      const uint16_t* orr = reinterpret_cast<const uint16_t*>(buf + St::bytes);
-      const uint16_t* ott = reinterpret_cast<const uint16_t*>(buf + St::bytes + St::rowBytes);
+      const char* qtile = smem + cur * L::bufBytes;
+      const char* otile = qtile + T::bytes;
       f32x16_t sacc = f32x16_t{}, pacc = f32x16_t{};
 #pragma unroll
-      for (int t = 0; t < NT; ++t) sacc = mfma32(frag_rows<St::rStride>(qr, c, h, t), kf[t], sacc);
+      for (int t = 0; t < NT; ++t) sacc = mfma32(frag_row_swz<D>(qtile, c, h, t), kf[t], sacc);
 #pragma unroll
-      for (int t = 0; t < NT; ++t) pacc = mfma32(frag_rows<St::rStride>(orr, c, h, t), vf[t], pacc);
+      for (int t = 0; t < NT; ++t) pacc = mfma32(frag_row_swz<D>(otile, c, h, t), vf[t], pacc);
       const float lse2 = lse[stat + i] * kLog2e;
       const float dlt = delta[stat + i];
       const bool colok = jme <= i && jme > i - w1 && jme < N;
-      float pv[16], dsv[16];
+      u32x4_t pf[2], df[2];
 #pragma unroll
-      for (int vv = 0; vv < 16; ++vv) {
-        const int r = acc_row(vv, h);
-        const int kk = i - W2P + 1 + 32 * g + r;
-        const bool ok = colok && kk >= 0 && kk > i - w2;
-        const float p = ok ? fast_exp2(sacc[vv] - lse2) : 0.f;
-        pv[vv] = p;
-        dsv[vv] = p * (pacc[vv] - dlt);
+      for (int vv = 0; vv < 16; vv += 2) {
+        float p2[2], d2[2];
+#pragma unroll
+        for (int x = 0; x < 2; ++x) {
+          const int r = acc_row(vv + x, h);
+          const int kk = i - W2P + 1 + 32 * g + r;
+          const bool ok = colok && kk >= 0 && kk > i - w2;
+          const float pr = ok ? fast_exp2(sacc[vv + x] - lse2) : 0.f;
+          p2[x] = pr;
+          d2[x] = pr * (pacc[vv + x] - dlt);
+        }
+        pf[vv >> 3][(vv & 7) >> 1] = pack_bf16x2(p2[0], p2[1]);
+        df[vv >> 3][(vv & 7) >> 1] = pack_bf16x2(d2[0], d2[1]);
       }
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
-        u32x4_t pf, df;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          pf[e] = pack_bf16x2(pv[8 * u + 2 * e], pv[8 * u + 2 * e + 1]);
-          df[e] = pack_bf16x2(dsv[8 * u + 2 * e], dsv[8 * u + 2 * e + 1]);
-        }
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) {
-          adv[dt] = mfma32(pf, frag_cols<St::tStride>(ott, 32 * dt + c, h, u), adv[dt]);
-          adk[dt] = mfma32(df, frag_cols<St::tStride>(qtt, 32 * dt + c, h, u), adk[dt]);
+          adv[dt] = mfma32(pf[u], frag_tr_swz<D>(otile, lane, dt, u), adv[dt]);
+          adk[dt] = mfma32(df[u], frag_tr_swz<D>(qtile, lane, dt, u), adk[dt]);
         }
       }
     }
@@ -589,9 +584,9 @@ hipError_t launch_stage(const Shape& s, BwdStage stage, const void* q, const voi
   const auto* VP = static_cast<const uint16_t*>(vp);
   const auto* DO = static_cast<const uint16_t*>(dout);
   if (stage == BwdStage::Query) {
-    constexpr int WAVES = 4;
+    constexpr int WAVES = 4, NS = 3;
     const long totq = static_cast<long>(plan.nchunks) * s.B * s.H;
-    hipLaunchKernelGGL((bwd_q_kernel<D, G, WAVES>), dim3(static_cast<unsigned>(((totq + 7) / 8) * 8)),
+    hipLaunchKernelGGL((bwd_q_kernel<D, G, WAVES, NS>), dim3(static_cast<unsigned>(((totq + 7) / 8) * 8)),
                        dim3(64 * WAVES), 0, st, s, plan, Q, K, KP, V, VP, DO, lse, delta,
                        static_cast<uint16_t*>(g0), static_cast<uint16_t*>(g1),
                        static_cast<uint16_t*>(g2), halo);

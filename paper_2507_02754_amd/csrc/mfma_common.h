@@ -166,25 +166,6 @@ __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(
 // Accumulator register v of a 32x32 tile holds row 8*(v/4) + 4*h + (v%4).
 __device__ __forceinline__ int acc_row(int v, int h) { return 8 * (v >> 2) + 4 * h + (v & 3); }
 
-// A/B-operand fragment (32 rows x 16 K-slots) from a row-major bf16 LDS tile:
-// lane (h, c) takes row c, columns 16t + 8h .. 16t + 8h + 7.
-template <int STRIDE>
-__device__ __forceinline__ u32x4_t frag_rows(const uint16_t* tile, int c, int h, int t) {
-  return *reinterpret_cast<const u32x4_t*>(tile + c * STRIDE + 16 * t + 8 * h);
-}
-
-// Fragment whose K-slots run over 16 of the 32 rows of a transposed LDS tile
-// (tile[col][row]), in the order a 32x32 accumulator produces them: slot e of
-// half h is row 16u + 8(e/4) + 4h + e%4, so accumulator registers 8u..8u+7 of
-// one product can feed the next product directly.
-template <int STRIDE>
-__device__ __forceinline__ u32x4_t frag_cols(const uint16_t* ttile, int row, int h, int u) {
-  const uint16_t* p = ttile + row * STRIDE + 16 * u + 4 * h;
-  const u32x2_t a0 = *reinterpret_cast<const u32x2_t*>(p);
-  const u32x2_t a1 = *reinterpret_cast<const u32x2_t*>(p + 8);
-  return u32x4_t{a0[0], a0[1], a1[0], a1[1]};
-}
-
 // Packs accumulator registers 8u..8u+7 (fp32) into a bf16 operand fragment.
 __device__ __forceinline__ u32x4_t pack_frag(const float* x, int u) {
   u32x4_t r;
@@ -192,79 +173,5 @@ __device__ __forceinline__ u32x4_t pack_frag(const float* x, int u) {
   for (int e = 0; e < 4; ++e) r[e] = pack_bf16x2(x[8 * u + 2 * e], x[8 * u + 2 * e + 1]);
   return r;
 }
-
-// Staging of one 32-row block of a [.., N, H, D] bf16 tensor into LDS, as a
-// row-major tile ([32][D + 8], ROW) and/or a transposed tile ([D][32 + 4], TR);
-// rows outside [0, N) read as zero. One work item = (row pair p, 8-column
-// chunk dc); the paddings keep the fragment reads above conflict-free.
-template <int D, int NTHREADS, bool ROW, bool TR>
-struct BlockStage {
-  static constexpr int rStride = D + 8;
-  static constexpr int tStride = 32 + 4;
-  static constexpr int rowBytes = ROW ? 32 * rStride * 2 : 0;
-  static constexpr int tBytes = TR ? D * tStride * 2 : 0;
-  static constexpr int bytes = rowBytes + tBytes;
-  static constexpr int items = 16 * (D / 8);
-  static constexpr int perThread = (items + NTHREADS - 1) / NTHREADS;
-  u32x4_t reg[perThread][2];
-
-  // `slot` is the caller's thread index, possibly rotated so that two stagings
-  // issued together use disjoint threads.
-  __device__ __forceinline__ void load(const uint16_t* src, size_t base, size_t rs, int jb, int N,
-                                       int slot) {
-#pragma unroll
-    for (int x = 0; x < perThread; ++x) {
-      const int it = slot + x * NTHREADS;
-      const int p = it & 15, dc = it >> 4;
-#pragma unroll
-      for (int y = 0; y < 2; ++y) {
-        const int j = jb + 2 * p + y;
-        u32x4_t z = {0u, 0u, 0u, 0u};
-        if (it < items && j >= 0 && j < N) z = ldg128(src + base + static_cast<size_t>(j) * rs + 8 * dc);
-        reg[x][y] = z;
-      }
-    }
-  }
-  // Same as load(), through a raw buffer resource covering the head's rows
-  // (row j at byte offset j * rsb); rows outside the resource read as zero.
-  __device__ __forceinline__ void load_buf(__amdgpu_buffer_rsrc_t r, int rsb, int jb, int slot) {
-#pragma unroll
-    for (int x = 0; x < perThread; ++x) {
-      const int it = slot + x * NTHREADS;
-      const int p = it & 15, dc = it >> 4;
-#pragma unroll
-      for (int y = 0; y < 2; ++y) {
-        u32x4_t z = {0u, 0u, 0u, 0u};
-        if (it < items) z = ldbuf128(r, (jb + 2 * p + y) * rsb + 16 * dc);
-        reg[x][y] = z;
-      }
-    }
-  }
-  __device__ __forceinline__ void store(char* dst, int slot) const {
-    uint16_t* rm = reinterpret_cast<uint16_t*>(dst);
-    uint16_t* tr = reinterpret_cast<uint16_t*>(dst + rowBytes);
-#pragma unroll
-    for (int x = 0; x < perThread; ++x) {
-      const int it = slot + x * NTHREADS;
-      if (it >= items) continue;
-      const int p = it & 15, dc = it >> 4;
-      if (ROW) {
-        *reinterpret_cast<u32x4_t*>(rm + (2 * p) * rStride + 8 * dc) = reg[x][0];
-        *reinterpret_cast<u32x4_t*>(rm + (2 * p + 1) * rStride + 8 * dc) = reg[x][1];
-      }
-      if (TR) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          // (low halves of rows 2p, 2p+1) and (high halves), one v_perm_b32 each
-          const unsigned a = reg[x][0][e], b = reg[x][1][e];
-          *reinterpret_cast<unsigned*>(tr + (8 * dc + 2 * e) * tStride + 2 * p) =
-              __builtin_amdgcn_perm(b, a, 0x05040100u);
-          *reinterpret_cast<unsigned*>(tr + (8 * dc + 2 * e + 1) * tStride + 2 * p) =
-              __builtin_amdgcn_perm(b, a, 0x07060302u);
-        }
-      }
-    }
-  }
-};
 
 }  // namespace sa
