@@ -452,63 +452,87 @@ __global__ __launch_bounds__(256) void bwd_kv_kernel(
   const int nrb = (i_end - j0) * G;
 
   // Formation of one row block: rows (2p, 2p+1), 8 columns per work item.
+  // fetch() issues the global loads of the next row block before the current
+  // one is computed; form_put() multiplies and stores them afterwards, so the
+  // load latency hides behind a whole row block of matrix work.
   constexpr int items = 16 * (D / 8);
   const int p_ = tid & 15, dc = tid >> 4;
   const bool fitem = tid < items;
-  u32x4_t fq[2], fo[2];
-  auto form = [&](int rb) {
+  u32x4_t rq, ro, rk[2], rv[2];
+  auto fetch = [&](int rb) {
     const int i = j0 + rb / G, g = rb % G;
-    u32x4_t qa = {0u, 0u, 0u, 0u}, oa = {0u, 0u, 0u, 0u};
+    const u32x4_t z = {0u, 0u, 0u, 0u};
+    rq = z;
+    ro = z;
     if (fitem) {
-      qa = ldg128(q + base + static_cast<size_t>(i) * rs + 8 * dc);
-      oa = ldg128(dout + base + static_cast<size_t>(i) * rs + 8 * dc);
+      rq = ldg128(q + base + static_cast<size_t>(i) * rs + 8 * dc);
+      ro = ldg128(dout + base + static_cast<size_t>(i) * rs + 8 * dc);
     }
 #pragma unroll
     for (int y = 0; y < 2; ++y) {
       const int kk = i - W2P + 1 + 32 * g + 2 * p_ + y;
-      u32x4_t a4 = {0u, 0u, 0u, 0u}, b4 = {0u, 0u, 0u, 0u};
+      rk[y] = z;
+      rv[y] = z;
       if (fitem && kk >= 0 && kk > i - w2) {
-        const u32x4_t ka = ldg128(kp + base + static_cast<size_t>(kk) * rs + 8 * dc);
-        const u32x4_t va = ldg128(vp + base + static_cast<size_t>(kk) * rs + 8 * dc);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          a4[e] = pack_bf16x2(bf16_lo(qa[e]) * bf16_lo(ka[e]) * qscale,
-                              bf16_hi(qa[e]) * bf16_hi(ka[e]) * qscale);
-          b4[e] = pack_bf16x2(bf16_lo(oa[e]) * bf16_lo(va[e]), bf16_hi(oa[e]) * bf16_hi(va[e]));
-        }
+        rk[y] = ldg128(kp + base + static_cast<size_t>(kk) * rs + 8 * dc);
+        rv[y] = ldg128(vp + base + static_cast<size_t>(kk) * rs + 8 * dc);
       }
-      fq[y] = a4;
-      fo[y] = b4;
     }
   };
   // Row-major swizzled tiles: rows (2p, 2p+1), 16-byte chunk dc of each.
-  auto put = [&](char* buf) {
+  // Rows whose k is outside the window were fetched as zero, so q~ = do~ = 0.
+  auto form_put = [&](char* buf) {
     if (!fitem) return;
-    *reinterpret_cast<u32x4_t*>(buf + T::off(2 * p_, dc)) = fq[0];
-    *reinterpret_cast<u32x4_t*>(buf + T::off(2 * p_ + 1, dc)) = fq[1];
-    *reinterpret_cast<u32x4_t*>(buf + T::bytes + T::off(2 * p_, dc)) = fo[0];
-    *reinterpret_cast<u32x4_t*>(buf + T::bytes + T::off(2 * p_ + 1, dc)) = fo[1];
+#pragma unroll
+    for (int y = 0; y < 2; ++y) {
+      u32x4_t a4, b4;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        a4[e] = pack_bf16x2(bf16_lo(rq[e]) * bf16_lo(rk[y][e]) * qscale,
+                            bf16_hi(rq[e]) * bf16_hi(rk[y][e]) * qscale);
+        b4[e] = pack_bf16x2(bf16_lo(ro[e]) * bf16_lo(rv[y][e]), bf16_hi(ro[e]) * bf16_hi(rv[y][e]));
+      }
+      *reinterpret_cast<u32x4_t*>(buf + T::off(2 * p_ + y, dc)) = a4;
+      *reinterpret_cast<u32x4_t*>(buf + T::bytes + T::off(2 * p_ + y, dc)) = b4;
+    }
   };
 
   if (nrb > 0) {
-    form(0);
-    put(smem);
+    fetch(0);
+    form_put(smem);
   }
   __syncthreads();
   for (int rb = 0; rb < nrb; ++rb) {
     const int cur = rb & 1;
-    if (rb + 1 < nrb) form(rb + 1);
+    if (rb + 1 < nrb) fetch(rb + 1);
     const int i = j0 + rb / G, g = rb % G;
     // this wavefront's keys see query i iff jw + 31 >= i - w1 + 1 and jw <= i
     const bool act = jw <= i && jw + 31 > i - w1 && jw < N;
     if (act) {
       const char* qtile = smem + cur * L::bufBytes;
       const char* otile = qtile + T::bytes;
+      // All operand reads of the row block are issued before the products
+      // that consume them, so LDS latency overlaps the matrix work.
+      u32x4_t qa[NT], oa[NT];
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        qa[t] = frag_row_swz<D>(qtile, c, h, t);
+        oa[t] = frag_row_swz<D>(otile, c, h, t);
+      }
+      u32x4_t otr[2][NDT], qtr[2][NDT];
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+          otr[u][dt] = frag_tr_swz<D>(otile, lane, dt, u);
+          qtr[u][dt] = frag_tr_swz<D>(qtile, lane, dt, u);
+        }
       f32x16_t sacc = f32x16_t{}, pacc = f32x16_t{};
 #pragma unroll
-      for (int t = 0; t < NT; ++t) sacc = mfma32(frag_row_swz<D>(qtile, c, h, t), kf[t], sacc);
-#pragma unroll
-      for (int t = 0; t < NT; ++t) pacc = mfma32(frag_row_swz<D>(otile, c, h, t), vf[t], pacc);
+      for (int t = 0; t < NT; ++t) {
+        sacc = mfma32(qa[t], kf[t], sacc);
+        pacc = mfma32(oa[t], vf[t], pacc);
+      }
       const float lse2 = lse[stat + i] * kLog2e;
       const float dlt = delta[stat + i];
       const bool colok = jme <= i && jme > i - w1 && jme < N;
@@ -532,12 +556,21 @@ __global__ __launch_bounds__(256) void bwd_kv_kernel(
       for (int u = 0; u < 2; ++u) {
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) {
-          adv[dt] = mfma32(pf[u], frag_tr_swz<D>(otile, lane, dt, u), adv[dt]);
-          adk[dt] = mfma32(df[u], frag_tr_swz<D>(qtile, lane, dt, u), adk[dt]);
+          adv[dt] = mfma32(pf[u], otr[u][dt], adv[dt]);
+          adk[dt] = mfma32(df[u], qtr[u][dt], adk[dt]);
         }
       }
+      // Schedule: the row-fragment reads first, then the logit/dP products
+      // with two transposing reads slipped in behind each, so the operands of
+      // the dV/dK products arrive while the first products and the softmax run.
+      __builtin_amdgcn_sched_group_barrier(0x100, 2 * NT, 0);
+#pragma unroll
+      for (int x = 0; x < 2 * NT; ++x) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2 * 2 * NDT * 2 / (2 * NT), 0);
+      }
     }
-    if (rb + 1 < nrb) put(smem + (cur ^ 1) * L::bufBytes);
+    if (rb + 1 < nrb) form_put(smem + (cur ^ 1) * L::bufBytes);
     __syncthreads();
   }
 
