@@ -454,48 +454,61 @@ __global__ __launch_bounds__(256) void bwd_kv_kernel(
   // Formation of one row block: rows (2p, 2p+1), 8 columns per work item.
   // fetch() issues the global loads of the next row block before the current
   // one is computed; form_put() multiplies and stores them afterwards, so the
-  // load latency hides behind a whole row block of matrix work.
+  // load latency hides behind a whole row block of matrix work. Loads go
+  // through buffer resources over one head: a row outside [0, N) or outside
+  // the k-window gets offset -1, which the range check turns into zeros.
   constexpr int items = 16 * (D / 8);
   const int p_ = tid & 15, dc = tid >> 4;
-  const bool fitem = tid < items;
+  const bool fitem = items >= 256 || tid < items;  // all 256 threads at D = 128
+  const int rsb = static_cast<int>(rs) * 2;
+  const unsigned hb = head_bytes(N, rsb, D);
+  const __amdgpu_buffer_rsrc_t rsq = make_rsrc(q + base, hb), rso = make_rsrc(dout + base, hb);
+  const __amdgpu_buffer_rsrc_t rskp = make_rsrc(kp + base, hb), rsvp = make_rsrc(vp + base, hb);
   u32x4_t rq, ro, rk[2], rv[2];
   auto fetch = [&](int rb) {
-    const int i = j0 + rb / G, g = rb % G;
-    const u32x4_t z = {0u, 0u, 0u, 0u};
-    rq = z;
-    ro = z;
-    if (fitem) {
-      rq = ldg128(q + base + static_cast<size_t>(i) * rs + 8 * dc);
-      ro = ldg128(dout + base + static_cast<size_t>(i) * rs + 8 * dc);
-    }
+    const int i = j0 + rb / G, g = rb - (rb / G) * G;
+    const int qoff = fitem ? i * rsb + 16 * dc : -1;
+    rq = ldbuf128(rsq, qoff);
+    ro = ldbuf128(rso, qoff);
 #pragma unroll
     for (int y = 0; y < 2; ++y) {
       const int kk = i - W2P + 1 + 32 * g + 2 * p_ + y;
-      rk[y] = z;
-      rv[y] = z;
-      if (fitem && kk >= 0 && kk > i - w2) {
-        rk[y] = ldg128(kp + base + static_cast<size_t>(kk) * rs + 8 * dc);
-        rv[y] = ldg128(vp + base + static_cast<size_t>(kk) * rs + 8 * dc);
-      }
+      const int koff = fitem && kk > i - w2 ? kk * rsb + 16 * dc : -1;
+      rk[y] = ldbuf128(rskp, koff);
+      rv[y] = ldbuf128(rsvp, koff);
     }
   };
   // Row-major swizzled tiles: rows (2p, 2p+1), 16-byte chunk dc of each.
-  // Rows whose k is outside the window were fetched as zero, so q~ = do~ = 0.
+  // Rows whose k is outside the window were fetched as zero, so q~ = do~ = 0
+  // there and those rows add nothing to dK or dV whatever their P and dS.
   auto form_put = [&](char* buf) {
     if (!fitem) return;
+    float qlo[4], qhi[4], olo[4], ohi[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      qlo[e] = bf16_lo(rq[e]);
+      qhi[e] = bf16_hi(rq[e]);
+      olo[e] = bf16_lo(ro[e]);
+      ohi[e] = bf16_hi(ro[e]);
+    }
 #pragma unroll
     for (int y = 0; y < 2; ++y) {
       u32x4_t a4, b4;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        a4[e] = pack_bf16x2(bf16_lo(rq[e]) * bf16_lo(rk[y][e]) * qscale,
-                            bf16_hi(rq[e]) * bf16_hi(rk[y][e]) * qscale);
-        b4[e] = pack_bf16x2(bf16_lo(ro[e]) * bf16_lo(rv[y][e]), bf16_hi(ro[e]) * bf16_hi(rv[y][e]));
+        a4[e] = pack_bf16x2(qlo[e] * bf16_lo(rk[y][e]), qhi[e] * bf16_hi(rk[y][e]));
+        b4[e] = pack_bf16x2(olo[e] * bf16_lo(rv[y][e]), ohi[e] * bf16_hi(rv[y][e]));
       }
       *reinterpret_cast<u32x4_t*>(buf + T::off(2 * p_ + y, dc)) = a4;
       *reinterpret_cast<u32x4_t*>(buf + T::bytes + T::off(2 * p_ + y, dc)) = b4;
     }
   };
+
+  // Per-row-block statistics, 64 row blocks at a time: lane l holds
+  // -lse * log2(e) and Delta of row block (rb & ~63) + l; each iteration
+  // takes its pair with a lane read instead of a scalar load, which would
+  // share the LDS completion counter and serialise the fragment reads.
+  float st_l = 0.f, dl_l = 0.f;
 
   if (nrb > 0) {
     fetch(0);
@@ -504,79 +517,110 @@ __global__ __launch_bounds__(256) void bwd_kv_kernel(
   __syncthreads();
   for (int rb = 0; rb < nrb; ++rb) {
     const int cur = rb & 1;
-    if (rb + 1 < nrb) fetch(rb + 1);
-    const int i = j0 + rb / G, g = rb % G;
-    // this wavefront's keys see query i iff jw + 31 >= i - w1 + 1 and jw <= i
-    const bool act = jw <= i && jw + 31 > i - w1 && jw < N;
-    if (act) {
-      const char* qtile = smem + cur * L::bufBytes;
-      const char* otile = qtile + T::bytes;
-      // All operand reads of the row block are issued before the products
-      // that consume them, so LDS latency overlaps the matrix work.
-      u32x4_t qa[NT], oa[NT];
-#pragma unroll
-      for (int t = 0; t < NT; ++t) {
-        qa[t] = frag_row_swz<D>(qtile, c, h, t);
-        oa[t] = frag_row_swz<D>(otile, c, h, t);
-      }
-      u32x4_t otr[2][NDT], qtr[2][NDT];
-#pragma unroll
-      for (int u = 0; u < 2; ++u)
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) {
-          otr[u][dt] = frag_tr_swz<D>(otile, lane, dt, u);
-          qtr[u][dt] = frag_tr_swz<D>(qtile, lane, dt, u);
-        }
-      f32x16_t sacc = f32x16_t{}, pacc = f32x16_t{};
-#pragma unroll
-      for (int t = 0; t < NT; ++t) {
-        sacc = mfma32(qa[t], kf[t], sacc);
-        pacc = mfma32(oa[t], vf[t], pacc);
-      }
-      const float lse2 = lse[stat + i] * kLog2e;
-      const float dlt = delta[stat + i];
-      const bool colok = jme <= i && jme > i - w1 && jme < N;
-      u32x4_t pf[2], df[2];
-#pragma unroll
-      for (int vv = 0; vv < 16; vv += 2) {
-        float p2[2], d2[2];
-#pragma unroll
-        for (int x = 0; x < 2; ++x) {
-          const int r = acc_row(vv + x, h);
-          const int kk = i - W2P + 1 + 32 * g + r;
-          const bool ok = colok && kk >= 0 && kk > i - w2;
-          const float pr = ok ? fast_exp2(sacc[vv + x] - lse2) : 0.f;
-          p2[x] = pr;
-          d2[x] = pr * (pacc[vv + x] - dlt);
-        }
-        pf[vv >> 3][(vv & 7) >> 1] = pack_bf16x2(p2[0], p2[1]);
-        df[vv >> 3][(vv & 7) >> 1] = pack_bf16x2(d2[0], d2[1]);
-      }
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) {
-          adv[dt] = mfma32(pf[u], otr[u][dt], adv[dt]);
-          adk[dt] = mfma32(df[u], qtr[u][dt], adk[dt]);
-        }
-      }
-      // Schedule: the row-fragment reads first, then the logit/dP products
-      // with two transposing reads slipped in behind each, so the operands of
-      // the dV/dK products arrive while the first products and the softmax run.
-      __builtin_amdgcn_sched_group_barrier(0x100, 2 * NT, 0);
-#pragma unroll
-      for (int x = 0; x < 2 * NT; ++x) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 2 * 2 * NDT * 2 / (2 * NT), 0);
-      }
+    const int i = j0 + rb / G, g = rb - (rb / G) * G;
+    if ((rb & 63) == 0) {
+      const int ii = min(j0 + (rb + lane) / G, N - 1);
+      st_l = -lse[stat + ii] * kLog2e;
+      dl_l = delta[stat + ii];
     }
-    if (rb + 1 < nrb) form_put(smem + (cur ^ 1) * L::bufBytes);
-    __syncthreads();
+    // The last iteration fetches and forms one row block past the end: its
+    // loads are out of range (zeros) or harmless, and the buffer it fills is
+    // never read. This keeps the loop body free of branches around the work.
+    fetch(rb + 1);
+    // Keep the loads here, a whole row block ahead of their use.
+    __builtin_amdgcn_sched_barrier(0);
+    const float nl2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, st_l), rb & 63));
+    const float dlt = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, dl_l), rb & 63));
+    char* nbuf = smem + (cur ^ 1) * L::bufBytes;
+    // Every wavefront runs every row block: the workgroup advances in
+    // lockstep, so one whose keys miss query i's window would only wait at
+    // the barrier; its key columns are masked below and contribute zeros.
+    const char* qtile = smem + cur * L::bufBytes;
+    const char* otile = qtile + T::bytes;
+
+    // (1) Logits S = q~ K^T, with the transposing reads for dV queued behind.
+    u32x4_t qa[NT], oa[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) qa[t] = frag_row_swz<D>(qtile, c, h, t);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) oa[t] = frag_row_swz<D>(otile, c, h, t);
+    u32x4_t otr[2][NDT], qtr[2][NDT];
+    f32x16_t sacc = f32x16_t{}, pacc = f32x16_t{};
+#pragma unroll
+    for (int t = 0; t < NT; ++t) sacc = mfma32(qa[t], kf[t], sacc);
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) otr[u][dt] = frag_tr_swz<D>(otile, lane, dt, u);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * NT, 0);
+#pragma unroll
+    for (int x = 0; x < NT; ++x) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 4 * NDT / NT, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+
+    // (2) dP = do~ V^T, overlapped with the probabilities. Keys outside
+    // query i's window get an infinite log-normaliser, so their P (and dS)
+    // is exactly 0. Rows with k outside the window hold zero operands; their
+    // P is exp2(-lse2), finite unless the normaliser is tiny, so the
+    // exponent is clamped at 0 (valid probabilities never exceed 1).
+#pragma unroll
+    for (int t = 0; t < NT; ++t) pacc = mfma32(oa[t], vf[t], pacc);
+    const bool colok = jme <= i && jme > i - w1 && jme < N;
+    const float nlse2 = nl2 - (colok ? 0.f : __builtin_inff());
+    float pr[16];
+#pragma unroll
+    for (int vv = 0; vv < 16; ++vv) pr[vv] = fast_exp2(fminf(__builtin_fmaf(sacc[vv], qscale, nlse2), 0.f));
+    u32x4_t pf[2], df[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) pf[u] = pack_frag(pr, u);
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) qtr[u][dt] = frag_tr_swz<D>(qtile, lane, dt, u);
+#pragma unroll
+    for (int x = 0; x < NT; ++x) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 4 * NDT / NT, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+
+    // (3) dV += P^T do~, overlapped with dS = P (dP - Delta).
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) adv[dt] = mfma32(pf[u], otr[u][dt], adv[dt]);
+#pragma unroll
+    for (int vv = 0; vv < 16; ++vv) pr[vv] *= pacc[vv] - dlt;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) df[u] = pack_frag(pr, u);
+#pragma unroll
+    for (int x = 0; x < 2 * NDT; ++x) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+
+    // (4) dK += dS^T q~, overlapped with forming the next row block's tiles.
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) adk[dt] = mfma32(df[u], qtr[u][dt], adk[dt]);
+    form_put(nbuf);
+#pragma unroll
+    for (int x = 0; x < 2 * NDT; ++x) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 12, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    lds_barrier();
   }
 
   // ---- store: accumulator rows are keys, lanes are columns d ----
   float* ob = reinterpret_cast<float*>(smem) + wave * 32 * L::oStride;
-  const float kscale = 1.0f / kLog2e;  // q~ carried scale * log2(e); dK needs scale only
+  const float kscale = s.scale;  // q~ = q * k' is formed unscaled
 #pragma unroll
   for (int pass = 0; pass < 2; ++pass) {
 #pragma unroll
