@@ -90,7 +90,14 @@ struct BwdQLds {
   static constexpr int redWaves = 2;                // dq column sums, two wavefronts a round
   static constexpr int redOff = NS * stageBytes;
   static constexpr int accOff = redOff + redWaves * 32 * rStride * 4;
-  static constexpr int bytes = accOff + 2 * RB * rStride * 4;
+  // raw bf16 operands of the tile epilogue, kept from the tile prologue:
+  // q_i and dO_i of each wavefront and, where LDS has room, k' of its 32 rows
+  // (rows padded by 16 bytes); otherwise the epilogue reloads k' from memory
+  static constexpr int rowOff = accOff + 2 * RB * rStride * 4;
+  static constexpr int stashOff = rowOff + WAVES * 2 * 2 * D;
+  static constexpr int kStride = 2 * D + 16;
+  static constexpr bool kStash = stashOff + WAVES * 32 * kStride <= 160 * 1024;
+  static constexpr int bytes = stashOff + (kStash ? WAVES * 32 * kStride : 0);
 };
 
 template <int D, int G, int WAVES, int NS>
@@ -189,6 +196,9 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
   float lse2 = 0.f, dlt = 0.f;
   int i = 0, kk = 0;
   bool rowvalid = false, qvalid = false;
+  char* kstash = smem + L::stashOff + wave * 32 * L::kStride;
+  char* qrow = smem + L::rowOff + wave * 4 * D;
+  char* orow = qrow + 2 * D;
 
   for (int it = 0; it < total_it; ++it) {
     const int tile = it / nb, blk = it - tile * nb;
@@ -203,10 +213,13 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
         u32x4_t a4 = {0u, 0u, 0u, 0u}, b4 = {0u, 0u, 0u, 0u};
+        u32x4_t qa = a4, ka = a4, oa = a4;
+        if (qvalid) {
+          qa = ldg128(q + base + static_cast<size_t>(i) * rs + 16 * t + 8 * h);
+          oa = ldg128(dout + base + static_cast<size_t>(i) * rs + 16 * t + 8 * h);
+        }
         if (rowvalid) {
-          const u32x4_t qa = ldg128(q + base + static_cast<size_t>(i) * rs + 16 * t + 8 * h);
-          const u32x4_t ka = ldg128(kp + base + static_cast<size_t>(kk) * rs + 16 * t + 8 * h);
-          const u32x4_t oa = ldg128(dout + base + static_cast<size_t>(i) * rs + 16 * t + 8 * h);
+          ka = ldg128(kp + base + static_cast<size_t>(kk) * rs + 16 * t + 8 * h);
           const u32x4_t va = ldg128(vp + base + static_cast<size_t>(kk) * rs + 16 * t + 8 * h);
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
@@ -217,8 +230,16 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
         }
         qt[t] = a4;
         ot[t] = b4;
+        // The previous tile's epilogue finished reading the stash before its
+        // last barrier.
+        if constexpr (L::kStash) *reinterpret_cast<u32x4_t*>(kstash + c * L::kStride + 32 * t + 16 * h) = ka;
+        if (c == 0) {
+          *reinterpret_cast<u32x4_t*>(qrow + 32 * t + 16 * h) = qa;
+          *reinterpret_cast<u32x4_t*>(orow + 32 * t + 16 * h) = oa;
+        }
       }
-      lse2 = qvalid ? lse[stat + i] * kLog2e : 0.f;
+      // Rows outside the window get an infinite normaliser: P = dS = 0.
+      lse2 = rowvalid ? lse[stat + i] * kLog2e : __builtin_inff();
       dlt = qvalid ? delta[stat + i] : 0.f;
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt) {
@@ -231,41 +252,93 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
     else wait_vmem<0>();
     lds_barrier();
     if (it + NS - 1 < total_it) issue(it + NS - 1);
+    __builtin_amdgcn_sched_barrier(0);
     const char* kt = smem + (it % NS) * L::stageBytes;
     const char* vt = kt + T::bytes;
-
+    // Keys of this block inside query i's window and inside [0, N).
     const int lo = max(qs, -jlo) - 32 * blk;
     const int hi = min(qs + w1 - 1, N - 1 - jlo) - 32 * blk;
-    if (qvalid && hi >= 0 && lo <= 31 && lo <= hi) {
-      f32x16_t sacc = f32x16_t{}, pacc = f32x16_t{};
+    const bool edge = lo > 0 || hi < 31;
+
+    // Operand reads run one section ahead of the products that use them.
+    // (1) S^T = K q~^T, with the V row fragments read behind it.
+    u32x4_t ka[NT], va[NT], ktr[2][NDT], vtr[2][NDT];
 #pragma unroll
-      for (int t = 0; t < NT; ++t) sacc = mfma32(frag_row_swz<D>(kt, c, h, t), qt[t], sacc);
+    for (int t = 0; t < NT; ++t) ka[t] = frag_row_swz<D>(kt, c, h, t);
+    f32x16_t sacc = f32x16_t{}, pacc = f32x16_t{};
 #pragma unroll
-      for (int t = 0; t < NT; ++t) pacc = mfma32(frag_row_swz<D>(vt, c, h, t), ot[t], pacc);
-      u32x4_t pf[2], df[2];
+    for (int t = 0; t < NT; ++t) sacc = mfma32(ka[t], qt[t], sacc);
 #pragma unroll
-      for (int vv = 0; vv < 16; vv += 2) {
-        float p2[2], d2[2];
+    for (int t = 0; t < NT; ++t) va[t] = frag_row_swz<D>(vt, c, h, t);
+    __builtin_amdgcn_sched_group_barrier(0x100, NT, 0);
 #pragma unroll
-        for (int x = 0; x < 2; ++x) {
-          const int jl = acc_row(vv + x, h);
-          const bool ok = rowvalid && jl >= lo && jl <= hi;
-          const float pr = ok ? fast_exp2(sacc[vv + x] - lse2) : 0.f;
-          p2[x] = pr;
-          d2[x] = pr * (pacc[vv + x] - dlt);
-        }
-        pf[vv >> 3][(vv & 7) >> 1] = pack_bf16x2(p2[0], p2[1]);
-        df[vv >> 3][(vv & 7) >> 1] = pack_bf16x2(d2[0], d2[1]);
-      }
+    for (int x = 0; x < NT; ++x) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+
+    // (2) dP^T = V do~^T, overlapped with the probabilities; the transposed
+    // V fragments are read behind it.
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
+    for (int t = 0; t < NT; ++t) pacc = mfma32(va[t], ot[t], pacc);
+    float pr[16];
 #pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) {
-          adq[dt] = mfma32(frag_tr_swz<D>(kt, lane, dt, u), df[u], adq[dt]);
-          au[dt] = mfma32(frag_tr_swz<D>(vt, lane, dt, u), pf[u], au[dt]);
-        }
+    for (int vv = 0; vv < 16; ++vv) pr[vv] = fast_exp2(sacc[vv] - lse2);
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) vtr[u][dt] = frag_tr_swz<D>(vt, lane, dt, u);
+#pragma unroll
+    for (int x = 0; x < NT; ++x) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 4 * NDT / NT, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    // Blocks at the ends of the window (and of the sequence) mask their keys;
+    // the empty asm keeps this a branch rather than selects on every block.
+    if (edge) {
+      asm volatile("" ::: "memory");
+#pragma unroll
+      for (int vv = 0; vv < 16; ++vv) {
+        const int jl = acc_row(vv, h);
+        pr[vv] = jl >= lo && jl <= hi ? pr[vv] : 0.f;
       }
     }
+    u32x4_t pf[2], df[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) pf[u] = pack_frag(pr, u);
+    __builtin_amdgcn_sched_barrier(0);
+
+    // (3) U~^T += V^T P^T, overlapped with dS = P (dP - Delta); the
+    // transposed K fragments are read behind it.
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) au[dt] = mfma32(vtr[u][dt], pf[u], au[dt]);
+#pragma unroll
+    for (int vv = 0; vv < 16; ++vv) pr[vv] *= pacc[vv] - dlt;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) df[u] = pack_frag(pr, u);
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) ktr[u][dt] = frag_tr_swz<D>(kt, lane, dt, u);
+#pragma unroll
+    for (int x = 0; x < 2 * NDT; ++x) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+
+    // (4) dQ~^T += K^T dS^T.
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) adq[dt] = mfma32(ktr[u][dt], df[u], adq[dt]);
+    __builtin_amdgcn_sched_barrier(0);
 
     if (blk == nb - 1) {
       // ---- tile epilogue ----
@@ -281,8 +354,13 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
 #pragma unroll
             for (int qd = 0; qd < 4; ++qd) {
               const int d = 32 * dt + 8 * qd + 4 * h;
-              u32x2_t kv = {0u, 0u};
-              if (rowvalid) kv = *reinterpret_cast<const u32x2_t*>(kp + base + static_cast<size_t>(kk) * rs + d);
+              u32x2_t kv;
+              if constexpr (L::kStash) {
+                kv = *reinterpret_cast<const u32x2_t*>(kstash + c * L::kStride + 2 * d);
+              } else {
+                kv = u32x2_t{0u, 0u};
+                if (rowvalid) kv = *reinterpret_cast<const u32x2_t*>(kp + base + static_cast<size_t>(kk) * rs + d);
+              }
               float4 val;
               val.x = bf16_lo(kv[0]) * adq[dt][4 * qd + 0];
               val.y = bf16_hi(kv[0]) * adq[dt][4 * qd + 1];
@@ -315,6 +393,23 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
       }
 
       // dk'/dv' contributions into the ring, one wavefront at a time.
+      float qs_[4 * NDT][4], os_[4 * NDT][4];
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+        for (int qd = 0; qd < 4; ++qd) {
+          const int d = 32 * dt + 8 * qd + 4 * h;
+          const u32x2_t qv = *reinterpret_cast<const u32x2_t*>(qrow + 2 * d);
+          const u32x2_t ov = *reinterpret_cast<const u32x2_t*>(orow + 2 * d);
+          qs_[4 * dt + qd][0] = s.scale * bf16_lo(qv[0]);
+          qs_[4 * dt + qd][1] = s.scale * bf16_hi(qv[0]);
+          qs_[4 * dt + qd][2] = s.scale * bf16_lo(qv[1]);
+          qs_[4 * dt + qd][3] = s.scale * bf16_hi(qv[1]);
+          os_[4 * dt + qd][0] = bf16_lo(ov[0]);
+          os_[4 * dt + qd][1] = bf16_hi(ov[0]);
+          os_[4 * dt + qd][2] = bf16_lo(ov[1]);
+          os_[4 * dt + qd][3] = bf16_hi(ov[1]);
+        }
       for (int ww = 0; ww < WAVES; ++ww) {
         if (wave == ww && rowvalid) {
           const int slot = (kk - kbase) % RB;
@@ -323,19 +418,17 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
 #pragma unroll
             for (int qd = 0; qd < 4; ++qd) {
               const int d = 32 * dt + 8 * qd + 4 * h;
-              const u32x2_t qv = *reinterpret_cast<const u32x2_t*>(q + base + static_cast<size_t>(i) * rs + d);
-              const u32x2_t ov = *reinterpret_cast<const u32x2_t*>(dout + base + static_cast<size_t>(i) * rs + d);
               float4* a = reinterpret_cast<float4*>(ring_kp + slot * L::rStride + d);
               float4* bb = reinterpret_cast<float4*>(ring_vp + slot * L::rStride + d);
               float4 x = *a, y = *bb;
-              x.x += s.scale * bf16_lo(qv[0]) * adq[dt][4 * qd + 0];
-              x.y += s.scale * bf16_hi(qv[0]) * adq[dt][4 * qd + 1];
-              x.z += s.scale * bf16_lo(qv[1]) * adq[dt][4 * qd + 2];
-              x.w += s.scale * bf16_hi(qv[1]) * adq[dt][4 * qd + 3];
-              y.x += bf16_lo(ov[0]) * au[dt][4 * qd + 0];
-              y.y += bf16_hi(ov[0]) * au[dt][4 * qd + 1];
-              y.z += bf16_lo(ov[1]) * au[dt][4 * qd + 2];
-              y.w += bf16_hi(ov[1]) * au[dt][4 * qd + 3];
+              x.x += qs_[4 * dt + qd][0] * adq[dt][4 * qd + 0];
+              x.y += qs_[4 * dt + qd][1] * adq[dt][4 * qd + 1];
+              x.z += qs_[4 * dt + qd][2] * adq[dt][4 * qd + 2];
+              x.w += qs_[4 * dt + qd][3] * adq[dt][4 * qd + 3];
+              y.x += os_[4 * dt + qd][0] * au[dt][4 * qd + 0];
+              y.y += os_[4 * dt + qd][1] * au[dt][4 * qd + 1];
+              y.z += os_[4 * dt + qd][2] * au[dt][4 * qd + 2];
+              y.w += os_[4 * dt + qd][3] * au[dt][4 * qd + 3];
               *a = x;
               *bb = y;
             }
