@@ -200,175 +200,207 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
   char* qrow = smem + L::rowOff + wave * 4 * D;
   char* orow = qrow + 2 * D;
 
-  for (int it = 0; it < total_it; ++it) {
-    const int tile = it / nb, blk = it - tile * nb;
+  // Raw rows of a tile (q_i, dO_i and k'_k, v'_k of this lane's row),
+  // loaded one tile ahead: the next tile's loads are issued at the start of
+  // the current tile's epilogue. Rows outside [0, N) or the window come back
+  // as zeros from the buffer range check (offset -1).
+  const unsigned hb = head_bytes(N, rsb, D);
+  const __amdgpu_buffer_rsrc_t rq = make_rsrc(q + base, hb), ro = make_rsrc(dout + base, hb);
+  const __amdgpu_buffer_rsrc_t rkp = make_rsrc(kp + base, hb), rvp = make_rsrc(vp + base, hb);
+  u32x4_t nq[NT], nk[NT], no[NT], nv[NT];
+  float nlse = 0.f, ndlt = 0.f;
+  int ni = 0, nkk = 0;
+  auto load_rows = [&](int tile) {
+    ni = cs + tile * QW + qs;
+    nkk = ni - W2P + 1 + 32 * g + c;
+    const bool qv = ni < ce, rv = qv && nkk > ni - w2;
+    const int qo = qv ? ni * rsb + 16 * h : -1;
+    const int ko = rv ? nkk * rsb + 16 * h : -1;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      nq[t] = ldbuf128(rq, qo < 0 ? -1 : qo + 32 * t);
+      no[t] = ldbuf128(ro, qo < 0 ? -1 : qo + 32 * t);
+      nk[t] = ldbuf128(rkp, ko < 0 ? -1 : ko + 32 * t);
+      nv[t] = ldbuf128(rvp, ko < 0 ? -1 : ko + 32 * t);
+    }
+    const int si = min(ni, N - 1);
+    nlse = lse[stat + si];
+    ndlt = delta[stat + si];
+  };
+  if (total_it > 0) load_rows(0);
+
+  int it = 0;
+  for (int tile = 0; tile < ntiles; ++tile) {
     const int i0 = cs + tile * QW;
-    const int jlo = i0 - w1 + 1;
-    if (blk == 0) {
+    {
       // ---- tile prologue: modulated operands of this wavefront's 32 rows ----
-      i = i0 + qs;
-      kk = i - W2P + 1 + 32 * g + c;
+      i = ni;
+      kk = nkk;
       qvalid = i < ce;
       rowvalid = qvalid && kk >= 0 && kk > i - w2;
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        u32x4_t a4 = {0u, 0u, 0u, 0u}, b4 = {0u, 0u, 0u, 0u};
-        u32x4_t qa = a4, ka = a4, oa = a4;
-        if (qvalid) {
-          qa = ldg128(q + base + static_cast<size_t>(i) * rs + 16 * t + 8 * h);
-          oa = ldg128(dout + base + static_cast<size_t>(i) * rs + 16 * t + 8 * h);
-        }
-        if (rowvalid) {
-          ka = ldg128(kp + base + static_cast<size_t>(kk) * rs + 16 * t + 8 * h);
-          const u32x4_t va = ldg128(vp + base + static_cast<size_t>(kk) * rs + 16 * t + 8 * h);
+        u32x4_t a4, b4;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            a4[e] = pack_bf16x2(bf16_lo(qa[e]) * bf16_lo(ka[e]) * qscale,
-                                bf16_hi(qa[e]) * bf16_hi(ka[e]) * qscale);
-            b4[e] = pack_bf16x2(bf16_lo(oa[e]) * bf16_lo(va[e]), bf16_hi(oa[e]) * bf16_hi(va[e]));
-          }
+        for (int e = 0; e < 4; ++e) {
+          a4[e] = pack_bf16x2(bf16_lo(nq[t][e]) * bf16_lo(nk[t][e]) * qscale,
+                              bf16_hi(nq[t][e]) * bf16_hi(nk[t][e]) * qscale);
+          b4[e] = pack_bf16x2(bf16_lo(no[t][e]) * bf16_lo(nv[t][e]), bf16_hi(no[t][e]) * bf16_hi(nv[t][e]));
         }
         qt[t] = a4;
         ot[t] = b4;
         // The previous tile's epilogue finished reading the stash before its
         // last barrier.
-        if constexpr (L::kStash) *reinterpret_cast<u32x4_t*>(kstash + c * L::kStride + 32 * t + 16 * h) = ka;
+        if constexpr (L::kStash) *reinterpret_cast<u32x4_t*>(kstash + c * L::kStride + 32 * t + 16 * h) = nk[t];
         if (c == 0) {
-          *reinterpret_cast<u32x4_t*>(qrow + 32 * t + 16 * h) = qa;
-          *reinterpret_cast<u32x4_t*>(orow + 32 * t + 16 * h) = oa;
+          *reinterpret_cast<u32x4_t*>(qrow + 32 * t + 16 * h) = nq[t];
+          *reinterpret_cast<u32x4_t*>(orow + 32 * t + 16 * h) = no[t];
         }
       }
       // Rows outside the window get an infinite normaliser: P = dS = 0.
-      lse2 = rowvalid ? lse[stat + i] * kLog2e : __builtin_inff();
-      dlt = qvalid ? delta[stat + i] : 0.f;
+      lse2 = rowvalid ? nlse * kLog2e : __builtin_inff();
+      dlt = qvalid ? ndlt : 0.f;
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt) {
         adq[dt] = f32x16_t{};
         au[dt] = f32x16_t{};
       }
     }
+    for (int blk = 0; blk < nb; ++blk, ++it) {
+      const int jlo = i0 - w1 + 1;
 
-    if (it + NS - 2 < total_it) wait_vmem<LPB * (NS - 2)>();
-    else wait_vmem<0>();
-    lds_barrier();
-    if (it + NS - 1 < total_it) issue(it + NS - 1);
-    __builtin_amdgcn_sched_barrier(0);
-    const char* kt = smem + (it % NS) * L::stageBytes;
-    const char* vt = kt + T::bytes;
-    // Keys of this block inside query i's window and inside [0, N).
-    const int lo = max(qs, -jlo) - 32 * blk;
-    const int hi = min(qs + w1 - 1, N - 1 - jlo) - 32 * blk;
-    const bool edge = lo > 0 || hi < 31;
+      if (it + NS - 2 < total_it) wait_vmem<LPB * (NS - 2)>();
+      else wait_vmem<0>();
+      lds_barrier();
+      if (it + NS - 1 < total_it) issue(it + NS - 1);
+      __builtin_amdgcn_sched_barrier(0);
+      const char* kt = smem + (it % NS) * L::stageBytes;
+      const char* vt = kt + T::bytes;
+      // Keys of this block inside query i's window and inside [0, N).
+      const int lo = max(qs, -jlo) - 32 * blk;
+      const int hi = min(qs + w1 - 1, N - 1 - jlo) - 32 * blk;
+      const bool edge = lo > 0 || hi < 31;
 
-    // Operand reads run one section ahead of the products that use them.
-    // (1) S^T = K q~^T, with the V row fragments read behind it.
-    u32x4_t ka[NT], va[NT], ktr[2][NDT], vtr[2][NDT];
+      // Operand reads run one section ahead of the products that use them.
+      // (1) S^T = K q~^T, with the V row fragments read behind it.
+      u32x4_t ka[NT], va[NT], ktr[2][NDT], vtr[2][NDT];
 #pragma unroll
-    for (int t = 0; t < NT; ++t) ka[t] = frag_row_swz<D>(kt, c, h, t);
-    f32x16_t sacc = f32x16_t{}, pacc = f32x16_t{};
+      for (int t = 0; t < NT; ++t) ka[t] = frag_row_swz<D>(kt, c, h, t);
+      f32x16_t sacc = f32x16_t{}, pacc = f32x16_t{};
 #pragma unroll
-    for (int t = 0; t < NT; ++t) sacc = mfma32(ka[t], qt[t], sacc);
+      for (int t = 0; t < NT; ++t) sacc = mfma32(ka[t], qt[t], sacc);
 #pragma unroll
-    for (int t = 0; t < NT; ++t) va[t] = frag_row_swz<D>(vt, c, h, t);
-    __builtin_amdgcn_sched_group_barrier(0x100, NT, 0);
+      for (int t = 0; t < NT; ++t) va[t] = frag_row_swz<D>(vt, c, h, t);
+      __builtin_amdgcn_sched_group_barrier(0x100, NT, 0);
 #pragma unroll
-    for (int x = 0; x < NT; ++x) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-
-    // (2) dP^T = V do~^T, overlapped with the probabilities; the transposed
-    // V fragments are read behind it.
-#pragma unroll
-    for (int t = 0; t < NT; ++t) pacc = mfma32(va[t], ot[t], pacc);
-    float pr[16];
-#pragma unroll
-    for (int vv = 0; vv < 16; ++vv) pr[vv] = fast_exp2(sacc[vv] - lse2);
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) vtr[u][dt] = frag_tr_swz<D>(vt, lane, dt, u);
-#pragma unroll
-    for (int x = 0; x < NT; ++x) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 4 * NDT / NT, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    // Blocks at the ends of the window (and of the sequence) mask their keys;
-    // the empty asm keeps this a branch rather than selects on every block.
-    if (edge) {
-      asm volatile("" ::: "memory");
-#pragma unroll
-      for (int vv = 0; vv < 16; ++vv) {
-        const int jl = acc_row(vv, h);
-        pr[vv] = jl >= lo && jl <= hi ? pr[vv] : 0.f;
+      for (int x = 0; x < NT; ++x) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       }
+      __builtin_amdgcn_sched_barrier(0);
+
+      // (2) dP^T = V do~^T, overlapped with the probabilities; the transposed
+      // V fragments are read behind it.
+#pragma unroll
+      for (int t = 0; t < NT; ++t) pacc = mfma32(va[t], ot[t], pacc);
+      float pr[16];
+#pragma unroll
+      for (int vv = 0; vv < 16; ++vv) pr[vv] = fast_exp2(sacc[vv] - lse2);
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) vtr[u][dt] = frag_tr_swz<D>(vt, lane, dt, u);
+#pragma unroll
+      for (int x = 0; x < NT; ++x) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 4 * NDT / NT, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      // Blocks at the ends of the window (and of the sequence) mask their keys;
+      // the empty asm keeps this a branch rather than selects on every block.
+      if (edge) {
+        asm volatile("" ::: "memory");
+#pragma unroll
+        for (int vv = 0; vv < 16; ++vv) {
+          const int jl = acc_row(vv, h);
+          pr[vv] = jl >= lo && jl <= hi ? pr[vv] : 0.f;
+        }
+      }
+      u32x4_t pf[2], df[2];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) pf[u] = pack_frag(pr, u);
+      __builtin_amdgcn_sched_barrier(0);
+
+      // (3) U~^T += V^T P^T, overlapped with dS = P (dP - Delta); the
+      // transposed K fragments are read behind it.
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) au[dt] = mfma32(vtr[u][dt], pf[u], au[dt]);
+#pragma unroll
+      for (int vv = 0; vv < 16; ++vv) pr[vv] *= pacc[vv] - dlt;
+#pragma unroll
+      for (int u = 0; u < 2; ++u) df[u] = pack_frag(pr, u);
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) ktr[u][dt] = frag_tr_swz<D>(kt, lane, dt, u);
+#pragma unroll
+      for (int x = 0; x < 2 * NDT; ++x) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+
+      // (4) dQ~^T += K^T dS^T.
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) adq[dt] = mfma32(ktr[u][dt], df[u], adq[dt]);
+      __builtin_amdgcn_sched_barrier(0);
+
     }
-    u32x4_t pf[2], df[2];
-#pragma unroll
-    for (int u = 0; u < 2; ++u) pf[u] = pack_frag(pr, u);
-    __builtin_amdgcn_sched_barrier(0);
-
-    // (3) U~^T += V^T P^T, overlapped with dS = P (dP - Delta); the
-    // transposed K fragments are read behind it.
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) au[dt] = mfma32(vtr[u][dt], pf[u], au[dt]);
-#pragma unroll
-    for (int vv = 0; vv < 16; ++vv) pr[vv] *= pacc[vv] - dlt;
-#pragma unroll
-    for (int u = 0; u < 2; ++u) df[u] = pack_frag(pr, u);
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) ktr[u][dt] = frag_tr_swz<D>(kt, lane, dt, u);
-#pragma unroll
-    for (int x = 0; x < 2 * NDT; ++x) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-
-    // (4) dQ~^T += K^T dS^T.
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) adq[dt] = mfma32(ktr[u][dt], df[u], adq[dt]);
-    __builtin_amdgcn_sched_barrier(0);
-
-    if (blk == nb - 1) {
+    {
       // ---- tile epilogue ----
+      if (tile + 1 < ntiles) load_rows(tile + 1);
       // dq_i = scale * sum_k k'_k o dQ~_(i,k): column sums over the k-rows.
       // accumulator layout: lane holds row c, d = 32 dt + 8 (v/4) + 4 h + v%4
+      // Every loop below issues all of its LDS reads before the arithmetic
+      // and the writes, so each pays the LDS latency once.
 #pragma unroll
       for (int round = 0; round < WAVES / L::redWaves; ++round) {
         const bool mine = wave / L::redWaves == round;
         if (mine) {
           float* rw = red + (wave % L::redWaves) * 32 * L::rStride;
+          u32x2_t kv[4 * NDT];
 #pragma unroll
-          for (int dt = 0; dt < NDT; ++dt) {
+          for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
             for (int qd = 0; qd < 4; ++qd) {
               const int d = 32 * dt + 8 * qd + 4 * h;
-              u32x2_t kv;
               if constexpr (L::kStash) {
-                kv = *reinterpret_cast<const u32x2_t*>(kstash + c * L::kStride + 2 * d);
+                kv[4 * dt + qd] = *reinterpret_cast<const u32x2_t*>(kstash + c * L::kStride + 2 * d);
               } else {
-                kv = u32x2_t{0u, 0u};
-                if (rowvalid) kv = *reinterpret_cast<const u32x2_t*>(kp + base + static_cast<size_t>(kk) * rs + d);
+                kv[4 * dt + qd] = u32x2_t{0u, 0u};
+                if (rowvalid)
+                  kv[4 * dt + qd] = *reinterpret_cast<const u32x2_t*>(kp + base + static_cast<size_t>(kk) * rs + d);
               }
+            }
+#pragma unroll
+          for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+            for (int qd = 0; qd < 4; ++qd) {
+              const int d = 32 * dt + 8 * qd + 4 * h;
+              const u32x2_t x = kv[4 * dt + qd];
               float4 val;
-              val.x = bf16_lo(kv[0]) * adq[dt][4 * qd + 0];
-              val.y = bf16_hi(kv[0]) * adq[dt][4 * qd + 1];
-              val.z = bf16_lo(kv[1]) * adq[dt][4 * qd + 2];
-              val.w = bf16_hi(kv[1]) * adq[dt][4 * qd + 3];
+              val.x = bf16_lo(x[0]) * adq[dt][4 * qd + 0];
+              val.y = bf16_hi(x[0]) * adq[dt][4 * qd + 1];
+              val.z = bf16_lo(x[1]) * adq[dt][4 * qd + 2];
+              val.w = bf16_hi(x[1]) * adq[dt][4 * qd + 3];
               *reinterpret_cast<float4*>(rw + c * L::rStride + d) = val;
             }
-          }
         }
         lds_barrier();
         // the G wavefronts of a query split its D columns
@@ -379,11 +411,13 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
 #pragma unroll
           for (int gg = 0; gg < G; ++gg) {
             const float* rw = red + ((wave - g + gg) % L::redWaves) * 32 * L::rStride + c0 + 2 * lane;
-#pragma unroll 8
+            float2 xs[32];
+#pragma unroll
+            for (int rr = 0; rr < 32; ++rr) xs[rr] = *reinterpret_cast<const float2*>(rw + rr * L::rStride);
+#pragma unroll
             for (int rr = 0; rr < 32; ++rr) {
-              const float2 x = *reinterpret_cast<const float2*>(rw + rr * L::rStride);
-              o0 += x.x;
-              o1 += x.y;
+              o0 += xs[rr].x;
+              o1 += xs[rr].y;
             }
           }
           *reinterpret_cast<unsigned*>(dq + base + static_cast<size_t>(i) * rs + c0 + 2 * lane) =
@@ -392,46 +426,43 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
         lds_barrier();
       }
 
-      // dk'/dv' contributions into the ring, one wavefront at a time.
-      float qs_[4 * NDT][4], os_[4 * NDT][4];
+      // dk'/dv' contributions into the ring, one wavefront at a time (a
+      // fixed order, so the sums are deterministic).
+      u32x2_t qv[4 * NDT], ov[4 * NDT];
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
         for (int qd = 0; qd < 4; ++qd) {
           const int d = 32 * dt + 8 * qd + 4 * h;
-          const u32x2_t qv = *reinterpret_cast<const u32x2_t*>(qrow + 2 * d);
-          const u32x2_t ov = *reinterpret_cast<const u32x2_t*>(orow + 2 * d);
-          qs_[4 * dt + qd][0] = s.scale * bf16_lo(qv[0]);
-          qs_[4 * dt + qd][1] = s.scale * bf16_hi(qv[0]);
-          qs_[4 * dt + qd][2] = s.scale * bf16_lo(qv[1]);
-          qs_[4 * dt + qd][3] = s.scale * bf16_hi(qv[1]);
-          os_[4 * dt + qd][0] = bf16_lo(ov[0]);
-          os_[4 * dt + qd][1] = bf16_hi(ov[0]);
-          os_[4 * dt + qd][2] = bf16_lo(ov[1]);
-          os_[4 * dt + qd][3] = bf16_hi(ov[1]);
+          qv[4 * dt + qd] = *reinterpret_cast<const u32x2_t*>(qrow + 2 * d);
+          ov[4 * dt + qd] = *reinterpret_cast<const u32x2_t*>(orow + 2 * d);
         }
       for (int ww = 0; ww < WAVES; ++ww) {
         if (wave == ww && rowvalid) {
           const int slot = (kk - kbase) % RB;
 #pragma unroll
-          for (int dt = 0; dt < NDT; ++dt) {
+          for (int pass = 0; pass < 2; ++pass) {
+            float* rowp = (pass == 0 ? ring_kp : ring_vp) + slot * L::rStride;
+            float4 xa[4 * NDT];
 #pragma unroll
-            for (int qd = 0; qd < 4; ++qd) {
-              const int d = 32 * dt + 8 * qd + 4 * h;
-              float4* a = reinterpret_cast<float4*>(ring_kp + slot * L::rStride + d);
-              float4* bb = reinterpret_cast<float4*>(ring_vp + slot * L::rStride + d);
-              float4 x = *a, y = *bb;
-              x.x += qs_[4 * dt + qd][0] * adq[dt][4 * qd + 0];
-              x.y += qs_[4 * dt + qd][1] * adq[dt][4 * qd + 1];
-              x.z += qs_[4 * dt + qd][2] * adq[dt][4 * qd + 2];
-              x.w += qs_[4 * dt + qd][3] * adq[dt][4 * qd + 3];
-              y.x += os_[4 * dt + qd][0] * au[dt][4 * qd + 0];
-              y.y += os_[4 * dt + qd][1] * au[dt][4 * qd + 1];
-              y.z += os_[4 * dt + qd][2] * au[dt][4 * qd + 2];
-              y.w += os_[4 * dt + qd][3] * au[dt][4 * qd + 3];
-              *a = x;
-              *bb = y;
-            }
+            for (int j = 0; j < 4 * NDT; ++j)
+              xa[j] = *reinterpret_cast<const float4*>(rowp + 32 * (j / 4) + 8 * (j % 4) + 4 * h);
+#pragma unroll
+            for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+              for (int qd = 0; qd < 4; ++qd) {
+                const int j = 4 * dt + qd;
+                const u32x2_t m = pass == 0 ? qv[j] : ov[j];
+                const float f = pass == 0 ? s.scale : 1.f;
+                const f32x16_t& ac = pass == 0 ? adq[dt] : au[dt];
+                xa[j].x += f * bf16_lo(m[0]) * ac[4 * qd + 0];
+                xa[j].y += f * bf16_hi(m[0]) * ac[4 * qd + 1];
+                xa[j].z += f * bf16_lo(m[1]) * ac[4 * qd + 2];
+                xa[j].w += f * bf16_hi(m[1]) * ac[4 * qd + 3];
+              }
+#pragma unroll
+            for (int j = 0; j < 4 * NDT; ++j)
+              *reinterpret_cast<float4*>(rowp + 32 * (j / 4) + 8 * (j % 4) + 4 * h) = xa[j];
           }
         }
         lds_barrier();
