@@ -87,9 +87,11 @@ struct BwdQLds {
   static constexpr int rStride = D + 4;             // fp32 rows of the reductions
   static constexpr int QW = WAVES / G;
   static constexpr int RB = 32 * G + QW;            // rows of the dk'/dv' ring
-  static constexpr int redWaves = 2;                // dq column sums, two wavefronts a round
+  // dq column sums: every wavefront stages its 32 rows x 64 columns at once
+  static constexpr int redCols = D < 64 ? D : 64;
+  static constexpr int cStride = redCols + 4;
   static constexpr int redOff = NS * stageBytes;
-  static constexpr int accOff = redOff + redWaves * 32 * rStride * 4;
+  static constexpr int accOff = redOff + WAVES * 32 * cStride * 4;
   // raw bf16 operands of the tile epilogue, kept from the tile prologue:
   // q_i and dO_i of each wavefront and, where LDS has room, k' of its 32 rows
   // (rows padded by 16 bytes); otherwise the epilogue reloads k' from memory
@@ -113,8 +115,7 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
   using L = BwdQLds<D, G, WAVES, NS>;
   using T = typename L::T;
   constexpr int QW = L::QW, RB = L::RB;
-  constexpr int LPB = 2 * ((T::instrs + WAVES - 1) / WAVES);  // loads per wavefront per block
-  static_assert(WAVES % L::redWaves == 0 && L::redWaves % G == 0, "reduction rounds");
+  static_assert(WAVES % G == 0 && (L::redCols / G) <= 64 && D % L::redCols == 0, "reduction rounds");
   __shared__ __attribute__((aligned(16))) char smem[L::bytes];
   float* red = reinterpret_cast<float*>(smem + L::redOff);
   float* ring_kp = reinterpret_cast<float*>(smem + L::accOff);
@@ -179,17 +180,42 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
   const int nb = (w1 + QW - 1 + 31) / 32;
   const int ntiles = (ce - cs + QW - 1) / QW;
   const int total_it = ntiles * nb;
-  auto issue = [&](int it) {
+  // K/V blocks are staged through registers: stage_fetch loads this
+  // wavefront's share of block `it` (16 bytes per lane per load, the chunk
+  // that belongs at LDS offset 1024 k + 16 lane of the swizzled tile), and
+  // stage_put writes it into a ring stage one block later. Rows outside
+  // [0, N) come back as zeros from the buffer range check.
+  constexpr int SPW = (T::instrs + WAVES - 1) / WAVES;  // loads per tile per wavefront
+  u32x4_t skr[SPW], svr[SPW];
+  auto stage_fetch = [&](int it) {
     const int tile = it / nb, blk = it - tile * nb;
     const int jb = cs + tile * QW - w1 + 1 + 32 * blk;
-    char* st = smem + (it % NS) * L::stageBytes;
-    tile_load_lds<D, WAVES>(rk, rsb, jb, st, wave, lane);
-    tile_load_lds<D, WAVES>(rv, rsb, jb, st + T::bytes, wave, lane);
-  };
 #pragma unroll
-  for (int p = 0; p < NS - 1; ++p)
-    if (p < total_it) issue(p);
-  lds_barrier();  // ring rows cleared
+    for (int x = 0; x < SPW; ++x) {
+      const int kx = x * WAVES + wave;
+      const int p = 64 * kx + lane;
+      const int row = p / T::CH, ch = (p % T::CH) ^ T::swz(row);
+      const int off = kx < T::instrs ? (jb + row) * rsb + 16 * ch : -1;
+      skr[x] = ldbuf128(rk, off);
+      svr[x] = ldbuf128(rv, off);
+    }
+  };
+  auto stage_put = [&](char* st) {
+#pragma unroll
+    for (int x = 0; x < SPW; ++x) {
+      const int kx = x * WAVES + wave;
+      if (kx < T::instrs) {
+        *reinterpret_cast<u32x4_t*>(st + 1024 * kx + 16 * lane) = skr[x];
+        *reinterpret_cast<u32x4_t*>(st + T::bytes + 1024 * kx + 16 * lane) = svr[x];
+      }
+    }
+  };
+  if (total_it > 0) {
+    stage_fetch(0);
+    stage_put(smem);
+  }
+  if (total_it > 1) stage_fetch(1);
+  lds_barrier();  // ring rows cleared, block 0 staged
 
   u32x4_t qt[NT], ot[NT];
   f32x16_t adq[NDT], au[NDT];
@@ -269,10 +295,13 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
     for (int blk = 0; blk < nb; ++blk, ++it) {
       const int jlo = i0 - w1 + 1;
 
-      if (it + NS - 2 < total_it) wait_vmem<LPB * (NS - 2)>();
-      else wait_vmem<0>();
       lds_barrier();
-      if (it + NS - 1 < total_it) issue(it + NS - 1);
+      // Block it + 1 (loaded into registers during block it - 1) goes into
+      // its stage, visible to all wavefronts after the next barrier; then the
+      // loads of block it + 2 are issued. That stage was last read in block
+      // it - 1, which every wavefront finished before the barrier above.
+      if (it + 1 < total_it) stage_put(smem + ((it + 1) % NS) * L::stageBytes);
+      if (it + 2 < total_it) stage_fetch(it + 2);
       __builtin_amdgcn_sched_barrier(0);
       const char* kt = smem + (it % NS) * L::stageBytes;
       const char* vt = kt + T::bytes;
@@ -317,6 +346,7 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
         __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
       }
       __builtin_amdgcn_sched_barrier(0);
+
       // Blocks at the ends of the window (and of the sequence) mask their keys;
       // the empty asm keeps this a branch rather than selects on every block.
       if (edge) {
@@ -369,100 +399,107 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
       // accumulator layout: lane holds row c, d = 32 dt + 8 (v/4) + 4 h + v%4
       // Every loop below issues all of its LDS reads before the arithmetic
       // and the writes, so each pays the LDS latency once.
+      // In each round every wavefront writes k'_k o dQ~ for 64 columns of its
+      // 32 rows; after the barrier the G wavefronts of a query sum the rows
+      // of their regions, splitting the columns.
+      float* rw = red + wave * 32 * L::cStride;
 #pragma unroll
-      for (int round = 0; round < WAVES / L::redWaves; ++round) {
-        const bool mine = wave / L::redWaves == round;
-        if (mine) {
-          float* rw = red + (wave % L::redWaves) * 32 * L::rStride;
-          u32x2_t kv[4 * NDT];
+      for (int round = 0; round < D / L::redCols; ++round) {
+        constexpr int DT_R = L::redCols / 32;  // accumulator tiles per round
+        u32x2_t kv[4 * DT_R];
 #pragma unroll
-          for (int dt = 0; dt < NDT; ++dt)
+        for (int x = 0; x < DT_R; ++x)
 #pragma unroll
-            for (int qd = 0; qd < 4; ++qd) {
-              const int d = 32 * dt + 8 * qd + 4 * h;
-              if constexpr (L::kStash) {
-                kv[4 * dt + qd] = *reinterpret_cast<const u32x2_t*>(kstash + c * L::kStride + 2 * d);
-              } else {
-                kv[4 * dt + qd] = u32x2_t{0u, 0u};
-                if (rowvalid)
-                  kv[4 * dt + qd] = *reinterpret_cast<const u32x2_t*>(kp + base + static_cast<size_t>(kk) * rs + d);
-              }
-            }
-#pragma unroll
-          for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-            for (int qd = 0; qd < 4; ++qd) {
-              const int d = 32 * dt + 8 * qd + 4 * h;
-              const u32x2_t x = kv[4 * dt + qd];
-              float4 val;
-              val.x = bf16_lo(x[0]) * adq[dt][4 * qd + 0];
-              val.y = bf16_hi(x[0]) * adq[dt][4 * qd + 1];
-              val.z = bf16_lo(x[1]) * adq[dt][4 * qd + 2];
-              val.w = bf16_hi(x[1]) * adq[dt][4 * qd + 3];
-              *reinterpret_cast<float4*>(rw + c * L::rStride + d) = val;
-            }
-        }
-        lds_barrier();
-        // the G wavefronts of a query split its D columns
-        constexpr int COLS = D / G;
-        if (mine && qvalid && 2 * lane < COLS) {
-          const int c0 = g * COLS;
-          float o0 = 0.f, o1 = 0.f;
-#pragma unroll
-          for (int gg = 0; gg < G; ++gg) {
-            const float* rw = red + ((wave - g + gg) % L::redWaves) * 32 * L::rStride + c0 + 2 * lane;
-            float2 xs[32];
-#pragma unroll
-            for (int rr = 0; rr < 32; ++rr) xs[rr] = *reinterpret_cast<const float2*>(rw + rr * L::rStride);
-#pragma unroll
-            for (int rr = 0; rr < 32; ++rr) {
-              o0 += xs[rr].x;
-              o1 += xs[rr].y;
+          for (int qd = 0; qd < 4; ++qd) {
+            const int d = 32 * (DT_R * round + x) + 8 * qd + 4 * h;
+            if constexpr (L::kStash) {
+              kv[4 * x + qd] = *reinterpret_cast<const u32x2_t*>(kstash + c * L::kStride + 2 * d);
+            } else {
+              kv[4 * x + qd] = u32x2_t{0u, 0u};
+              if (rowvalid)
+                kv[4 * x + qd] = *reinterpret_cast<const u32x2_t*>(kp + base + static_cast<size_t>(kk) * rs + d);
             }
           }
-          *reinterpret_cast<unsigned*>(dq + base + static_cast<size_t>(i) * rs + c0 + 2 * lane) =
-              pack_bf16x2(o0 * s.scale, o1 * s.scale);
+#pragma unroll
+        for (int x = 0; x < DT_R; ++x)
+#pragma unroll
+          for (int qd = 0; qd < 4; ++qd) {
+            const int dt = DT_R * round + x;
+            const u32x2_t m = kv[4 * x + qd];
+            float4 val;
+            val.x = bf16_lo(m[0]) * adq[dt][4 * qd + 0];
+            val.y = bf16_hi(m[0]) * adq[dt][4 * qd + 1];
+            val.z = bf16_lo(m[1]) * adq[dt][4 * qd + 2];
+            val.w = bf16_hi(m[1]) * adq[dt][4 * qd + 3];
+            *reinterpret_cast<float4*>(rw + c * L::cStride + 32 * x + 8 * qd + 4 * h) = val;
+          }
+        lds_barrier();
+        constexpr int COLS = L::redCols / G;
+        if (qvalid && lane < COLS) {
+          const int col = g * COLS + lane;
+          float acc = 0.f;
+#pragma unroll
+          for (int gg = 0; gg < G; ++gg) {
+            const float* src = red + (wave - g + gg) * 32 * L::cStride + col;
+            float xs[32];
+#pragma unroll
+            for (int rr = 0; rr < 32; ++rr) xs[rr] = src[rr * L::cStride];
+#pragma unroll
+            for (int rr = 0; rr < 32; ++rr) acc += xs[rr];
+          }
+          dq[base + static_cast<size_t>(i) * rs + L::redCols * round + col] = f32_to_bf16(acc * s.scale);
         }
         lds_barrier();
       }
 
-      // dk'/dv' contributions into the ring, one wavefront at a time (a
-      // fixed order, so the sums are deterministic).
-      u32x2_t qv[4 * NDT], ov[4 * NDT];
+      // dk'/dv' contributions: every wavefront scales its accumulators in
+      // place (scale q_i o dQ~ and dO_i o U~), then adds them into the ring
+      // one wavefront at a time, a fixed order, so the sums are deterministic.
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
         for (int qd = 0; qd < 4; ++qd) {
           const int d = 32 * dt + 8 * qd + 4 * h;
-          qv[4 * dt + qd] = *reinterpret_cast<const u32x2_t*>(qrow + 2 * d);
-          ov[4 * dt + qd] = *reinterpret_cast<const u32x2_t*>(orow + 2 * d);
+          const u32x2_t qv = *reinterpret_cast<const u32x2_t*>(qrow + 2 * d);
+          const u32x2_t ov = *reinterpret_cast<const u32x2_t*>(orow + 2 * d);
+          adq[dt][4 * qd + 0] *= s.scale * bf16_lo(qv[0]);
+          adq[dt][4 * qd + 1] *= s.scale * bf16_hi(qv[0]);
+          adq[dt][4 * qd + 2] *= s.scale * bf16_lo(qv[1]);
+          adq[dt][4 * qd + 3] *= s.scale * bf16_hi(qv[1]);
+          au[dt][4 * qd + 0] *= bf16_lo(ov[0]);
+          au[dt][4 * qd + 1] *= bf16_hi(ov[0]);
+          au[dt][4 * qd + 2] *= bf16_lo(ov[1]);
+          au[dt][4 * qd + 3] *= bf16_hi(ov[1]);
         }
       for (int ww = 0; ww < WAVES; ++ww) {
         if (wave == ww && rowvalid) {
           const int slot = (kk - kbase) % RB;
+          float* rk_ = ring_kp + slot * L::rStride + 4 * h;
+          float* rv_ = ring_vp + slot * L::rStride + 4 * h;
+          float4 xa[4 * NDT], ya[4 * NDT];
 #pragma unroll
-          for (int pass = 0; pass < 2; ++pass) {
-            float* rowp = (pass == 0 ? ring_kp : ring_vp) + slot * L::rStride;
-            float4 xa[4 * NDT];
+          for (int j = 0; j < 4 * NDT; ++j) {
+            xa[j] = *reinterpret_cast<const float4*>(rk_ + 32 * (j / 4) + 8 * (j % 4));
+            ya[j] = *reinterpret_cast<const float4*>(rv_ + 32 * (j / 4) + 8 * (j % 4));
+          }
 #pragma unroll
-            for (int j = 0; j < 4 * NDT; ++j)
-              xa[j] = *reinterpret_cast<const float4*>(rowp + 32 * (j / 4) + 8 * (j % 4) + 4 * h);
+          for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-            for (int dt = 0; dt < NDT; ++dt)
+            for (int qd = 0; qd < 4; ++qd) {
+              const int j = 4 * dt + qd;
+              xa[j].x += adq[dt][4 * qd + 0];
+              xa[j].y += adq[dt][4 * qd + 1];
+              xa[j].z += adq[dt][4 * qd + 2];
+              xa[j].w += adq[dt][4 * qd + 3];
+              ya[j].x += au[dt][4 * qd + 0];
+              ya[j].y += au[dt][4 * qd + 1];
+              ya[j].z += au[dt][4 * qd + 2];
+              ya[j].w += au[dt][4 * qd + 3];
+            }
 #pragma unroll
-              for (int qd = 0; qd < 4; ++qd) {
-                const int j = 4 * dt + qd;
-                const u32x2_t m = pass == 0 ? qv[j] : ov[j];
-                const float f = pass == 0 ? s.scale : 1.f;
-                const f32x16_t& ac = pass == 0 ? adq[dt] : au[dt];
-                xa[j].x += f * bf16_lo(m[0]) * ac[4 * qd + 0];
-                xa[j].y += f * bf16_hi(m[0]) * ac[4 * qd + 1];
-                xa[j].z += f * bf16_lo(m[1]) * ac[4 * qd + 2];
-                xa[j].w += f * bf16_hi(m[1]) * ac[4 * qd + 3];
-              }
-#pragma unroll
-            for (int j = 0; j < 4 * NDT; ++j)
-              *reinterpret_cast<float4*>(rowp + 32 * (j / 4) + 8 * (j % 4) + 4 * h) = xa[j];
+          for (int j = 0; j < 4 * NDT; ++j) {
+            *reinterpret_cast<float4*>(rk_ + 32 * (j / 4) + 8 * (j % 4)) = xa[j];
+            *reinterpret_cast<float4*>(rv_ + 32 * (j / 4) + 8 * (j % 4)) = ya[j];
           }
         }
         lds_barrier();
