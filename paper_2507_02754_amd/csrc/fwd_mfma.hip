@@ -48,7 +48,8 @@ struct FwdLds {
   static constexpr int bytes = statOff + kWaves * 32 * 4;
 };
 
-// NS = stages of the ring of 32-key K/V blocks in LDS (prefetch distance NS-1).
+// NS = stages of the ring of 32-key K/V blocks in LDS (2 suffices: a block is
+// written one block before it is read, into the stage read two blocks ago).
 template <int D, int G, int NS>
 __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const uint16_t* __restrict__ q,
                                                                const uint16_t* __restrict__ k,
@@ -63,7 +64,6 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
   constexpr int W2P = 32 * G;    // rows per query (w2 padded up to a multiple of 32)
   using L = FwdLds<D, NS>;
   using T = typename L::T;
-  constexpr int LPB = 2 * ((T::instrs + kWaves - 1) / kWaves);  // loads per wavefront per block
   __shared__ __attribute__((aligned(16))) char smem[L::bytes];
   float* stat = reinterpret_cast<float*>(smem + L::statOff);
 
@@ -122,20 +122,46 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
   float m = -INFINITY, l = 0.f, m_used = 0.f;
   f32x16_t negm = f32x16_t{};
 
-  auto issue = [&](int blk) {
-    char* st = smem + (blk % NS) * L::stageBytes;
-    tile_load_lds<D, kWaves>(rk, rsb, jlo + 32 * blk, st, wave, lane);
-    tile_load_lds<D, kWaves>(rv, rsb, jlo + 32 * blk, st + T::bytes, wave, lane);
-  };
+  // K/V blocks are staged through registers: fetch loads this wavefront's
+  // share of a block (16 bytes per lane per load, the chunk that belongs at
+  // LDS offset 1024 k + 16 lane of the swizzled tile; rows outside [0, N)
+  // come back as zeros from the buffer range check), put writes it into a
+  // ring stage one block later.
+  constexpr int SPW = (T::instrs + kWaves - 1) / kWaves;  // loads per tile per wavefront
+  u32x4_t skr[SPW], svr[SPW];
+  auto fetch = [&](int blk) {
+    const int jb = jlo + 32 * blk;
 #pragma unroll
-  for (int p = 0; p < NS - 1; ++p)
-    if (p < nb) issue(p);
+    for (int x = 0; x < SPW; ++x) {
+      const int kx = x * kWaves + wave;
+      const int p = 64 * kx + lane;
+      const int row = p / T::CH, ch = (p % T::CH) ^ T::swz(row);
+      const int off = kx < T::instrs ? (jb + row) * rsb + 16 * ch : -1;
+      skr[x] = ldbuf128(rk, off);
+      svr[x] = ldbuf128(rv, off);
+    }
+  };
+  auto put = [&](char* st) {
+#pragma unroll
+    for (int x = 0; x < SPW; ++x) {
+      const int kx = x * kWaves + wave;
+      if (kx < T::instrs) {
+        *reinterpret_cast<u32x4_t*>(st + 1024 * kx + 16 * lane) = skr[x];
+        *reinterpret_cast<u32x4_t*>(st + T::bytes + 1024 * kx + 16 * lane) = svr[x];
+      }
+    }
+  };
+  fetch(0);
+  put(smem);
+  if (nb > 1) fetch(1);
 
   for (int blk = 0; blk < nb; ++blk) {
-    if (blk + NS - 2 < nb) wait_vmem<LPB * (NS - 2)>();
-    else wait_vmem<0>();
     lds_barrier();
-    if (blk + NS - 1 < nb) issue(blk + NS - 1);
+    // Block blk + 1 goes into its stage (last read in block blk - 1, which
+    // every wavefront finished before the barrier), then block blk + 2 is
+    // fetched into the registers.
+    if (blk + 1 < nb) put(smem + ((blk + 1) % NS) * L::stageBytes);
+    if (blk + 2 < nb) fetch(blk + 2);
     const char* kt = smem + (blk % NS) * L::stageBytes;
     const char* vt = kt + T::bytes;
 
@@ -192,7 +218,6 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
       }
     }
   }
-  wait_vmem<0>();
   __syncthreads();
 
   // ---- epilogue: merge the k-rows of each query (log-sum-exp), apply v'_k ----
@@ -269,7 +294,7 @@ template <int D, int G>
 hipError_t launch(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
                   const void* vp, void* out, float* lse, hipStream_t st) {
   constexpr int QW = kWaves / G;
-  constexpr int NS = 4;
+  constexpr int NS = 2;
   const long tiles = (s.N + QW - 1) / QW;
   const long total = tiles * s.B * s.H;
   const long grid = ((total + 7) / 8) * 8;
