@@ -79,30 +79,33 @@ __global__ __launch_bounds__(256) void delta_kernel(Shape s, const uint16_t* __r
 }
 
 // ------------------------------------------------------------------ bwd_q ---
-template <int D, int G, int WAVES, int NS>
+// LDS of the query-side kernel (D = 128: 101 KB for w2 <= 32, 148 KB for w2 = 64):
+//   stage[2]  K and V tiles of one 32-key block (swizzled row-major), double
+//             buffered; during a tile epilogue the stage just consumed holds
+//             the dq column sums
+//   acc       fp32 dk'/dv' ring of k-rows (RB rows)
+//   kring     bf16 k' and v' rows (RK rows each, swizzled like the tiles)
+//   qring     bf16 q and dO rows (RQ rows each)
+template <int D, int G, int WAVES>
 struct BwdQLds {
   using T = SwzTile<D>;
-  static constexpr int stageBytes = 2 * T::bytes;   // K tile + V tile of one 32-key block
-  static constexpr int ringOff = 0;                 // NS stages of the K/V ring
-  static constexpr int rStride = D + 4;             // fp32 rows of the reductions
   static constexpr int QW = WAVES / G;
-  static constexpr int RB = 32 * G + QW;            // rows of the dk'/dv' ring
-  // dq column sums: every wavefront stages its 32 rows x 64 columns at once
-  static constexpr int redCols = D < 64 ? D : 64;
-  static constexpr int cStride = redCols + 4;
-  static constexpr int redOff = NS * stageBytes;
-  static constexpr int accOff = redOff + WAVES * 32 * cStride * 4;
-  // raw bf16 operands of the tile epilogue, kept from the tile prologue:
-  // q_i and dO_i of each wavefront and, where LDS has room, k' of its 32 rows
-  // (rows padded by 16 bytes); otherwise the epilogue reloads k' from memory
-  static constexpr int rowOff = accOff + 2 * RB * rStride * 4;
-  static constexpr int stashOff = rowOff + WAVES * 2 * 2 * D;
-  static constexpr int kStride = 2 * D + 16;
-  static constexpr bool kStash = stashOff + WAVES * 32 * kStride <= 160 * 1024;
-  static constexpr int bytes = stashOff + (kStash ? WAVES * 32 * kStride : 0);
+  static constexpr int W2P = 32 * G;
+  static constexpr int RL = 64 / T::CH;  // rows moved by one 64-lane row load
+  static constexpr int stageBytes = 2 * T::bytes;
+  static constexpr int rStride = D + 4;  // fp32 acc ring rows
+  static constexpr int RB = W2P + QW;
+  // k' rows in use by a tile plus the RL rows loaded for the next one
+  static constexpr int RK = ((W2P + QW - 1 + RL + 15) / 16) * 16;
+  static constexpr int RQ = 16;
+  static constexpr int RC = stageBytes / (WAVES * 32 * 4);  // dq columns per round
+  static constexpr int accOff = 2 * stageBytes;
+  static constexpr int kringOff = accOff + 2 * RB * rStride * 4;
+  static constexpr int qringOff = kringOff + 2 * RK * 2 * D;
+  static constexpr int bytes = qringOff + 2 * RQ * 2 * D;
 };
 
-template <int D, int G, int WAVES, int NS>
+template <int D, int G, int WAVES>
 __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
     Shape s, BwdPlan plan, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ kp, const uint16_t* __restrict__ v, const uint16_t* __restrict__ vp,
@@ -110,16 +113,18 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
     uint16_t* __restrict__ dq, uint16_t* __restrict__ dkp, uint16_t* __restrict__ dvp,
     float* __restrict__ ws) {
   constexpr int NT = D / 16, NDT = D / 32;
-  constexpr int W2P = 32 * G;
   constexpr int NTH = 64 * WAVES;
-  using L = BwdQLds<D, G, WAVES, NS>;
+  using L = BwdQLds<D, G, WAVES>;
   using T = typename L::T;
-  constexpr int QW = L::QW, RB = L::RB;
-  static_assert(WAVES % G == 0 && (L::redCols / G) <= 64 && D % L::redCols == 0, "reduction rounds");
+  constexpr int QW = L::QW, W2P = L::W2P, RB = L::RB, RK = L::RK, RQ = L::RQ, RC = L::RC, RL = L::RL;
+  constexpr int SW = D / WAVES;  // columns of one ring phase slice
+  static_assert(WAVES == 4, "one row tensor per wavefront in the row loads");
+  static_assert(RC % 8 == 0 && D % RC == 0 && RC / G <= 64 && RQ >= QW + RL && SW % 8 == 0, "layout");
   __shared__ __attribute__((aligned(16))) char smem[L::bytes];
-  float* red = reinterpret_cast<float*>(smem + L::redOff);
   float* ring_kp = reinterpret_cast<float*>(smem + L::accOff);
   float* ring_vp = ring_kp + RB * L::rStride;
+  char* kring = smem + L::kringOff;  // k' rows, then v' rows
+  char* qring = smem + L::qringOff;  // q rows, then dO rows
 
   const int total = plan.nchunks * s.B * s.H;
   const int per_xcd = (total + 7) / 8;
@@ -130,13 +135,14 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
   const int b = bh / s.H, hh = bh - b * s.H;
 
   const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63, c = lane & 31, h = lane >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63, c = lane & 31, h = lane >> 5;
   const int qs = wave / G, g = wave % G;
   const size_t rs = static_cast<size_t>(s.H) * D;
   const size_t base = (static_cast<size_t>(b) * s.N * s.H + hh) * D;
   const int N = s.N, w1 = s.w1, w2 = s.w2;
   const int cs = chunk * plan.CQ, ce = min(N, cs + plan.CQ);
-  const int kbase = cs - W2P + 1;  // ring row of k is (k - kbase) % RB
+  const int kbase = cs - W2P + 1;  // k-row k lives in acc ring row (k - kbase) % RB, k' ring row (k - kbase) % RK
   const float qscale = s.scale * kLog2e;
   const size_t stat = static_cast<size_t>(bh) * N;
   const size_t halo = static_cast<size_t>(W2P - 1) * D;
@@ -145,12 +151,12 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
   float* ws_tail_kp = ws_head_vp + plan.halo_floats;
   float* ws_tail_vp = ws_tail_kp + plan.halo_floats;
   const int rsb = static_cast<int>(rs) * 2;
-  const __amdgpu_buffer_rsrc_t rk = make_rsrc(k + base, head_bytes(N, rsb, D));
-  const __amdgpu_buffer_rsrc_t rv = make_rsrc(v + base, head_bytes(N, rsb, D));
+  const unsigned hb = head_bytes(N, rsb, D);
+  const __amdgpu_buffer_rsrc_t rk = make_rsrc(k + base, hb), rv = make_rsrc(v + base, hb);
 
   for (int x = tid; x < 2 * RB * L::rStride; x += NTH) ring_kp[x] = 0.f;
 
-  // Writes ring row k (complete or partial) to its destination and clears it.
+  // Writes acc ring row k (complete or partial) to its destination and clears it.
   auto flush_row = [&](int kr, bool tail) {
     const int slot = (kr - kbase) % RB;
     for (int d = lane; d < D; d += 64) {
@@ -175,17 +181,48 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
     }
   };
 
-  // One flattened pipeline over (query tile, 32-key block): the K/V ring keeps
-  // NS-1 blocks in flight across tile boundaries.
+  // ---- row rings ----
+  // Wavefront w moves RL consecutive rows of one tensor per load (w = 0: k',
+  // 1: v', 2: q, 3: dO), 16 bytes per lane; rows outside [0, N) come back as
+  // zeros from the buffer range check. A tile's k' and v' rows (and q, dO of
+  // its queries) are in the rings before its prologue; the RL rows after them
+  // are loaded during the tile and written in its epilogue.
+  const __amdgpu_buffer_rsrc_t rrow = make_rsrc(
+      (wave == 0 ? kp : wave == 1 ? vp : wave == 2 ? q : dout) + base, hb);
+  const int rl_row = lane / T::CH, rl_ch = lane % T::CH;
+  auto row_load = [&](int r0) { return ldbuf128(rrow, (r0 + rl_row) * rsb + 16 * rl_ch); };
+  auto row_put = [&](int r0, u32x4_t x) {
+    const int r = r0 + rl_row;
+    if (wave < 2) {
+      const int slot = (r - kbase) % RK;
+      *reinterpret_cast<u32x4_t*>(kring + wave * RK * 2 * D + slot * 2 * D + 16 * (rl_ch ^ T::swz(slot))) = x;
+    } else {
+      const int slot = (r - cs) % RQ;
+      *reinterpret_cast<u32x4_t*>(qring + (wave - 2) * RQ * 2 * D + slot * 2 * D + 16 * rl_ch) = x;
+    }
+  };
+  {
+    // Rows of the first tile: k-rows kbase .. cs + QW - 1, queries cs .. cs + QW - 1.
+    constexpr int NG = (W2P + QW - 1 + RL - 1) / RL;
+    const int r00 = wave < 2 ? kbase : cs;
+    const int ng = wave < 2 ? NG : 1;
+    u32x4_t x[NG];
+#pragma unroll
+    for (int gi = 0; gi < NG; ++gi) x[gi] = row_load(gi < ng ? r00 + gi * RL : -RL - 1);
+#pragma unroll
+    for (int gi = 0; gi < NG; ++gi)
+      if (gi < ng) row_put(r00 + gi * RL, x[gi]);
+  }
+
+  // ---- K/V blocks: one pipeline over (query tile, 32-key block) ----
+  // stage_fetch loads this wavefront's share of block `it` into registers
+  // (16 bytes per lane per load, the chunk that belongs at LDS offset
+  // 1024 k + 16 lane of the swizzled tile); stage_put writes it into a stage
+  // one block later.
   const int nb = (w1 + QW - 1 + 31) / 32;
   const int ntiles = (ce - cs + QW - 1) / QW;
   const int total_it = ntiles * nb;
-  // K/V blocks are staged through registers: stage_fetch loads this
-  // wavefront's share of block `it` (16 bytes per lane per load, the chunk
-  // that belongs at LDS offset 1024 k + 16 lane of the swizzled tile), and
-  // stage_put writes it into a ring stage one block later. Rows outside
-  // [0, N) come back as zeros from the buffer range check.
-  constexpr int SPW = (T::instrs + WAVES - 1) / WAVES;  // loads per tile per wavefront
+  constexpr int SPW = (T::instrs + WAVES - 1) / WAVES;
   u32x4_t skr[SPW], svr[SPW];
   auto stage_fetch = [&](int it) {
     const int tile = it / nb, blk = it - tile * nb;
@@ -215,83 +252,58 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
     stage_put(smem);
   }
   if (total_it > 1) stage_fetch(1);
-  lds_barrier();  // ring rows cleared, block 0 staged
+  float nlse = lse[stat + min(cs + qs, N - 1)], ndlt = delta[stat + min(cs + qs, N - 1)];
+  lds_barrier();  // acc ring cleared, first rows and block 0 in LDS
 
   u32x4_t qt[NT], ot[NT];
   f32x16_t adq[NDT], au[NDT];
-  float lse2 = 0.f, dlt = 0.f;
-  int i = 0, kk = 0;
-  bool rowvalid = false, qvalid = false;
-  char* kstash = smem + L::stashOff + wave * 32 * L::kStride;
-  char* qrow = smem + L::rowOff + wave * 4 * D;
-  char* orow = qrow + 2 * D;
-
-  // Raw rows of a tile (q_i, dO_i and k'_k, v'_k of this lane's row),
-  // loaded one tile ahead: the next tile's loads are issued at the start of
-  // the current tile's epilogue. Rows outside [0, N) or the window come back
-  // as zeros from the buffer range check (offset -1).
-  const unsigned hb = head_bytes(N, rsb, D);
-  const __amdgpu_buffer_rsrc_t rq = make_rsrc(q + base, hb), ro = make_rsrc(dout + base, hb);
-  const __amdgpu_buffer_rsrc_t rkp = make_rsrc(kp + base, hb), rvp = make_rsrc(vp + base, hb);
-  u32x4_t nq[NT], nk[NT], no[NT], nv[NT];
-  float nlse = 0.f, ndlt = 0.f;
-  int ni = 0, nkk = 0;
-  auto load_rows = [&](int tile) {
-    ni = cs + tile * QW + qs;
-    nkk = ni - W2P + 1 + 32 * g + c;
-    const bool qv = ni < ce, rv = qv && nkk > ni - w2;
-    const int qo = qv ? ni * rsb + 16 * h : -1;
-    const int ko = rv ? nkk * rsb + 16 * h : -1;
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      nq[t] = ldbuf128(rq, qo < 0 ? -1 : qo + 32 * t);
-      no[t] = ldbuf128(ro, qo < 0 ? -1 : qo + 32 * t);
-      nk[t] = ldbuf128(rkp, ko < 0 ? -1 : ko + 32 * t);
-      nv[t] = ldbuf128(rvp, ko < 0 ? -1 : ko + 32 * t);
-    }
-    const int si = min(ni, N - 1);
-    nlse = lse[stat + si];
-    ndlt = delta[stat + si];
-  };
-  if (total_it > 0) load_rows(0);
-
   int it = 0;
   for (int tile = 0; tile < ntiles; ++tile) {
     const int i0 = cs + tile * QW;
+    const int i = i0 + qs;
+    const int kk = i - W2P + 1 + 32 * g + c;
+    const bool qvalid = i < ce;
+    const bool rowvalid = qvalid && kk >= 0 && kk > i - w2;
+    const int kslot = (kk - kbase) % RK;
+    const char* krow = kring + kslot * 2 * D;
+    const char* qrow = qring + ((i - cs) % RQ) * 2 * D;
+    // Rows outside the window get an infinite normaliser: P = dS = 0.
+    const float lse2 = rowvalid ? nlse * kLog2e : __builtin_inff();
+    const float dlt = qvalid ? ndlt : 0.f;
+    // ---- tile prologue: modulated operands of this wavefront's 32 rows ----
     {
-      // ---- tile prologue: modulated operands of this wavefront's 32 rows ----
-      i = ni;
-      kk = nkk;
-      qvalid = i < ce;
-      rowvalid = qvalid && kk >= 0 && kk > i - w2;
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        u32x4_t a4, b4;
+        const int ch = 2 * t + h;
+        const u32x4_t qa = *reinterpret_cast<const u32x4_t*>(qrow + 16 * ch);
+        const u32x4_t oa = *reinterpret_cast<const u32x4_t*>(qrow + RQ * 2 * D + 16 * ch);
+        const u32x4_t ka = *reinterpret_cast<const u32x4_t*>(krow + 16 * (ch ^ T::swz(kslot)));
+        const u32x4_t va = *reinterpret_cast<const u32x4_t*>(krow + RK * 2 * D + 16 * (ch ^ T::swz(kslot)));
+        u32x4_t a4 = {0u, 0u, 0u, 0u}, b4 = {0u, 0u, 0u, 0u};
+        if (rowvalid) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          a4[e] = pack_bf16x2(bf16_lo(nq[t][e]) * bf16_lo(nk[t][e]) * qscale,
-                              bf16_hi(nq[t][e]) * bf16_hi(nk[t][e]) * qscale);
-          b4[e] = pack_bf16x2(bf16_lo(no[t][e]) * bf16_lo(nv[t][e]), bf16_hi(no[t][e]) * bf16_hi(nv[t][e]));
+          for (int e = 0; e < 4; ++e) {
+            a4[e] = pack_bf16x2(bf16_lo(qa[e]) * bf16_lo(ka[e]) * qscale, bf16_hi(qa[e]) * bf16_hi(ka[e]) * qscale);
+            b4[e] = pack_bf16x2(bf16_lo(oa[e]) * bf16_lo(va[e]), bf16_hi(oa[e]) * bf16_hi(va[e]));
+          }
         }
         qt[t] = a4;
         ot[t] = b4;
-        // The previous tile's epilogue finished reading the stash before its
-        // last barrier.
-        if constexpr (L::kStash) *reinterpret_cast<u32x4_t*>(kstash + c * L::kStride + 32 * t + 16 * h) = nk[t];
-        if (c == 0) {
-          *reinterpret_cast<u32x4_t*>(qrow + 32 * t + 16 * h) = nq[t];
-          *reinterpret_cast<u32x4_t*>(orow + 32 * t + 16 * h) = no[t];
-        }
       }
-      // Rows outside the window get an infinite normaliser: P = dS = 0.
-      lse2 = rowvalid ? nlse * kLog2e : __builtin_inff();
-      dlt = qvalid ? ndlt : 0.f;
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt) {
         adq[dt] = f32x16_t{};
         au[dt] = f32x16_t{};
       }
     }
+    // Rows of the next tile, written in this tile's epilogue.
+    const bool more = tile + 1 < ntiles;
+    const u32x4_t nrow = row_load(more ? i0 + QW : -RL - 1);
+    if (more) {
+      nlse = lse[stat + min(i + QW, N - 1)];
+      ndlt = delta[stat + min(i + QW, N - 1)];
+    }
+
     for (int blk = 0; blk < nb; ++blk, ++it) {
       const int jlo = i0 - w1 + 1;
 
@@ -300,16 +312,15 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
       // its stage, visible to all wavefronts after the next barrier; then the
       // loads of block it + 2 are issued. That stage was last read in block
       // it - 1, which every wavefront finished before the barrier above.
-      if (it + 1 < total_it) stage_put(smem + ((it + 1) % NS) * L::stageBytes);
+      if (it + 1 < total_it) stage_put(smem + ((it + 1) & 1) * L::stageBytes);
       if (it + 2 < total_it) stage_fetch(it + 2);
       __builtin_amdgcn_sched_barrier(0);
-      const char* kt = smem + (it % NS) * L::stageBytes;
+      const char* kt = smem + (it & 1) * L::stageBytes;
       const char* vt = kt + T::bytes;
       // Keys of this block inside query i's window and inside [0, N).
       const int lo = max(qs, -jlo) - 32 * blk;
       const int hi = min(qs + w1 - 1, N - 1 - jlo) - 32 * blk;
       const bool edge = lo > 0 || hi < 31;
-
       // Operand reads run one section ahead of the products that use them.
       // (1) S^T = K q~^T, with the V row fragments read behind it.
       u32x4_t ka[NT], va[NT], ktr[2][NDT], vtr[2][NDT];
@@ -392,125 +403,124 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
       __builtin_amdgcn_sched_barrier(0);
 
     }
-    {
-      // ---- tile epilogue ----
-      if (tile + 1 < ntiles) load_rows(tile + 1);
-      // dq_i = scale * sum_k k'_k o dQ~_(i,k): column sums over the k-rows.
-      // accumulator layout: lane holds row c, d = 32 dt + 8 (v/4) + 4 h + v%4
-      // Every loop below issues all of its LDS reads before the arithmetic
-      // and the writes, so each pays the LDS latency once.
-      // In each round every wavefront writes k'_k o dQ~ for 64 columns of its
-      // 32 rows; after the barrier the G wavefronts of a query sum the rows
-      // of their regions, splitting the columns.
-      float* rw = red + wave * 32 * L::cStride;
-#pragma unroll
-      for (int round = 0; round < D / L::redCols; ++round) {
-        constexpr int DT_R = L::redCols / 32;  // accumulator tiles per round
-        u32x2_t kv[4 * DT_R];
-#pragma unroll
-        for (int x = 0; x < DT_R; ++x)
-#pragma unroll
-          for (int qd = 0; qd < 4; ++qd) {
-            const int d = 32 * (DT_R * round + x) + 8 * qd + 4 * h;
-            if constexpr (L::kStash) {
-              kv[4 * x + qd] = *reinterpret_cast<const u32x2_t*>(kstash + c * L::kStride + 2 * d);
-            } else {
-              kv[4 * x + qd] = u32x2_t{0u, 0u};
-              if (rowvalid)
-                kv[4 * x + qd] = *reinterpret_cast<const u32x2_t*>(kp + base + static_cast<size_t>(kk) * rs + d);
-            }
-          }
-#pragma unroll
-        for (int x = 0; x < DT_R; ++x)
-#pragma unroll
-          for (int qd = 0; qd < 4; ++qd) {
-            const int dt = DT_R * round + x;
-            const u32x2_t m = kv[4 * x + qd];
-            float4 val;
-            val.x = bf16_lo(m[0]) * adq[dt][4 * qd + 0];
-            val.y = bf16_hi(m[0]) * adq[dt][4 * qd + 1];
-            val.z = bf16_lo(m[1]) * adq[dt][4 * qd + 2];
-            val.w = bf16_hi(m[1]) * adq[dt][4 * qd + 3];
-            *reinterpret_cast<float4*>(rw + c * L::cStride + 32 * x + 8 * qd + 4 * h) = val;
-          }
-        lds_barrier();
-        constexpr int COLS = L::redCols / G;
-        if (qvalid && lane < COLS) {
-          const int col = g * COLS + lane;
-          float acc = 0.f;
-#pragma unroll
-          for (int gg = 0; gg < G; ++gg) {
-            const float* src = red + (wave - g + gg) * 32 * L::cStride + col;
-            float xs[32];
-#pragma unroll
-            for (int rr = 0; rr < 32; ++rr) xs[rr] = src[rr * L::cStride];
-#pragma unroll
-            for (int rr = 0; rr < 32; ++rr) acc += xs[rr];
-          }
-          dq[base + static_cast<size_t>(i) * rs + L::redCols * round + col] = f32_to_bf16(acc * s.scale);
-        }
-        lds_barrier();
-      }
 
-      // dk'/dv' contributions: every wavefront scales its accumulators in
-      // place (scale q_i o dQ~ and dO_i o U~), then adds them into the ring
-      // one wavefront at a time, a fixed order, so the sums are deterministic.
+    // ---- tile epilogue ----
+    // The stage read by the last block is free once every wavefront is past
+    // it; it holds the dq column sums. The next tile's rows go into the rings.
+    lds_barrier();
+    if (more) row_put(i0 + QW, nrow);
+    float* red = reinterpret_cast<float*>(smem + ((it - 1) & 1) * L::stageBytes);
+    // dq_i = scale * sum_k k'_k o dQ~_(i,k): column sums over the k-rows, RC
+    // columns a round. accumulator layout: lane holds row c, d = 32 dt +
+    // 8 (v/4) + 4 h + v%4. In a wavefront's region row r holds its RC columns
+    // as float4 groups, group x stored at x ^ rsw(r): conflict-free for the
+    // float4 writes (16 rows a time) and for the column reads.
+    auto rsw = [](int r) { return (r / (64 / RC)) & (RC / 4 - 1); };
+    float* rw = red + wave * 32 * RC;
+#pragma unroll
+    for (int round = 0; round < D / RC; ++round) {
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
         for (int qd = 0; qd < 4; ++qd) {
-          const int d = 32 * dt + 8 * qd + 4 * h;
-          const u32x2_t qv = *reinterpret_cast<const u32x2_t*>(qrow + 2 * d);
-          const u32x2_t ov = *reinterpret_cast<const u32x2_t*>(orow + 2 * d);
-          adq[dt][4 * qd + 0] *= s.scale * bf16_lo(qv[0]);
-          adq[dt][4 * qd + 1] *= s.scale * bf16_hi(qv[0]);
-          adq[dt][4 * qd + 2] *= s.scale * bf16_lo(qv[1]);
-          adq[dt][4 * qd + 3] *= s.scale * bf16_hi(qv[1]);
-          au[dt][4 * qd + 0] *= bf16_lo(ov[0]);
-          au[dt][4 * qd + 1] *= bf16_hi(ov[0]);
-          au[dt][4 * qd + 2] *= bf16_lo(ov[1]);
-          au[dt][4 * qd + 3] *= bf16_hi(ov[1]);
+          const int d0 = 32 * dt + 8 * qd;
+          if (d0 / RC != round) continue;
+          const int d = d0 + 4 * h;
+          const u32x2_t m = *reinterpret_cast<const u32x2_t*>(krow + 16 * ((d >> 3) ^ T::swz(kslot)) + 8 * h);
+          float4 val;
+          val.x = bf16_lo(m[0]) * adq[dt][4 * qd + 0];
+          val.y = bf16_hi(m[0]) * adq[dt][4 * qd + 1];
+          val.z = bf16_lo(m[1]) * adq[dt][4 * qd + 2];
+          val.w = bf16_hi(m[1]) * adq[dt][4 * qd + 3];
+          const int grp = (d - RC * round) >> 2;
+          *reinterpret_cast<float4*>(rw + c * RC + 4 * (grp ^ rsw(c))) = val;
         }
-      for (int ww = 0; ww < WAVES; ++ww) {
-        if (wave == ww && rowvalid) {
-          const int slot = (kk - kbase) % RB;
-          float* rk_ = ring_kp + slot * L::rStride + 4 * h;
-          float* rv_ = ring_vp + slot * L::rStride + 4 * h;
-          float4 xa[4 * NDT], ya[4 * NDT];
+      lds_barrier();
+      // the G wavefronts of a query split the round's columns
+      constexpr int COLS = RC / G;
+      if (qvalid && lane < COLS) {
+        const int col = g * COLS + lane;
+        float xs[32 * G];
 #pragma unroll
-          for (int j = 0; j < 4 * NDT; ++j) {
-            xa[j] = *reinterpret_cast<const float4*>(rk_ + 32 * (j / 4) + 8 * (j % 4));
-            ya[j] = *reinterpret_cast<const float4*>(rv_ + 32 * (j / 4) + 8 * (j % 4));
-          }
+        for (int gg = 0; gg < G; ++gg) {
+          const float* src = red + (wave - g + gg) * 32 * RC + (col & 3);
 #pragma unroll
-          for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-            for (int qd = 0; qd < 4; ++qd) {
-              const int j = 4 * dt + qd;
-              xa[j].x += adq[dt][4 * qd + 0];
-              xa[j].y += adq[dt][4 * qd + 1];
-              xa[j].z += adq[dt][4 * qd + 2];
-              xa[j].w += adq[dt][4 * qd + 3];
-              ya[j].x += au[dt][4 * qd + 0];
-              ya[j].y += au[dt][4 * qd + 1];
-              ya[j].z += au[dt][4 * qd + 2];
-              ya[j].w += au[dt][4 * qd + 3];
-            }
-#pragma unroll
-          for (int j = 0; j < 4 * NDT; ++j) {
-            *reinterpret_cast<float4*>(rk_ + 32 * (j / 4) + 8 * (j % 4)) = xa[j];
-            *reinterpret_cast<float4*>(rv_ + 32 * (j / 4) + 8 * (j % 4)) = ya[j];
-          }
+          for (int rr = 0; rr < 32; ++rr) xs[32 * gg + rr] = src[rr * RC + 4 * ((col >> 2) ^ rsw(rr))];
         }
-        lds_barrier();
+        float acc = 0.f;
+#pragma unroll
+        for (int rr = 0; rr < 32 * G; ++rr) acc += xs[rr];
+        dq[base + static_cast<size_t>(i) * rs + RC * round + col] = f32_to_bf16(acc * s.scale);
       }
-
-      // Rows no later query of the chunk touches are complete.
-      const int fl_lo = i0 - W2P + 1;
-      const int fl_hi = min(i0 + QW, ce) - W2P;  // inclusive
-      for (int kr = fl_lo + wave; kr <= fl_hi; kr += WAVES) flush_row(kr, false);
       lds_barrier();
     }
+
+    // dk'/dv' contributions: every wavefront scales its accumulators in place
+    // (scale q_i o dQ~ and dO_i o U~), then in phase p adds column slice
+    // (wave + p) % WAVES of them into the acc ring. Each slice of a ring row
+    // receives the wavefronts' contributions in a fixed order, so the sums
+    // are deterministic, and no two wavefronts touch one slice in a phase.
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int qd = 0; qd < 4; ++qd) {
+        const int d = 32 * dt + 8 * qd + 4 * h;
+        const u32x2_t qv = *reinterpret_cast<const u32x2_t*>(qrow + 2 * d);
+        const u32x2_t ov = *reinterpret_cast<const u32x2_t*>(qrow + RQ * 2 * D + 2 * d);
+        adq[dt][4 * qd + 0] *= s.scale * bf16_lo(qv[0]);
+        adq[dt][4 * qd + 1] *= s.scale * bf16_hi(qv[0]);
+        adq[dt][4 * qd + 2] *= s.scale * bf16_lo(qv[1]);
+        adq[dt][4 * qd + 3] *= s.scale * bf16_hi(qv[1]);
+        au[dt][4 * qd + 0] *= bf16_lo(ov[0]);
+        au[dt][4 * qd + 1] *= bf16_hi(ov[0]);
+        au[dt][4 * qd + 2] *= bf16_lo(ov[1]);
+        au[dt][4 * qd + 3] *= bf16_hi(ov[1]);
+      }
+    const int aslot = (kk - kbase) % RB;
+    float* rk_ = ring_kp + aslot * L::rStride + 4 * h;
+    float* rv_ = ring_vp + aslot * L::rStride + 4 * h;
+    for (int p = 0; p < WAVES; ++p) {
+      const int sl = (wave + p) % WAVES;
+#pragma unroll
+      for (int slc = 0; slc < WAVES; ++slc) {
+        if (slc != sl || !rowvalid) continue;
+        float4 xa[4 * NDT], ya[4 * NDT];
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+          for (int qd = 0; qd < 4; ++qd) {
+            const int d0 = 32 * dt + 8 * qd;
+            if (d0 / SW != slc) continue;
+            xa[4 * dt + qd] = *reinterpret_cast<const float4*>(rk_ + d0);
+            ya[4 * dt + qd] = *reinterpret_cast<const float4*>(rv_ + d0);
+          }
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+          for (int qd = 0; qd < 4; ++qd) {
+            const int d0 = 32 * dt + 8 * qd;
+            if (d0 / SW != slc) continue;
+            const int j = 4 * dt + qd;
+            xa[j].x += adq[dt][4 * qd + 0];
+            xa[j].y += adq[dt][4 * qd + 1];
+            xa[j].z += adq[dt][4 * qd + 2];
+            xa[j].w += adq[dt][4 * qd + 3];
+            ya[j].x += au[dt][4 * qd + 0];
+            ya[j].y += au[dt][4 * qd + 1];
+            ya[j].z += au[dt][4 * qd + 2];
+            ya[j].w += au[dt][4 * qd + 3];
+            *reinterpret_cast<float4*>(rk_ + d0) = xa[j];
+            *reinterpret_cast<float4*>(rv_ + d0) = ya[j];
+          }
+      }
+      lds_barrier();
+    }
+
+    // Rows no later query of the chunk touches are complete.
+    const int fl_lo = i0 - W2P + 1;
+    const int fl_hi = min(i0 + QW, ce) - W2P;  // inclusive
+    for (int kr = fl_lo + wave; kr <= fl_hi; kr += WAVES) flush_row(kr, false);
+    lds_barrier();
   }
   // Rows still open at the end of the chunk.
   for (int kr = ce - W2P + 1 + wave; kr <= ce - 1; kr += WAVES) flush_row(kr, ce < N);
@@ -822,9 +832,9 @@ hipError_t launch_stage(const Shape& s, BwdStage stage, const void* q, const voi
   const auto* VP = static_cast<const uint16_t*>(vp);
   const auto* DO = static_cast<const uint16_t*>(dout);
   if (stage == BwdStage::Query) {
-    constexpr int WAVES = 4, NS = 3;
+    constexpr int WAVES = 4;
     const long totq = static_cast<long>(plan.nchunks) * s.B * s.H;
-    hipLaunchKernelGGL((bwd_q_kernel<D, G, WAVES, NS>), dim3(static_cast<unsigned>(((totq + 7) / 8) * 8)),
+    hipLaunchKernelGGL((bwd_q_kernel<D, G, WAVES>), dim3(static_cast<unsigned>(((totq + 7) / 8) * 8)),
                        dim3(64 * WAVES), 0, st, s, plan, Q, K, KP, V, VP, DO, lse, delta,
                        static_cast<uint16_t*>(g0), static_cast<uint16_t*>(g1),
                        static_cast<uint16_t*>(g2), halo);
