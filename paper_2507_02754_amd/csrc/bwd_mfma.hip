@@ -247,13 +247,18 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
       }
     }
   };
+  // Blocks 0 and 1 go into the two stages, block 2 into the registers.
   if (total_it > 0) {
     stage_fetch(0);
     stage_put(smem);
   }
-  if (total_it > 1) stage_fetch(1);
+  if (total_it > 1) {
+    stage_fetch(1);
+    stage_put(smem + L::stageBytes);
+  }
+  if (total_it > 2) stage_fetch(2);
   float nlse = lse[stat + min(cs + qs, N - 1)], ndlt = delta[stat + min(cs + qs, N - 1)];
-  lds_barrier();  // acc ring cleared, first rows and block 0 in LDS
+  lds_barrier();  // acc ring cleared, first rows and blocks 0, 1 in LDS
 
   u32x4_t qt[NT], ot[NT];
   f32x16_t adq[NDT], au[NDT];
@@ -304,43 +309,51 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
       ndlt = delta[stat + min(i + QW, N - 1)];
     }
 
-    for (int blk = 0; blk < nb; ++blk, ++it) {
-      const int jlo = i0 - w1 + 1;
-
-      lds_barrier();
-      // Block it + 1 (loaded into registers during block it - 1) goes into
-      // its stage, visible to all wavefronts after the next barrier; then the
-      // loads of block it + 2 are issued. That stage was last read in block
-      // it - 1, which every wavefront finished before the barrier above.
+    // ---- main loop, software-pipelined over the tile's 32-key blocks ----
+    // Block it's logits S are computed at the end of block it - 1 (for a
+    // tile's first block, here), so its exponentials overlap its dP products.
+    // Stages: block it + 1 was written during block it - 1; after the barrier
+    // in block it, block it's stage is free and takes block it + 2. At a
+    // tile's last block that write waits for the next prologue, because the
+    // epilogue uses the freed stage for the dq sums.
+    const int jlo = i0 - w1 + 1;
+    if (tile > 0) {
       if (it + 1 < total_it) stage_put(smem + ((it + 1) & 1) * L::stageBytes);
       if (it + 2 < total_it) stage_fetch(it + 2);
-      __builtin_amdgcn_sched_barrier(0);
-      const char* kt = smem + (it & 1) * L::stageBytes;
-      const char* vt = kt + T::bytes;
-      // Keys of this block inside query i's window and inside [0, N).
-      const int lo = max(qs, -jlo) - 32 * blk;
-      const int hi = min(qs + w1 - 1, N - 1 - jlo) - 32 * blk;
-      const bool edge = lo > 0 || hi < 31;
-      // Operand reads run one section ahead of the products that use them.
-      // (1) S^T = K q~^T, with the V row fragments read behind it.
-      u32x4_t ka[NT], va[NT], ktr[2][NDT], vtr[2][NDT];
+    }
+    lds_barrier();
+    u32x4_t ka[NT], va[NT], ktr[2][NDT], vtr[2][NDT];
+    f32x16_t sacc = f32x16_t{};
+    // S^T = K q~^T of a block from stage `st`, with its V row fragments read behind.
+    auto logits = [&](const char* st) {
 #pragma unroll
-      for (int t = 0; t < NT; ++t) ka[t] = frag_row_swz<D>(kt, c, h, t);
-      f32x16_t sacc = f32x16_t{}, pacc = f32x16_t{};
+      for (int t = 0; t < NT; ++t) ka[t] = frag_row_swz<D>(st, c, h, t);
+      sacc = f32x16_t{};
 #pragma unroll
       for (int t = 0; t < NT; ++t) sacc = mfma32(ka[t], qt[t], sacc);
 #pragma unroll
-      for (int t = 0; t < NT; ++t) va[t] = frag_row_swz<D>(vt, c, h, t);
+      for (int t = 0; t < NT; ++t) va[t] = frag_row_swz<D>(st + T::bytes, c, h, t);
       __builtin_amdgcn_sched_group_barrier(0x100, NT, 0);
 #pragma unroll
       for (int x = 0; x < NT; ++x) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       }
-      __builtin_amdgcn_sched_barrier(0);
+    };
+    logits(smem + (it & 1) * L::stageBytes);
+    __builtin_amdgcn_sched_barrier(0);
 
-      // (2) dP^T = V do~^T, overlapped with the probabilities; the transposed
-      // V fragments are read behind it.
+    for (int blk = 0; blk < nb; ++blk, ++it) {
+      const char* kt = smem + (it & 1) * L::stageBytes;
+      const char* vt = kt + T::bytes;
+      // Keys of this block inside query i's window and inside [0, N).
+      const int lo = max(qs, -jlo) - 32 * blk;
+      const int hi = min(qs + w1 - 1, N - 1 - jlo) - 32 * blk;
+      const bool edge = lo > 0 || hi < 31;
+
+      // (A) dP^T = V do~^T, overlapped with the probabilities; the
+      // transposed V fragments are read behind it.
+      f32x16_t pacc = f32x16_t{};
 #pragma unroll
       for (int t = 0; t < NT; ++t) pacc = mfma32(va[t], ot[t], pacc);
       float pr[16];
@@ -354,12 +367,11 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
       for (int x = 0; x < NT; ++x) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x100, 4 * NDT / NT, 0);
-        __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
       }
       __builtin_amdgcn_sched_barrier(0);
-
-      // Blocks at the ends of the window (and of the sequence) mask their keys;
-      // the empty asm keeps this a branch rather than selects on every block.
+      // Blocks at the ends of the window (and of the sequence) mask their
+      // keys; the empty asm keeps this a branch rather than selects on every block.
       if (edge) {
         asm volatile("" ::: "memory");
 #pragma unroll
@@ -373,7 +385,7 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
       for (int u = 0; u < 2; ++u) pf[u] = pack_frag(pr, u);
       __builtin_amdgcn_sched_barrier(0);
 
-      // (3) U~^T += V^T P^T, overlapped with dS = P (dP - Delta); the
+      // (B) U~^T += V^T P^T, overlapped with dS = P (dP - Delta); the
       // transposed K fragments are read behind it.
 #pragma unroll
       for (int u = 0; u < 2; ++u)
@@ -395,13 +407,22 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
       }
       __builtin_amdgcn_sched_barrier(0);
 
-      // (4) dQ~^T += K^T dS^T.
+      // (C) dQ~^T += K^T dS^T.
 #pragma unroll
       for (int u = 0; u < 2; ++u)
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) adq[dt] = mfma32(ktr[u][dt], df[u], adq[dt]);
       __builtin_amdgcn_sched_barrier(0);
 
+      // (D) the next block's logits, after its stage is visible.
+      if (blk + 1 < nb) {
+        lds_barrier();
+        if (it + 2 < total_it) stage_put(smem + (it & 1) * L::stageBytes);
+        if (it + 3 < total_it) stage_fetch(it + 3);
+        __builtin_amdgcn_sched_barrier(0);
+        logits(smem + ((it + 1) & 1) * L::stageBytes);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
 
     // ---- tile epilogue ----
