@@ -25,6 +25,7 @@
 // Delta is computed by a small row-dot kernel first.
 #include "mfma_common.h"
 
+
 namespace sa {
 
 // ---- workspace layout (shared with the host's size query) --------------------
@@ -316,21 +317,30 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
     // in block it, block it's stage is free and takes block it + 2. At a
     // tile's last block that write waits for the next prologue, because the
     // epilogue uses the freed stage for the dq sums.
+    // The products start from loop-invariant accumulator tiles: S from
+    // -lse2 (the logits come out already normalised) and dP from -Delta.
     const int jlo = i0 - w1 + 1;
     if (tile > 0) {
       if (it + 1 < total_it) stage_put(smem + ((it + 1) & 1) * L::stageBytes);
       if (it + 2 < total_it) stage_fetch(it + 2);
     }
     lds_barrier();
+    f32x16_t c_s, c_dp;
+#pragma unroll
+    for (int vv = 0; vv < 16; ++vv) {
+      c_s[vv] = -lse2;
+      c_dp[vv] = -dlt;
+    }
     u32x4_t ka[NT], va[NT], ktr[2][NDT], vtr[2][NDT];
-    f32x16_t sacc = f32x16_t{};
-    // S^T = K q~^T of a block from stage `st`, with its V row fragments read behind.
-    auto logits = [&](const char* st) {
+    f32x16_t sacc;
+    // S^T - lse2 = K q~^T - lse2 of the block in stage `st`, with its V row
+    // fragments read behind.
+    auto logits = [&](const char* st) __attribute__((always_inline)) {
 #pragma unroll
       for (int t = 0; t < NT; ++t) ka[t] = frag_row_swz<D>(st, c, h, t);
-      sacc = f32x16_t{};
+      sacc = mfma32(ka[0], qt[0], c_s);
 #pragma unroll
-      for (int t = 0; t < NT; ++t) sacc = mfma32(ka[t], qt[t], sacc);
+      for (int t = 1; t < NT; ++t) sacc = mfma32(ka[t], qt[t], sacc);
 #pragma unroll
       for (int t = 0; t < NT; ++t) va[t] = frag_row_swz<D>(st + T::bytes, c, h, t);
       __builtin_amdgcn_sched_group_barrier(0x100, NT, 0);
@@ -340,25 +350,24 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       }
     };
-    logits(smem + (it & 1) * L::stageBytes);
-    __builtin_amdgcn_sched_barrier(0);
 
-    for (int blk = 0; blk < nb; ++blk, ++it) {
-      const char* kt = smem + (it & 1) * L::stageBytes;
+    // One block, read from stage S.
+    auto iter = [&](int S, int blk) __attribute__((always_inline)) {
+      const char* kt = smem + S * L::stageBytes;
       const char* vt = kt + T::bytes;
       // Keys of this block inside query i's window and inside [0, N).
       const int lo = max(qs, -jlo) - 32 * blk;
       const int hi = min(qs + w1 - 1, N - 1 - jlo) - 32 * blk;
       const bool edge = lo > 0 || hi < 31;
 
-      // (A) dP^T = V do~^T, overlapped with the probabilities; the
-      // transposed V fragments are read behind it.
-      f32x16_t pacc = f32x16_t{};
+      // (A) dP^T - Delta = V do~^T - Delta, overlapped with the
+      // probabilities; the transposed V fragments are read behind it.
+      f32x16_t pacc = mfma32(va[0], ot[0], c_dp);
 #pragma unroll
-      for (int t = 0; t < NT; ++t) pacc = mfma32(va[t], ot[t], pacc);
+      for (int t = 1; t < NT; ++t) pacc = mfma32(va[t], ot[t], pacc);
       float pr[16];
 #pragma unroll
-      for (int vv = 0; vv < 16; ++vv) pr[vv] = fast_exp2(sacc[vv] - lse2);
+      for (int vv = 0; vv < 16; ++vv) pr[vv] = fast_exp2(sacc[vv]);
 #pragma unroll
       for (int u = 0; u < 2; ++u)
 #pragma unroll
@@ -367,7 +376,7 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
       for (int x = 0; x < NT; ++x) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x100, 4 * NDT / NT, 0);
-        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
       }
       __builtin_amdgcn_sched_barrier(0);
       // Blocks at the ends of the window (and of the sequence) mask their
@@ -392,7 +401,7 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) au[dt] = mfma32(vtr[u][dt], pf[u], au[dt]);
 #pragma unroll
-      for (int vv = 0; vv < 16; ++vv) pr[vv] *= pacc[vv] - dlt;
+      for (int vv = 0; vv < 16; ++vv) pr[vv] *= pacc[vv];
 #pragma unroll
       for (int u = 0; u < 2; ++u) df[u] = pack_frag(pr, u);
 #pragma unroll
@@ -403,7 +412,7 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
       for (int x = 0; x < 2 * NDT; ++x) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-        __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
       }
       __builtin_amdgcn_sched_barrier(0);
 
@@ -417,13 +426,17 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
       // (D) the next block's logits, after its stage is visible.
       if (blk + 1 < nb) {
         lds_barrier();
-        if (it + 2 < total_it) stage_put(smem + (it & 1) * L::stageBytes);
+        if (it + 2 < total_it) stage_put(smem + S * L::stageBytes);
         if (it + 3 < total_it) stage_fetch(it + 3);
         __builtin_amdgcn_sched_barrier(0);
-        logits(smem + ((it + 1) & 1) * L::stageBytes);
+        logits(smem + (S ^ 1) * L::stageBytes);
         __builtin_amdgcn_sched_barrier(0);
       }
-    }
+      ++it;
+    };
+    logits(smem + (it & 1) * L::stageBytes);
+    __builtin_amdgcn_sched_barrier(0);
+    for (int blk = 0; blk < nb; ++blk) iter(it & 1, blk);
 
     // ---- tile epilogue ----
     // The stage read by the last block is free once every wavefront is past
