@@ -12,16 +12,16 @@
 // Following Section 7's split into two kernels that avoid atomics:
 //   * bwd_q  (query-stationary): recomputes S and dP per j-block of the window
 //     and accumulates dQ~ and U~ on the matrix cores; its epilogue reduces the
-//     k-rows into dq_i and scatters the dk'/dv' contributions into an LDS ring
-//     of k-rows. A workgroup walks a chunk of consecutive query tiles, so each
+//     k-rows into dq_i and adds the dk'/dv' contributions into an LDS ring of
+//     k-rows. A workgroup walks a chunk of consecutive query tiles, so each
 //     k-row is completed inside the chunk except the w2-1 rows at each chunk
 //     boundary; those partial sums go to the workspace and a fix-up kernel adds
 //     the two halves in a fixed order (deterministic, no atomics). This plays
 //     the role of the paper's even/odd two-stage scheme (Algorithm 2).
 //   * bwd_kv (key-stationary): each wavefront keeps 32 rows of K and V in
 //     registers and walks the query rows (i, k) that see them; the workgroup
-//     forms q~ and do~ of one query's rows cooperatively in LDS (row-major and
-//     transposed) and every wavefront contracts them with its keys.
+//     forms q~ and do~ of one query's rows cooperatively in swizzled LDS tiles
+//     and every wavefront contracts them with its keys.
 // Delta is computed by a small row-dot kernel first.
 #include "mfma_common.h"
 

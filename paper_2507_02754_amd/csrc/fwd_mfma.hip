@@ -18,11 +18,13 @@
 // uses two wavefronts per query). All accumulators live in VGPRs so that two
 // workgroups share a CU (two wavefronts per SIMD): one's exponentials overlap
 // the other's matrix products. The j-window union of the workgroup is walked
-// in 32-key blocks. K and V blocks go from HBM straight into a 4-stage ring of
-// swizzled row-major LDS tiles (buffer loads with the LDS destination, no
-// staging registers; the buffer range check zero-fills rows outside [0, N)),
-// issued three blocks ahead. K fragments are read row-wise; V fragments are
-// read with the gfx950 transposing LDS read, so V needs no transposed copy.
+// in 32-key blocks. K and V blocks are loaded into registers (16 bytes per
+// lane, buffer loads whose range check zero-fills rows outside [0, N)) two
+// blocks ahead and written one block ahead into a 2-stage ring of swizzled
+// row-major LDS tiles. (Loads with an LDS destination measured slower here:
+// their issue stalled the wavefront for hundreds of cycles per block.) K
+// fragments are read row-wise; V fragments are read with the gfx950
+// transposing LDS read, so V needs no transposed copy.
 // Within a wavefront all rows share one query, so a block is skipped, fully
 // valid, or masked by column only. The running maximum is rescaled lazily: only when some row's
 // block maximum exceeds it by more than 2^8 (p stays <= 256, exact in fp32 and

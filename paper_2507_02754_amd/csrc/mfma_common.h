@@ -83,7 +83,7 @@ __device__ __forceinline__ unsigned head_bytes(int N, int rs_bytes, int D) {
   return static_cast<unsigned>(N - 1) * static_cast<unsigned>(rs_bytes) + 2u * static_cast<unsigned>(D);
 }
 
-// ---- swizzled row-major tiles, filled by the buffer unit straight into LDS ----
+// ---- swizzled row-major tiles in LDS ----
 //
 // A tile holds 32 rows of D bf16 with no padding; row r's 16-byte chunk ch is
 // stored at chunk slot ch ^ swz(r), swz(r) = 4*(r%4) + (r/4)%4 (mod D/8). This
@@ -94,59 +94,10 @@ template <int D>
 struct SwzTile {
   static constexpr int CH = D / 8;  // 16-byte chunks per row
   static constexpr int bytes = 32 * D * 2;
-  static constexpr int instrs = 32 * CH / 64;  // 64-lane x 16-byte loads per tile
+  static constexpr int instrs = 32 * CH / 64;  // 64-lane x 16-byte transfers per tile
   __device__ static __forceinline__ int swz(int r) { return (4 * (r & 3) + ((r >> 2) & 3)) & (CH - 1); }
   __device__ static __forceinline__ int off(int r, int ch) { return (r * CH + (ch ^ swz(r))) * 16; }
 };
-
-// One direct-to-LDS 16-byte-per-lane load: lane l's 16 bytes from the
-// buffer at byte offset `voff` land at LDS address `lds` + 16 l. Written as
-// inline asm on purpose: when the compiler sees such a load it cannot prove
-// that later LDS reads miss its destination, and puts a full vmcnt(0) wait
-// in front of them, which would drain every prefetch in flight. The callers
-// wait for these loads themselves (wait_vmem, then a barrier); waits the
-// compiler derives for its own loads only become more conservative, since
-// it does not count these. M0 is saved and restored around the load.
-__device__ __forceinline__ void dma_load16(__amdgpu_buffer_rsrc_t r, int voff, unsigned lds) {
-  unsigned saved;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\t"
-      "s_mov_b32 m0, %1\n\t"
-      "s_nop 0\n\t"
-      "buffer_load_dwordx4 %2, %3, 0 offen lds\n\t"
-      "s_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voff), "s"(r)
-      : "memory");
-}
-
-// Issues this wavefront's share of the direct-to-LDS loads of one tile: rows
-// jb .. jb+31 of the head behind `r` (row j at byte offset j * rsb). Load k of
-// the tile fills LDS bytes [1024 k, 1024 k + 1024) with lane l writing 16 bytes
-// at 1024 k + 16 l, so lane l fetches the global chunk that belongs there.
-// Rows outside the resource (j < 0 or j >= N) are zero-filled by the range check.
-// tile_load_lds_part issues only the part-th of those loads (part <
-// ceil(instrs / NWAVES)), so a caller can spread a tile's loads over its loop
-// body instead of issuing them in one burst.
-template <int D, int NWAVES>
-__device__ __forceinline__ void tile_load_lds_part(__amdgpu_buffer_rsrc_t r, int rsb, int jb, char* tile,
-                                                   int wave, int lane, int part) {
-  using T = SwzTile<D>;
-  const int k = part * NWAVES + wave;
-  if (k < T::instrs) {
-    const int p = 64 * k + lane;
-    const int row = p / T::CH, slot = p % T::CH;
-    const int ch = slot ^ T::swz(row);
-    dma_load16(r, (jb + row) * rsb + 16 * ch, static_cast<unsigned>(reinterpret_cast<uintptr_t>(tile + 1024 * k)));
-  }
-}
-template <int D, int NWAVES>
-__device__ __forceinline__ void tile_load_lds(__amdgpu_buffer_rsrc_t r, int rsb, int jb, char* tile,
-                                              int wave, int lane) {
-  constexpr int parts = (SwzTile<D>::instrs + NWAVES - 1) / NWAVES;
-#pragma unroll
-  for (int part = 0; part < parts; ++part) tile_load_lds_part<D, NWAVES>(r, rsb, jb, tile, wave, lane, part);
-}
 
 // Row fragment (lane (h, c): row c, K-slots = columns 16t + 8h .. +7).
 template <int D>
@@ -177,15 +128,10 @@ __device__ __forceinline__ u32x4_t frag_tr_swz(const char* tile, int lane, int d
   return u32x4_t{a[0], a[1], b[0], b[1]};
 }
 
-// Waits until at most N of this wavefront's vector-memory operations are
-// outstanding, then (lds_barrier) synchronises the workgroup. Written as
-// volatile asm with a memory clobber so the compiler keeps LDS accesses on
-// their side of it; the direct-to-LDS loads are invisible to its own waitcnt
-// bookkeeping.
-template <int N>
-__device__ __forceinline__ void wait_vmem() {
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
+// Waits for this wavefront's LDS operations, then synchronises the
+// workgroup. Volatile asm with a memory clobber so the compiler keeps LDS
+// accesses on their side of it, and without the vmcnt(0) wait that
+// __syncthreads adds, so global loads in flight stay in flight.
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 // Accumulator register v of a 32x32 tile holds row 8*(v/4) + 4*h + (v%4).
