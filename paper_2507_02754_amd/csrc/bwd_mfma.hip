@@ -25,6 +25,8 @@
 // Delta is computed by a small row-dot kernel first.
 #include "mfma_common.h"
 
+#include <type_traits>
+
 
 namespace sa {
 
@@ -80,10 +82,46 @@ __global__ __launch_bounds__(256) void delta_kernel(Shape s, const uint16_t* __r
 }
 
 // ------------------------------------------------------------------ bwd_q ---
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+
+// Sums v[j] over the 32 lanes of each half-wavefront (lanes with the same
+// lane >> 5), for NV values per lane, without LDS: each step pairs every lane
+// with one partner, and the lane keeps the sum of one half of its values
+// while the partner keeps the other half (v_permlane16_swap for the lane ^ 16
+// pairs, then DPP row_mirror, row_half_mirror and quad permutations). On
+// return v[0 .. NV/32 - 1] hold the sums of values j0 .. j0 + NV/32 - 1, with
+// j0 = sum over the bits b of c = lane & 31, from bit 4 down, of
+// bit * NV / 2^(step+1).
+template <int NV>
+__device__ __forceinline__ void reduce_lanes32(float* v, int lane) {
+  static_assert(NV >= 32 && NV % 32 == 0, "one value per lane at least");
+  constexpr int N1 = NV / 2;
+#pragma unroll
+  for (int j = 0; j < N1; ++j) {
+    auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v[j]), __float_as_uint(v[j + N1]), false, false);
+    v[j] = __uint_as_float(p[0]) + __uint_as_float(p[1]);
+  }
+  auto step = [&](auto ctrl, int n, int bit) __attribute__((always_inline)) {
+    constexpr int C = decltype(ctrl)::value;
+#pragma unroll
+    for (int j = 0; j < n; ++j) {
+      const float a = v[j] + dpp_f<C>(v[j]), b = v[j + n] + dpp_f<C>(v[j + n]);
+      v[j] = (lane & bit) ? b : a;
+    }
+  };
+  step(std::integral_constant<int, 0x140>{}, N1 / 2, 8);  // row_mirror: lane ^ 15 within 16
+  step(std::integral_constant<int, 0x141>{}, N1 / 4, 4);  // row_half_mirror: lane ^ 7 within 8
+  step(std::integral_constant<int, 0x4E>{}, N1 / 8, 2);   // quad_perm [2,3,0,1]
+  step(std::integral_constant<int, 0xB1>{}, N1 / 16, 1);  // quad_perm [1,0,3,2]
+}
+
 // LDS of the query-side kernel (D = 128: 101 KB for w2 <= 32, 148 KB for w2 = 64):
 //   stage[2]  K and V tiles of one 32-key block (swizzled row-major), double
-//             buffered; during a tile epilogue the stage just consumed holds
-//             the dq column sums
+//             buffered; during a tile epilogue (w2 > 32) the stage just
+//             consumed passes the two halves of each dq between wavefronts
 //   acc       fp32 dk'/dv' ring of k-rows (RB rows)
 //   kring     bf16 k' and v' rows (RK rows each, swizzled like the tiles)
 //   qring     bf16 q and dO rows (RQ rows each)
@@ -99,7 +137,6 @@ struct BwdQLds {
   // k' rows in use by a tile plus the RL rows loaded for the next one
   static constexpr int RK = ((W2P + QW - 1 + RL + 15) / 16) * 16;
   static constexpr int RQ = 16;
-  static constexpr int RC = stageBytes / (WAVES * 32 * 4);  // dq columns per round
   static constexpr int accOff = 2 * stageBytes;
   static constexpr int kringOff = accOff + 2 * RB * rStride * 4;
   static constexpr int qringOff = kringOff + 2 * RK * 2 * D;
@@ -117,10 +154,10 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
   constexpr int NTH = 64 * WAVES;
   using L = BwdQLds<D, G, WAVES>;
   using T = typename L::T;
-  constexpr int QW = L::QW, W2P = L::W2P, RB = L::RB, RK = L::RK, RQ = L::RQ, RC = L::RC, RL = L::RL;
+  constexpr int QW = L::QW, W2P = L::W2P, RB = L::RB, RK = L::RK, RQ = L::RQ, RL = L::RL;
   constexpr int SW = D / WAVES;  // columns of one ring phase slice
   static_assert(WAVES == 4, "one row tensor per wavefront in the row loads");
-  static_assert(RC % 8 == 0 && D % RC == 0 && RC / G <= 64 && RQ >= QW + RL && SW % 8 == 0, "layout");
+  static_assert(RQ >= QW + RL && SW % 8 == 0 && WAVES * 64 * D / 32 * 4 <= L::stageBytes, "layout");
   __shared__ __attribute__((aligned(16))) char smem[L::bytes];
   float* ring_kp = reinterpret_cast<float*>(smem + L::accOff);
   float* ring_vp = ring_kp + RB * L::rStride;
@@ -440,53 +477,54 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
 
     // ---- tile epilogue ----
     // The stage read by the last block is free once every wavefront is past
-    // it; it holds the dq column sums. The next tile's rows go into the rings.
+    // it. The next tile's rows go into the rings.
     lds_barrier();
     if (more) row_put(i0 + QW, nrow);
-    float* red = reinterpret_cast<float*>(smem + ((it - 1) & 1) * L::stageBytes);
-    // dq_i = scale * sum_k k'_k o dQ~_(i,k): column sums over the k-rows, RC
-    // columns a round. accumulator layout: lane holds row c, d = 32 dt +
-    // 8 (v/4) + 4 h + v%4. In a wavefront's region row r holds its RC columns
-    // as float4 groups, group x stored at x ^ rsw(r): conflict-free for the
-    // float4 writes (16 rows a time) and for the column reads.
-    auto rsw = [](int r) { return (r / (64 / RC)) & (RC / 4 - 1); };
-    float* rw = red + wave * 32 * RC;
-#pragma unroll
-    for (int round = 0; round < D / RC; ++round) {
+    // dq_i = scale * sum_k k'_k o dQ~_(i,k): every lane multiplies its
+    // accumulators (row c, d = 32 dt + 8 (v/4) + 4 h + v%4) by k'_k, then the
+    // sums over the 32 rows run across lanes in registers. With w2 > 32 the two
+    // wavefronts of a query add their halves through LDS.
+    {
+      constexpr int NV = 16 * NDT;
+      float xv[NV];
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
         for (int qd = 0; qd < 4; ++qd) {
-          const int d0 = 32 * dt + 8 * qd;
-          if (d0 / RC != round) continue;
-          const int d = d0 + 4 * h;
+          const int d = 32 * dt + 8 * qd + 4 * h;
           const u32x2_t m = *reinterpret_cast<const u32x2_t*>(krow + 16 * ((d >> 3) ^ T::swz(kslot)) + 8 * h);
-          float4 val;
-          val.x = bf16_lo(m[0]) * adq[dt][4 * qd + 0];
-          val.y = bf16_hi(m[0]) * adq[dt][4 * qd + 1];
-          val.z = bf16_lo(m[1]) * adq[dt][4 * qd + 2];
-          val.w = bf16_hi(m[1]) * adq[dt][4 * qd + 3];
-          const int grp = (d - RC * round) >> 2;
-          *reinterpret_cast<float4*>(rw + c * RC + 4 * (grp ^ rsw(c))) = val;
+          xv[16 * dt + 4 * qd + 0] = bf16_lo(m[0]) * adq[dt][4 * qd + 0];
+          xv[16 * dt + 4 * qd + 1] = bf16_hi(m[0]) * adq[dt][4 * qd + 1];
+          xv[16 * dt + 4 * qd + 2] = bf16_lo(m[1]) * adq[dt][4 * qd + 2];
+          xv[16 * dt + 4 * qd + 3] = bf16_hi(m[1]) * adq[dt][4 * qd + 3];
         }
-      lds_barrier();
-      // the G wavefronts of a query split the round's columns
-      constexpr int COLS = RC / G;
-      if (qvalid && lane < COLS) {
-        const int col = g * COLS + lane;
-        float xs[32 * G];
+      reduce_lanes32<NV>(xv, lane);
+      constexpr int NO = NV / 32;  // sums per lane: columns j0 .. j0 + NO - 1
+      const int j0 = NV / 2 * ((c >> 4) & 1) + NV / 4 * ((c >> 3) & 1) + NV / 8 * ((c >> 2) & 1) +
+                     NV / 16 * ((c >> 1) & 1) + NV / 32 * (c & 1);
+      // j = 16 dt + 4 qd + e  <->  d = 32 dt + 8 qd + 4 h + e
+      const int d0 = 32 * (j0 >> 4) + 8 * ((j0 >> 2) & 3) + 4 * h + (j0 & 3);
+      if constexpr (G > 1) {
+        float* part = reinterpret_cast<float*>(smem + ((it - 1) & 1) * L::stageBytes) + wave * 64 * NO;
 #pragma unroll
-        for (int gg = 0; gg < G; ++gg) {
-          const float* src = red + (wave - g + gg) * 32 * RC + (col & 3);
+        for (int t = 0; t < NO; ++t) part[lane * NO + t] = xv[t];
+        lds_barrier();
+        if (g == 0) {
 #pragma unroll
-          for (int rr = 0; rr < 32; ++rr) xs[32 * gg + rr] = src[rr * RC + 4 * ((col >> 2) ^ rsw(rr))];
+          for (int gg = 1; gg < G; ++gg)
+#pragma unroll
+            for (int t = 0; t < NO; ++t) xv[t] += part[gg * 64 * NO + lane * NO + t];
         }
-        float acc = 0.f;
-#pragma unroll
-        for (int rr = 0; rr < 32 * G; ++rr) acc += xs[rr];
-        dq[base + static_cast<size_t>(i) * rs + RC * round + col] = f32_to_bf16(acc * s.scale);
       }
-      lds_barrier();
+      if (qvalid && g == 0) {
+        uint16_t* dst = dq + base + static_cast<size_t>(i) * rs + d0;
+        if constexpr (NO == 2) {
+          *reinterpret_cast<unsigned*>(dst) = pack_bf16x2(xv[0] * s.scale, xv[1] * s.scale);
+        } else {
+#pragma unroll
+          for (int t = 0; t < NO; ++t) dst[t] = f32_to_bf16(xv[t] * s.scale);
+        }
+      }
     }
 
     // dk'/dv' contributions: every wavefront scales its accumulators in place
