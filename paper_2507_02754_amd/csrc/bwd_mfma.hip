@@ -25,8 +25,6 @@
 // Delta is computed by a small row-dot kernel first.
 #include "mfma_common.h"
 
-#include <type_traits>
-
 
 namespace sa {
 
@@ -82,41 +80,6 @@ __global__ __launch_bounds__(256) void delta_kernel(Shape s, const uint16_t* __r
 }
 
 // ------------------------------------------------------------------ bwd_q ---
-template <int CTRL>
-__device__ __forceinline__ float dpp_f(float x) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
-}
-
-// Sums v[j] over the 32 lanes of each half-wavefront (lanes with the same
-// lane >> 5), for NV values per lane, without LDS: each step pairs every lane
-// with one partner, and the lane keeps the sum of one half of its values
-// while the partner keeps the other half (v_permlane16_swap for the lane ^ 16
-// pairs, then DPP row_mirror, row_half_mirror and quad permutations). On
-// return v[0 .. NV/32 - 1] hold the sums of values j0 .. j0 + NV/32 - 1, with
-// j0 = sum over the bits b of c = lane & 31, from bit 4 down, of
-// bit * NV / 2^(step+1).
-template <int NV>
-__device__ __forceinline__ void reduce_lanes32(float* v, int lane) {
-  static_assert(NV >= 32 && NV % 32 == 0, "one value per lane at least");
-  constexpr int N1 = NV / 2;
-#pragma unroll
-  for (int j = 0; j < N1; ++j) {
-    auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v[j]), __float_as_uint(v[j + N1]), false, false);
-    v[j] = __uint_as_float(p[0]) + __uint_as_float(p[1]);
-  }
-  auto step = [&](auto ctrl, int n, int bit) __attribute__((always_inline)) {
-    constexpr int C = decltype(ctrl)::value;
-#pragma unroll
-    for (int j = 0; j < n; ++j) {
-      const float a = v[j] + dpp_f<C>(v[j]), b = v[j + n] + dpp_f<C>(v[j + n]);
-      v[j] = (lane & bit) ? b : a;
-    }
-  };
-  step(std::integral_constant<int, 0x140>{}, N1 / 2, 8);  // row_mirror: lane ^ 15 within 16
-  step(std::integral_constant<int, 0x141>{}, N1 / 4, 4);  // row_half_mirror: lane ^ 7 within 8
-  step(std::integral_constant<int, 0x4E>{}, N1 / 8, 2);   // quad_perm [2,3,0,1]
-  step(std::integral_constant<int, 0xB1>{}, N1 / 16, 1);  // quad_perm [1,0,3,2]
-}
 
 // LDS of the query-side kernel (D = 128: 101 KB for w2 <= 32, 148 KB for w2 = 64):
 //   stage[2]  K and V tiles of one 32-key block (swizzled row-major), double

@@ -43,10 +43,8 @@ template <int D, int NS>
 struct FwdLds {
   using T = SwzTile<D>;
   static constexpr int stageBytes = 2 * T::bytes;  // K tile + V tile of one 32-key block
-  static constexpr int mainBytes = NS * stageBytes;
-  static constexpr int rStride = D + 4;                  // epilogue rows (fp32)
-  static constexpr int redBytes = 2 * 32 * rStride * 4;  // two wavefronts per round
-  static constexpr int statOff = mainBytes > redBytes ? mainBytes : redBytes;
+  static constexpr int mainBytes = NS * stageBytes;  // also the epilogue's exchange area
+  static constexpr int statOff = mainBytes;
   static constexpr int bytes = statOff + kWaves * 32 * 4;
 };
 
@@ -220,13 +218,20 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
       }
     }
   }
-  __syncthreads();
-
   // ---- epilogue: merge the k-rows of each query (log-sum-exp), apply v'_k ----
+  // v'_k of this lane's row in the accumulator layout (d = 32 dt + 8 (v/4) +
+  // 4 h + v%4), loaded first so the merge below covers their latency.
+  const __amdgpu_buffer_rsrc_t rvp = make_rsrc(vp + base, head_bytes(N, rsb, D));
+  u32x2_t vpr[4 * NDT];
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+    for (int qd = 0; qd < 4; ++qd)
+      vpr[4 * dt + qd] = ldbuf64(rvp, rowvalid ? kk * rsb + 2 * (32 * dt + 8 * qd + 4 * h) : -1);
   const float lsum = l + swap_halves(l);
   const float lse2_row = rowvalid ? m + fast_log2(lsum) : -INFINITY;
   if (h == 0) stat[wave * 32 + c] = lse2_row;
-  __syncthreads();
+  lds_barrier();  // also: every wavefront is past its last K/V stage reads
   float mq = -INFINITY;
 #pragma unroll
   for (int gg = 0; gg < G; ++gg) mq = fmaxf(mq, stat[(qs * G + gg) * 32 + c]);
@@ -241,54 +246,48 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
   const float lse2 = mq + fast_log2(z);
   const float wgt = rowvalid ? fast_exp2(m - lse2) : 0.f;
 
-  float* red = reinterpret_cast<float*>(smem);
-  // Two wavefronts per round: rows (w * U_r o v'_k) of the round's wavefronts
-  // go to LDS, then column sums give O. For w2 = 64 a round is one query.
+  // O_i = sum over the query's rows of w_r v'_k o U_r: the sums over the 32
+  // rows of a wavefront run across lanes in registers; with w2 > 32 the two
+  // wavefronts of a query add their halves through LDS.
+  constexpr int NV = 16 * NDT;
+  constexpr int NO = NV / 32;  // sums per lane
+  float xv[NV];
 #pragma unroll
-  for (int round = 0; round < 2; ++round) {
-    const bool mine = (wave >> 1) == round;
-    if (mine) {
-      float* rw = red + (wave & 1) * 32 * L::rStride;
+  for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) {
-#pragma unroll
-        for (int qd = 0; qd < 4; ++qd) {
-          const int d = 32 * dt + 8 * qd + 4 * h;
-          u32x2_t vv = {0u, 0u};
-          if (rowvalid) vv = *reinterpret_cast<const u32x2_t*>(vp + base + static_cast<size_t>(kk) * rs + d);
-          float4 val;
-          val.x = wgt * bf16_lo(vv[0]) * acc[dt][4 * qd + 0];
-          val.y = wgt * bf16_hi(vv[0]) * acc[dt][4 * qd + 1];
-          val.z = wgt * bf16_lo(vv[1]) * acc[dt][4 * qd + 2];
-          val.w = wgt * bf16_hi(vv[1]) * acc[dt][4 * qd + 3];
-          *reinterpret_cast<float4*>(rw + c * L::rStride + d) = val;
-        }
-      }
+    for (int qd = 0; qd < 4; ++qd) {
+      const u32x2_t x = vpr[4 * dt + qd];
+      xv[16 * dt + 4 * qd + 0] = wgt * bf16_lo(x[0]) * acc[dt][4 * qd + 0];
+      xv[16 * dt + 4 * qd + 1] = wgt * bf16_hi(x[0]) * acc[dt][4 * qd + 1];
+      xv[16 * dt + 4 * qd + 2] = wgt * bf16_lo(x[1]) * acc[dt][4 * qd + 2];
+      xv[16 * dt + 4 * qd + 3] = wgt * bf16_hi(x[1]) * acc[dt][4 * qd + 3];
     }
-    __syncthreads();
-    if (mine && qvalid) {
-      // G = 1: each wavefront sums its own 32 rows over all D columns.
-      // G = 2: the pair sums 64 rows, each wavefront half of the columns.
-      constexpr int COLS = D / G;  // columns summed by this wavefront
-      const int c0 = G == 1 ? 0 : (wave & 1) * COLS;
-      if (2 * lane < COLS) {
-        float o0 = 0.f, o1 = 0.f;
+  reduce_lanes32<NV>(xv, lane);
+  const int j0 = NV / 2 * ((c >> 4) & 1) + NV / 4 * ((c >> 3) & 1) + NV / 8 * ((c >> 2) & 1) +
+                 NV / 16 * ((c >> 1) & 1) + NV / 32 * (c & 1);
+  // j = 16 dt + 4 qd + e  <->  d = 32 dt + 8 qd + 4 h + e
+  const int d0 = 32 * (j0 >> 4) + 8 * ((j0 >> 2) & 3) + 4 * h + (j0 & 3);
+  if constexpr (G > 1) {
+    float* part = reinterpret_cast<float*>(smem) + wave * 64 * NO;
 #pragma unroll
-        for (int gg = 0; gg < G; ++gg) {
-          const float* rw = red + (G == 1 ? (wave & 1) : gg) * 32 * L::rStride + c0 + 2 * lane;
-#pragma unroll 8
-          for (int rr = 0; rr < 32; ++rr) {
-            const float2 x = *reinterpret_cast<const float2*>(rw + rr * L::rStride);
-            o0 += x.x;
-            o1 += x.y;
-          }
-        }
-        *reinterpret_cast<unsigned*>(out + base + static_cast<size_t>(i) * rs + c0 + 2 * lane) =
-            pack_bf16x2(o0, o1);
-      }
-      if (lane == 0 && g == 0) lse[static_cast<size_t>(bh) * N + i] = lse2 * kLn2;
+    for (int t = 0; t < NO; ++t) part[lane * NO + t] = xv[t];
+    lds_barrier();
+    if (g == 0) {
+#pragma unroll
+      for (int gg = 1; gg < G; ++gg)
+#pragma unroll
+        for (int t = 0; t < NO; ++t) xv[t] += part[gg * 64 * NO + lane * NO + t];
     }
-    __syncthreads();
+  }
+  if (qvalid && g == 0) {
+    uint16_t* dst = out + base + static_cast<size_t>(i) * rs + d0;
+    if constexpr (NO == 2) {
+      *reinterpret_cast<unsigned*>(dst) = pack_bf16x2(xv[0], xv[1]);
+    } else {
+#pragma unroll
+      for (int t = 0; t < NO; ++t) dst[t] = f32_to_bf16(xv[t]);
+    }
+    if (lane == 0) lse[static_cast<size_t>(bh) * N + i] = lse2 * kLn2;
   }
 }
 

@@ -13,6 +13,8 @@
 
 #include "sa_internal.h"
 
+#include <type_traits>
+
 namespace sa {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
@@ -77,6 +79,9 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, unsig
 __device__ __forceinline__ u32x4_t ldbuf128(__amdgpu_buffer_rsrc_t r, int off) {
   return __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }
+__device__ __forceinline__ u32x2_t ldbuf64(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
+}
 // Byte-range of one head's rows of a [.., N, H, D] bf16 tensor, from row 0 to
 // the end of row N-1 (rows are rs_bytes apart).
 __device__ __forceinline__ unsigned head_bytes(int N, int rs_bytes, int D) {
@@ -133,6 +138,42 @@ __device__ __forceinline__ u32x4_t frag_tr_swz(const char* tile, int lane, int d
 // accesses on their side of it, and without the vmcnt(0) wait that
 // __syncthreads adds, so global loads in flight stay in flight.
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+
+// Sums v[j] over the 32 lanes of each half-wavefront (lanes with the same
+// lane >> 5), for NV values per lane, without LDS: each step pairs every lane
+// with one partner, and the lane keeps the sum of one half of its values
+// while the partner keeps the other half (v_permlane16_swap for the lane ^ 16
+// pairs, then DPP row_mirror, row_half_mirror and quad permutations). On
+// return v[0 .. NV/32 - 1] hold the sums of values j0 .. j0 + NV/32 - 1, with
+// j0 = sum over the bits b of c = lane & 31, from bit 4 down, of
+// bit * NV / 2^(step+1).
+template <int NV>
+__device__ __forceinline__ void reduce_lanes32(float* v, int lane) {
+  static_assert(NV >= 32 && NV % 32 == 0, "one value per lane at least");
+  constexpr int N1 = NV / 2;
+#pragma unroll
+  for (int j = 0; j < N1; ++j) {
+    auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v[j]), __float_as_uint(v[j + N1]), false, false);
+    v[j] = __uint_as_float(p[0]) + __uint_as_float(p[1]);
+  }
+  auto step = [&](auto ctrl, int n, int bit) __attribute__((always_inline)) {
+    constexpr int C = decltype(ctrl)::value;
+#pragma unroll
+    for (int j = 0; j < n; ++j) {
+      const float a = v[j] + dpp_f<C>(v[j]), b = v[j + n] + dpp_f<C>(v[j + n]);
+      v[j] = (lane & bit) ? b : a;
+    }
+  };
+  step(std::integral_constant<int, 0x140>{}, N1 / 2, 8);  // row_mirror: lane ^ 15 within 16
+  step(std::integral_constant<int, 0x141>{}, N1 / 4, 4);  // row_half_mirror: lane ^ 7 within 8
+  step(std::integral_constant<int, 0x4E>{}, N1 / 8, 2);   // quad_perm [2,3,0,1]
+  step(std::integral_constant<int, 0xB1>{}, N1 / 16, 1);  // quad_perm [1,0,3,2]
+}
 
 // Accumulator register v of a 32x32 tile holds row 8*(v/4) + 4*h + (v%4).
 __device__ __forceinline__ int acc_row(int v, int h) { return 8 * (v >> 2) + 4 * h + (v & 3); }
