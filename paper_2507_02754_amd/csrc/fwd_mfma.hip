@@ -89,23 +89,9 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
   const int i = i0 + qs;
   const bool qvalid = i < N;
 
-  // ---- modulated queries q~ = (scale*log2 e) * q_i o k'_k as B operands ----
   const int kk = i - W2P + 1 + 32 * g + c;
   const bool rowvalid = qvalid && kk >= 0 && kk > i - w2;
   const float qscale = s.scale * kLog2e;
-  u32x4_t qt[NT];
-#pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    u32x4_t r4 = {0u, 0u, 0u, 0u};
-    if (rowvalid) {
-      const u32x4_t a = ldg128(q + base + static_cast<size_t>(i) * rs + 16 * t + 8 * h);
-      const u32x4_t bb = ldg128(kp + base + static_cast<size_t>(kk) * rs + 16 * t + 8 * h);
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        r4[e] = pack_bf16x2(bf16_lo(a[e]) * bf16_lo(bb[e]) * qscale, bf16_hi(a[e]) * bf16_hi(bb[e]) * qscale);
-    }
-    qt[t] = r4;
-  }
 
   // ---- main loop over 32-key blocks of the workgroup's window union ----
   const int jlo = i0 - w1 + 1;
@@ -151,7 +137,29 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
       }
     }
   };
+  // The first block's K/V loads go out before the q~ loads, so their
+  // latencies overlap.
   fetch(0);
+
+  // ---- modulated queries q~ = (scale*log2 e) * q_i o k'_k as B operands ----
+  // (rows outside the window or the sequence load as zeros: offset -1)
+  u32x4_t qt[NT];
+  {
+    const __amdgpu_buffer_rsrc_t rq = make_rsrc(q + base, head_bytes(N, rsb, D));
+    const __amdgpu_buffer_rsrc_t rkp = make_rsrc(kp + base, head_bytes(N, rsb, D));
+    u32x4_t qa[NT], ka[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      qa[t] = ldbuf128(rq, rowvalid ? i * rsb + 32 * t + 16 * h : -1);
+      ka[t] = ldbuf128(rkp, rowvalid ? kk * rsb + 32 * t + 16 * h : -1);
+    }
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        qt[t][e] = pack_bf16x2(bf16_lo(qa[t][e]) * bf16_lo(ka[t][e]) * qscale,
+                               bf16_hi(qa[t][e]) * bf16_hi(ka[t][e]) * qscale);
+  }
   put(smem);
   if (nb > 1) fetch(1);
 
