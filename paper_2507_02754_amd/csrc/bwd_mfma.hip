@@ -657,7 +657,9 @@ __global__ __launch_bounds__(256) void bwd_kv_kernel(
   const int i_end = min(N, j0 + 127 + w1);
   const int nrb = (i_end - j0) * G;
 
-  // Formation of one row block: rows (2p, 2p+1), 8 columns per work item.
+  // Formation of one row block: rows p and p + 16, 8 columns per work item
+  // (16 consecutive rows per store instruction keep the swizzled writes
+  // free of bank conflicts).
   // fetch() issues the global loads of the next row block before the current
   // one is computed; form_put() multiplies and stores them afterwards, so the
   // load latency hides behind a whole row block of matrix work. Loads go
@@ -678,13 +680,13 @@ __global__ __launch_bounds__(256) void bwd_kv_kernel(
     ro = ldbuf128(rso, qoff);
 #pragma unroll
     for (int y = 0; y < 2; ++y) {
-      const int kk = i - W2P + 1 + 32 * g + 2 * p_ + y;
+      const int kk = i - W2P + 1 + 32 * g + p_ + 16 * y;
       const int koff = fitem && kk > i - w2 ? kk * rsb + 16 * dc : -1;
       rk[y] = ldbuf128(rskp, koff);
       rv[y] = ldbuf128(rsvp, koff);
     }
   };
-  // Row-major swizzled tiles: rows (2p, 2p+1), 16-byte chunk dc of each.
+  // Row-major swizzled tiles: rows p and p + 16, 16-byte chunk dc of each.
   // Rows whose k is outside the window were fetched as zero, so q~ = do~ = 0
   // there and those rows add nothing to dK or dV whatever their P and dS.
   auto form_put = [&](char* buf) {
@@ -705,8 +707,8 @@ __global__ __launch_bounds__(256) void bwd_kv_kernel(
         a4[e] = pack_bf16x2(qlo[e] * bf16_lo(rk[y][e]), qhi[e] * bf16_hi(rk[y][e]));
         b4[e] = pack_bf16x2(olo[e] * bf16_lo(rv[y][e]), ohi[e] * bf16_hi(rv[y][e]));
       }
-      *reinterpret_cast<u32x4_t*>(buf + T::off(2 * p_ + y, dc)) = a4;
-      *reinterpret_cast<u32x4_t*>(buf + T::bytes + T::off(2 * p_ + y, dc)) = b4;
+      *reinterpret_cast<u32x4_t*>(buf + T::off(p_ + 16 * y, dc)) = a4;
+      *reinterpret_cast<u32x4_t*>(buf + T::bytes + T::off(p_ + 16 * y, dc)) = b4;
     }
   };
 
