@@ -186,7 +186,7 @@ def main():
     algo = {
         "fwd": ("fwd_mfma_kernel", 4 * unit),
         "bwd_query_side": ("bwd_q_kernel", 8 * unit),   # S recompute, dP, dQ~, U~
-        "bwd_key_side": ("bwd_kv_kernel", 4 * unit),    # dV, dK (its S/dP recompute is not counted)
+        "bwd_key_side": ("bwd_key_kernel", 4 * unit),    # dV, dK (its S/dP recompute is not counted)
     }
     dom = max(algo, key=lambda p: ms[p])
     kname, kflops = algo[dom]

@@ -18,10 +18,8 @@
 //     boundary; those partial sums go to the workspace and a fix-up kernel adds
 //     the two halves in a fixed order (deterministic, no atomics). This plays
 //     the role of the paper's even/odd two-stage scheme (Algorithm 2).
-//   * bwd_kv (key-stationary): each wavefront keeps 32 rows of K and V in
-//     registers and walks the query rows (i, k) that see them; the workgroup
-//     forms q~ and do~ of one query's rows cooperatively in swizzled LDS tiles
-//     and every wavefront contracts them with its keys.
+//   * key side (bwd_key.hip, key-stationary): K and V rows stay in registers
+//     and the kernel walks the query rows (i, k) that see them.
 // Delta is computed by a small row-dot kernel first.
 #include "mfma_common.h"
 
@@ -590,270 +588,6 @@ __global__ __launch_bounds__(256) void halo_fixup_kernel(Shape s, BwdPlan plan, 
   dvp[dst] = f32_to_bf16(tail_vp[o] + head_vp[o]);
 }
 
-// ----------------------------------------------------------------- bwd_kv ---
-template <int D>
-struct BwdKvLds {
-  using T = SwzTile<D>;
-  static constexpr int bufBytes = 2 * T::bytes;  // q~ and do~ tiles of one row block
-  static constexpr int mainBytes = 2 * bufBytes;
-  static constexpr int oStride = D + 4;
-  static constexpr int outBytes = 4 * 32 * oStride * 4;
-  static constexpr int bytes = mainBytes > outBytes ? mainBytes : outBytes;
-};
-
-template <int D, int G>
-__global__ __launch_bounds__(256) void bwd_kv_kernel(
-    Shape s, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
-    const uint16_t* __restrict__ kp, const uint16_t* __restrict__ v, const uint16_t* __restrict__ vp,
-    const uint16_t* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ delta,
-    uint16_t* __restrict__ dk, uint16_t* __restrict__ dv) {
-  constexpr int NT = D / 16, NDT = D / 32;
-  constexpr int W2P = 32 * G;
-  using L = BwdKvLds<D>;
-  using T = typename L::T;
-  __shared__ __attribute__((aligned(16))) char smem[L::bytes];
-
-  const int jblocks = (s.N + 127) / 128;
-  const int total = jblocks * s.B * s.H;
-  const int per_xcd = (total + 7) / 8;
-  const int logical = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
-  if (logical >= total) return;
-  const int bh = logical / jblocks;
-  const int jblk = logical - bh * jblocks;
-  const int b = bh / s.H, hh = bh - b * s.H;
-
-  const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63, c = lane & 31, h = lane >> 5;
-  const size_t rs = static_cast<size_t>(s.H) * D;
-  const size_t base = (static_cast<size_t>(b) * s.N * s.H + hh) * D;
-  const int N = s.N, w1 = s.w1, w2 = s.w2;
-  const float qscale = s.scale * kLog2e;
-  const size_t stat = static_cast<size_t>(bh) * N;
-  const int j0 = jblk * 128;
-  const int jw = j0 + 32 * wave;  // this wavefront's keys jw .. jw + 31
-  const int jme = jw + c;         // key of this lane's accumulator column
-
-  // K and V rows of this wavefront as B operands (lane: key jw + c, 8 d's per slot group)
-  u32x4_t kf[NT], vf[NT];
-#pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    u32x4_t a = {0u, 0u, 0u, 0u}, bb = {0u, 0u, 0u, 0u};
-    if (jme < N) {
-      a = ldg128(k + base + static_cast<size_t>(jme) * rs + 16 * t + 8 * h);
-      bb = ldg128(v + base + static_cast<size_t>(jme) * rs + 16 * t + 8 * h);
-    }
-    kf[t] = a;
-    vf[t] = bb;
-  }
-
-  f32x16_t adk[NDT], adv[NDT];
-#pragma unroll
-  for (int dt = 0; dt < NDT; ++dt) {
-    adk[dt] = f32x16_t{};
-    adv[dt] = f32x16_t{};
-  }
-
-  // Row blocks: (query i, k-chunk g) for i in [j0, min(N, j0 + 127 + w1)).
-  const int i_end = min(N, j0 + 127 + w1);
-  const int nrb = (i_end - j0) * G;
-
-  // Formation of one row block: rows p and p + 16, 8 columns per work item
-  // (16 consecutive rows per store instruction keep the swizzled writes
-  // free of bank conflicts).
-  // fetch() issues the global loads of the next row block before the current
-  // one is computed; form_put() multiplies and stores them afterwards, so the
-  // load latency hides behind a whole row block of matrix work. Loads go
-  // through buffer resources over one head: a row outside [0, N) or outside
-  // the k-window gets offset -1, which the range check turns into zeros.
-  constexpr int items = 16 * (D / 8);
-  const int p_ = tid & 15, dc = tid >> 4;
-  const bool fitem = items >= 256 || tid < items;  // all 256 threads at D = 128
-  const int rsb = static_cast<int>(rs) * 2;
-  const unsigned hb = head_bytes(N, rsb, D);
-  const __amdgpu_buffer_rsrc_t rsq = make_rsrc(q + base, hb), rso = make_rsrc(dout + base, hb);
-  const __amdgpu_buffer_rsrc_t rskp = make_rsrc(kp + base, hb), rsvp = make_rsrc(vp + base, hb);
-  u32x4_t rq, ro, rk[2], rv[2];
-  auto fetch = [&](int rb) {
-    const int i = j0 + rb / G, g = rb - (rb / G) * G;
-    const int qoff = fitem ? i * rsb + 16 * dc : -1;
-    rq = ldbuf128(rsq, qoff);
-    ro = ldbuf128(rso, qoff);
-#pragma unroll
-    for (int y = 0; y < 2; ++y) {
-      const int kk = i - W2P + 1 + 32 * g + p_ + 16 * y;
-      const int koff = fitem && kk > i - w2 ? kk * rsb + 16 * dc : -1;
-      rk[y] = ldbuf128(rskp, koff);
-      rv[y] = ldbuf128(rsvp, koff);
-    }
-  };
-  // Row-major swizzled tiles: rows p and p + 16, 16-byte chunk dc of each.
-  // Rows whose k is outside the window were fetched as zero, so q~ = do~ = 0
-  // there and those rows add nothing to dK or dV whatever their P and dS.
-  auto form_put = [&](char* buf) {
-    if (!fitem) return;
-    float qlo[4], qhi[4], olo[4], ohi[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      qlo[e] = bf16_lo(rq[e]);
-      qhi[e] = bf16_hi(rq[e]);
-      olo[e] = bf16_lo(ro[e]);
-      ohi[e] = bf16_hi(ro[e]);
-    }
-#pragma unroll
-    for (int y = 0; y < 2; ++y) {
-      u32x4_t a4, b4;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        a4[e] = pack_bf16x2(qlo[e] * bf16_lo(rk[y][e]), qhi[e] * bf16_hi(rk[y][e]));
-        b4[e] = pack_bf16x2(olo[e] * bf16_lo(rv[y][e]), ohi[e] * bf16_hi(rv[y][e]));
-      }
-      *reinterpret_cast<u32x4_t*>(buf + T::off(p_ + 16 * y, dc)) = a4;
-      *reinterpret_cast<u32x4_t*>(buf + T::bytes + T::off(p_ + 16 * y, dc)) = b4;
-    }
-  };
-
-  // Per-row-block statistics, 64 row blocks at a time: lane l holds
-  // -lse * log2(e) and Delta of row block (rb & ~63) + l; each iteration
-  // takes its pair with a lane read instead of a scalar load, which would
-  // share the LDS completion counter and serialise the fragment reads.
-  float st_l = 0.f, dl_l = 0.f;
-
-  if (nrb > 0) {
-    fetch(0);
-    form_put(smem);
-  }
-  __syncthreads();
-  for (int rb = 0; rb < nrb; ++rb) {
-    const int cur = rb & 1;
-    const int i = j0 + rb / G, g = rb - (rb / G) * G;
-    if ((rb & 63) == 0) {
-      const int ii = min(j0 + (rb + lane) / G, N - 1);
-      st_l = -lse[stat + ii] * kLog2e;
-      dl_l = delta[stat + ii];
-    }
-    // The last iteration fetches and forms one row block past the end: its
-    // loads are out of range (zeros) or harmless, and the buffer it fills is
-    // never read. This keeps the loop body free of branches around the work.
-    fetch(rb + 1);
-    // Keep the loads here, a whole row block ahead of their use.
-    __builtin_amdgcn_sched_barrier(0);
-    const float nl2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, st_l), rb & 63));
-    const float dlt = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, dl_l), rb & 63));
-    char* nbuf = smem + (cur ^ 1) * L::bufBytes;
-    // Every wavefront runs every row block: the workgroup advances in
-    // lockstep, so one whose keys miss query i's window would only wait at
-    // the barrier; its key columns are masked below and contribute zeros.
-    const char* qtile = smem + cur * L::bufBytes;
-    const char* otile = qtile + T::bytes;
-
-    // (1) Logits S = q~ K^T, with the transposing reads for dV queued behind.
-    u32x4_t qa[NT], oa[NT];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) qa[t] = frag_row_swz<D>(qtile, c, h, t);
-#pragma unroll
-    for (int t = 0; t < NT; ++t) oa[t] = frag_row_swz<D>(otile, c, h, t);
-    u32x4_t otr[2][NDT], qtr[2][NDT];
-    f32x16_t sacc = f32x16_t{}, pacc = f32x16_t{};
-#pragma unroll
-    for (int t = 0; t < NT; ++t) sacc = mfma32(qa[t], kf[t], sacc);
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) otr[u][dt] = frag_tr_swz<D>(otile, lane, dt, u);
-    __builtin_amdgcn_sched_group_barrier(0x100, 2 * NT, 0);
-#pragma unroll
-    for (int x = 0; x < NT; ++x) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 4 * NDT / NT, 0);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-
-    // (2) dP = do~ V^T, overlapped with the probabilities. Keys outside
-    // query i's window get an infinite log-normaliser, so their P (and dS)
-    // is exactly 0. Rows with k outside the window hold zero operands; their
-    // P is exp2(-lse2), finite unless the normaliser is tiny, so the
-    // exponent is clamped at 0 (valid probabilities never exceed 1).
-#pragma unroll
-    for (int t = 0; t < NT; ++t) pacc = mfma32(oa[t], vf[t], pacc);
-    const bool colok = jme <= i && jme > i - w1 && jme < N;
-    const float nlse2 = nl2 - (colok ? 0.f : __builtin_inff());
-    float pr[16];
-#pragma unroll
-    for (int vv = 0; vv < 16; ++vv) pr[vv] = fast_exp2(fminf(__builtin_fmaf(sacc[vv], qscale, nlse2), 0.f));
-    u32x4_t pf[2], df[2];
-#pragma unroll
-    for (int u = 0; u < 2; ++u) pf[u] = pack_frag(pr, u);
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) qtr[u][dt] = frag_tr_swz<D>(qtile, lane, dt, u);
-#pragma unroll
-    for (int x = 0; x < NT; ++x) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 4 * NDT / NT, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-
-    // (3) dV += P^T do~, overlapped with dS = P (dP - Delta).
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) adv[dt] = mfma32(pf[u], otr[u][dt], adv[dt]);
-#pragma unroll
-    for (int vv = 0; vv < 16; ++vv) pr[vv] *= pacc[vv] - dlt;
-#pragma unroll
-    for (int u = 0; u < 2; ++u) df[u] = pack_frag(pr, u);
-#pragma unroll
-    for (int x = 0; x < 2 * NDT; ++x) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-
-    // (4) dK += dS^T q~, overlapped with forming the next row block's tiles.
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) adk[dt] = mfma32(df[u], qtr[u][dt], adk[dt]);
-    form_put(nbuf);
-#pragma unroll
-    for (int x = 0; x < 2 * NDT; ++x) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 12, 0);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    lds_barrier();
-  }
-
-  // ---- store: accumulator rows are keys, lanes are columns d ----
-  float* ob = reinterpret_cast<float*>(smem) + wave * 32 * L::oStride;
-  const float kscale = s.scale;  // q~ = q * k' is formed unscaled
-#pragma unroll
-  for (int pass = 0; pass < 2; ++pass) {
-#pragma unroll
-    for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-      for (int vv = 0; vv < 16; ++vv)
-        ob[acc_row(vv, h) * L::oStride + 32 * dt + c] = pass == 0 ? adk[dt][vv] * kscale : adv[dt][vv];
-    __syncthreads();
-    uint16_t* dst = pass == 0 ? dk : dv;
-    constexpr int CH = D / 8;
-    for (int x = lane; x < 32 * CH; x += 64) {
-      const int row = x / CH, col = x % CH;
-      const int j = jw + row;
-      if (j < N) {
-        const float* src = ob + row * L::oStride + 8 * col;
-        u32x4_t w;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(src[2 * e], src[2 * e + 1]);
-        *reinterpret_cast<u32x4_t*>(dst + base + static_cast<size_t>(j) * rs + 8 * col) = w;
-      }
-    }
-    __syncthreads();
-  }
-}
-
 template <int D, int G>
 hipError_t launch_stage(const Shape& s, BwdStage stage, const void* q, const void* k, const void* kp,
                         const void* v, const void* vp, const void* dout, const float* lse, void* g0,
@@ -881,10 +615,7 @@ hipError_t launch_stage(const Shape& s, BwdStage stage, const void* q, const voi
                          0, st, s, plan, halo, static_cast<uint16_t*>(g1), static_cast<uint16_t*>(g2));
     }
   } else {
-    const long totkv = static_cast<long>((s.N + 127) / 128) * s.B * s.H;
-    hipLaunchKernelGGL((bwd_kv_kernel<D, G>), dim3(static_cast<unsigned>(((totkv + 7) / 8) * 8)),
-                       dim3(256), 0, st, s, Q, K, KP, V, VP, DO, lse, delta,
-                       static_cast<uint16_t*>(g0), static_cast<uint16_t*>(g1));
+    return mfma_bwd_key(s, Q, K, KP, V, VP, DO, lse, delta, g0, g1, st);
   }
   return hipGetLastError();
 }

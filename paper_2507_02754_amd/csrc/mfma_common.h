@@ -117,6 +117,23 @@ __device__ __forceinline__ u32x2_t ds_read_tr16(const char* p) {
   return __builtin_bit_cast(u32x2_t, v);
 }
 
+// Typed access through LDS-address-space pointers: offsets added to such a
+// pointer fold into the DS instructions' immediate offset field.
+typedef __attribute__((address_space(3))) char lds_char;
+__device__ __forceinline__ lds_char* to_lds(char* p) { return (lds_char*)(p); }
+template <typename V>
+__device__ __forceinline__ V lds_ld(const lds_char* p) {
+  return *reinterpret_cast<const __attribute__((address_space(3))) V*>(p);
+}
+template <typename V>
+__device__ __forceinline__ void lds_st(lds_char* p, V v) {
+  *reinterpret_cast<__attribute__((address_space(3))) V*>(p) = v;
+}
+__device__ __forceinline__ u32x2_t lds_tr16(const lds_char* p) {
+  const s16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t*)(p));
+  return __builtin_bit_cast(u32x2_t, v);
+}
+
 // Transposed fragment from a row-major swizzled tile: lane (h, c) gets column
 // 32 dt + c, K-slot e of half h = row 16u + 8(e/4) + 4h + e%4 (the order the
 // 32x32 accumulator produces). Two ds_read_b64_tr_b16: within each group of 16

@@ -64,6 +64,11 @@ hipError_t mfma_bwd_stage(const Shape& s, BwdStage stage, const void* q, const v
                           const float* lse, void* g0, void* g1, void* g2, void* workspace,
                           hipStream_t st);
 
+// Key-side backward stage of the MFMA path (dK, dV) given Delta.
+hipError_t mfma_bwd_key(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
+                        const void* vp, const void* dout, const float* lse, const float* delta,
+                        void* dk, void* dv, hipStream_t st);
+
 // Delta_i = <dO_i, O_i> for every query, [B, H, N] float32.
 hipError_t launch_delta(const Shape& s, const void* out, const void* dout, float* delta,
                         hipStream_t st);
