@@ -602,7 +602,15 @@ hipError_t launch_stage(const Shape& s, BwdStage stage, const void* q, const voi
   const auto* V = static_cast<const uint16_t*>(v);
   const auto* VP = static_cast<const uint16_t*>(vp);
   const auto* DO = static_cast<const uint16_t*>(dout);
-  if (stage == BwdStage::Query) {
+  if (stage == BwdStage::Query && mfma_bwd_query_supported(s)) {
+    const hipError_t e = mfma_bwd_query(s, plan, Q, K, KP, V, VP, DO, lse, delta, g0, g1, g2, halo, st);
+    if (e != hipSuccess) return e;
+    if (plan.nchunks > 1) {
+      const long n = static_cast<long>(s.B) * s.H * (plan.nchunks - 1) * (plan.W2P - 1) * D;
+      hipLaunchKernelGGL(halo_fixup_kernel<D>, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256),
+                         0, st, s, plan, halo, static_cast<uint16_t*>(g1), static_cast<uint16_t*>(g2));
+    }
+  } else if (stage == BwdStage::Query) {
     constexpr int WAVES = 4;
     const long totq = static_cast<long>(plan.nchunks) * s.B * s.H;
     hipLaunchKernelGGL((bwd_q_kernel<D, G, WAVES>), dim3(static_cast<unsigned>(((totq + 7) / 8) * 8)),

@@ -150,6 +150,46 @@ __device__ __forceinline__ u32x4_t frag_tr_swz(const char* tile, int lane, int d
   return u32x4_t{a[0], a[1], b[0], b[1]};
 }
 
+// ---- fragment-major tiles in LDS ----
+//
+// A tile holds 32 rows of D bf16. The 16-byte chunk ch = 2t + hc of row r
+// (columns 8ch .. 8ch + 7) is stored in 1 KB block t at lane slot
+// 32 hc + (r ^ (4 hc + 8 (t & 1))). This layout gives:
+//   * row fragments (lane (h, c): row c, columns 16t + 8h .. + 7) as one
+//     ds_read_b128 per lane at a per-lane base (two bases, by t parity) plus
+//     the immediate 1024 t, the 64 lanes hitting 64 distinct 16-byte slots;
+//   * transposed fragments through ds_read_b64_tr_b16 at two per-lane bases
+//     plus immediates (2048 dt + 256 u), each half-wavefront covering all 64
+//     banks once;
+//   * staging stores of 4 (D = 128) or 8 (D = 64) full rows per wavefront
+//     instruction that touch every bank equally (the minimum LDS cycles).
+template <int D>
+struct FragTile {
+  static constexpr int CH = D / 8;  // 16-byte chunks per row
+  static constexpr int bytes = 32 * D * 2;
+  static constexpr int instrs = 32 * CH / 64;  // 64-lane x 16-byte transfers per tile
+  __device__ static __forceinline__ int slot(int r, int ch) {
+    const int t = ch >> 1, hc = ch & 1;
+    return t * 1024 + (32 * hc + (r ^ (4 * hc + 8 * (t & 1)))) * 16;
+  }
+  // Row fragment t of lane (h, c) is at row_base(p = t & 1) + 1024 t.
+  __device__ static __forceinline__ int row_base(int lane, int p) {
+    const int c = lane & 31, h = lane >> 5;
+    return (32 * h + (c ^ (4 * h + 8 * p))) * 16;
+  }
+  // Transposed fragment (dt, u): two ds_read_b64_tr_b16 at tr_base(lane, 0)
+  // and tr_base(lane, 1), each plus 2048 dt + 256 u. Lane (h, c) receives
+  // column 32 dt + c, K-slot e of half h = row 16u + 8(e/4) + 4h + e%4 (the
+  // accumulator's row order): within a 16-lane group (grp = lane / 16), lane s
+  // addresses row 16u + 4(grp/2) + s/4 (+ 8 for the second read), columns
+  // 32 dt + 16(grp%2) + 4(s%4) .. + 3.
+  __device__ static __forceinline__ int tr_base(int lane, int second) {
+    const int grp = lane >> 4, sl = lane & 15;
+    const int p = grp & 1, hg = grp >> 1, hd = (sl >> 1) & 1, x = sl >> 2;
+    return 1024 * p + 512 * hd + (4 * (hg ^ hd) + x) * 16 + 8 * (sl & 1) + 128 * (second ^ p);
+  }
+};
+
 // Waits for this wavefront's LDS operations, then synchronises the
 // workgroup. Volatile asm with a memory clobber so the compiler keeps LDS
 // accesses on their side of it, and without the vmcnt(0) wait that

@@ -69,6 +69,14 @@ hipError_t mfma_bwd_key(const Shape& s, const void* q, const void* k, const void
                         const void* vp, const void* dout, const float* lse, const float* delta,
                         void* dk, void* dv, hipStream_t st);
 
+// Query-side backward stage for w2 <= 32 (dq, dk', dv' and the chunk-boundary
+// partial sums in `halo`; the fix-up kernel runs afterwards).
+bool mfma_bwd_query_supported(const Shape& s);
+hipError_t mfma_bwd_query(const Shape& s, const BwdPlan& plan, const void* q, const void* k,
+                          const void* kp, const void* v, const void* vp, const void* dout,
+                          const float* lse, const float* delta, void* dq, void* dkp, void* dvp,
+                          float* halo, hipStream_t st);
+
 // Delta_i = <dO_i, O_i> for every query, [B, H, N] float32.
 hipError_t launch_delta(const Shape& s, const void* out, const void* dout, float* delta,
                         hipStream_t st);
