@@ -167,9 +167,8 @@ __global__ __launch_bounds__(kQThreads, 1) void bwd_query_kernel(
   }
 
   // ---- K/V blocks: one staging pipeline over (query tile, 32-key block) ----
-  // Wavefront w < F::instrs moves rows of the K and V tiles of a block, 16
-  // bytes per lane (row p / CH, chunk p % CH for p = 64 w + lane), into the
-  // fragment-major layout; block `it` goes into stage it % NS.
+  // Wavefronts w < F::instrs move the K and V tiles of a block, 16 bytes per
+  // lane, into the fragment-major layout; block `it` goes into stage it % NS.
   using F = FragTile<D>;
   const int nb = (w1 + QW - 1 + 31) / 32;
   const int ntiles = (ce - cs + QW - 1) / QW;
@@ -270,6 +269,9 @@ __global__ __launch_bounds__(kQThreads, 1) void bwd_query_kernel(
     }
   };
 
+  // Per-query statistic of this wavefront's query (A: LSE, B: Delta), loaded
+  // one tile ahead.
+  float st_cur = (roleA ? lse : delta)[stat + min(cs + qs, N - 1)];
   if (roleA) {
     u32x4_t qt[NT];
     f32x16_t au[NDT];
@@ -282,7 +284,8 @@ __global__ __launch_bounds__(kQThreads, 1) void bwd_query_kernel(
       const bool rowvalid = qvalid && kk >= 0 && kk > i - w2;
       const int jlo = i0 - w1 + 1;
       // Rows outside the window get an infinite normaliser: P = 0.
-      const float lse2 = rowvalid ? lse[stat + min(i, N - 1)] * kLog2e : __builtin_inff();
+      const float lse2 = rowvalid ? st_cur * kLog2e : __builtin_inff();
+      if (tile + 1 < ntiles) st_cur = lse[stat + min(i + QW, N - 1)];  // next tile's, ahead of use
       const u32x4_t nrow = row_load(rowloader && tile + 1 < ntiles ? i0 + QW : -RL - 1);
       {
         const int kslot = (kk - kbase) % RK;
@@ -397,7 +400,8 @@ __global__ __launch_bounds__(kQThreads, 1) void bwd_query_kernel(
       const int kk = i - W2P + 1 + c;
       const bool qvalid = i < ce;
       const bool rowvalid = qvalid && kk >= 0 && kk > i - w2;
-      const float dlt = qvalid ? delta[stat + min(i, N - 1)] : 0.f;
+      const float dlt = qvalid ? st_cur : 0.f;
+      if (tile + 1 < ntiles) st_cur = delta[stat + min(i + QW, N - 1)];  // next tile's, ahead of use
       const u32x4_t nrow = row_load(rowloader && tile + 1 < ntiles ? i0 + QW : -RL - 1);
       const int kslot = (kk - kbase) % RK;
       const char* krow = kring + kslot * 2 * D;
