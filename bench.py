@@ -185,7 +185,7 @@ def main():
     # Roofline of the dominant kernel: algorithmic FLOPs per launch / its time.
     algo = {
         "fwd": ("fwd_mfma_kernel", 4 * unit),
-        "bwd_query_side": ("bwd_q_kernel", 8 * unit),   # S recompute, dP, dQ~, U~
+        "bwd_query_side": ("bwd_query_kernel", 8 * unit),   # S recompute, dP, dQ~, U~
         "bwd_key_side": ("bwd_key_kernel", 4 * unit),    # dV, dK (its S/dP recompute is not counted)
     }
     dom = max(algo, key=lambda p: ms[p])

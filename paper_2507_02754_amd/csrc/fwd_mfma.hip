@@ -16,19 +16,29 @@
 // Tiling. A workgroup of 4 wavefronts owns QW consecutive queries of one
 // (batch, head); each wavefront owns 32 rows (one query's 32 k-rows; w2 = 64
 // uses two wavefronts per query). All accumulators live in VGPRs so that two
-// workgroups share a CU (two wavefronts per SIMD): one's exponentials overlap
-// the other's matrix products. The j-window union of the workgroup is walked
-// in 32-key blocks. K and V blocks are loaded into registers (16 bytes per
-// lane, buffer loads whose range check zero-fills rows outside [0, N)) two
-// blocks ahead and written one block ahead into a 2-stage ring of swizzled
-// row-major LDS tiles. (Loads with an LDS destination measured slower here:
-// their issue stalled the wavefront for hundreds of cycles per block.) K
-// fragments are read row-wise; V fragments are read with the gfx950
-// transposing LDS read, so V needs no transposed copy.
-// Within a wavefront all rows share one query, so a block is skipped, fully
-// valid, or masked by column only. The running maximum is rescaled lazily: only when some row's
-// block maximum exceeds it by more than 2^8 (p stays <= 256, exact in fp32 and
-// bf16 range), which after the first blocks is rare.
+// workgroups share a CU (two wavefronts per SIMD). The j-window union of the
+// workgroup is walked in 32-key blocks through a 4-stage ring of swizzled
+// row-major K/V tiles in LDS; K fragments are read row-wise, V fragments with
+// the gfx950 transposing LDS read (no transposed copy of V).
+//
+// Pipeline. K and V blocks go from HBM/L2 straight into LDS (buffer loads
+// with an LDS destination, 16 bytes per lane), each into its own 4-stage
+// ring, so no VGPRs are spent on staging and the loads run 2-3 iterations
+// ahead. Iteration n of the loop
+//   - issues the loads of K(n+4) and V(n+3),
+//   - masks and takes the running maximum of S(n), exponentiates and packs
+//     P(n), while the matrix cores compute S(n+1) from K fragments that were
+//     read one iteration earlier,
+//   - accumulates P(n) V(n) while the K fragments of block n+2 are read.
+// The iteration is unrolled over the 4 ring stages so every LDS address is a
+// per-lane base plus an immediate; each stage is a separate LDS array so the
+// compiler's wait for a stage's loads does not also wait for the others. Within a wavefront all rows share one
+// query, so a block is fully valid or masked by column only; masked columns
+// are set to -inf before the maximum.
+// The running maximum is rescaled lazily: only when some row's block maximum
+// exceeds it by more than 2^8 (p stays <= 256, exact in fp32 and bf16 range),
+// which after the first blocks is rare. The row sum l adds the bf16-rounded
+// p that the P V product consumes, so O is a convex combination of V rows.
 // Rows with k < 0 or k <= i - w2 get q~ = 0 and weight 0 in the merge.
 #include "mfma_common.h"
 
@@ -37,20 +47,22 @@ namespace {
 
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
+constexpr int kStages = 4;
 constexpr float kLazyRescale = 8.0f;  // log2 headroom before the running max is raised
 
-template <int D, int NS>
-struct FwdLds {
-  using T = SwzTile<D>;
-  static constexpr int stageBytes = 2 * T::bytes;  // K tile + V tile of one 32-key block
-  static constexpr int mainBytes = NS * stageBytes;  // also the epilogue's exchange area
-  static constexpr int statOff = mainBytes;
-  static constexpr int bytes = statOff + kWaves * 32 * 4;
-};
+template <int X>
+using IC = std::integral_constant<int, X>;
 
-// NS = stages of the ring of 32-key K/V blocks in LDS (2 suffices: a block is
-// written one block before it is read, into the stage read two blocks ago).
-template <int D, int G, int NS>
+// s_waitcnt vmcnt(N) with the other counters left alone (gfx9 encoding:
+// vmcnt low bits 3:0, high bits 15:14; expcnt 6:4 = 7, lgkmcnt 11:8 = 15).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+}
+
+
+template <int D, int G>
 __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const uint16_t* __restrict__ q,
                                                                const uint16_t* __restrict__ k,
                                                                const uint16_t* __restrict__ kp,
@@ -62,10 +74,23 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
   constexpr int NDT = D / 32;    // 32-wide d tiles of the output product
   constexpr int QW = kWaves / G; // queries per workgroup
   constexpr int W2P = 32 * G;    // rows per query (w2 padded up to a multiple of 32)
-  using L = FwdLds<D, NS>;
-  using T = typename L::T;
-  __shared__ __attribute__((aligned(16))) char smem[L::bytes];
-  float* stat = reinterpret_cast<float*>(smem + L::statOff);
+  using T = SwzTile<D>;
+  __shared__ __attribute__((aligned(16))) char kst0[T::bytes], kst1[T::bytes], kst2[T::bytes], kst3[T::bytes];
+  __shared__ __attribute__((aligned(16))) char vst0[T::bytes], vst1[T::bytes], vst2[T::bytes], vst3[T::bytes];
+  // v'_k rows kk0 .. kk0 + 34 of the workgroup's queries (w2 <= 32), rows of
+  // 2D bytes with the 16-byte chunk ch of row r at slot ch ^ (r % CH).
+  constexpr int VPR = ((35 * T::CH + 63) / 64 * 64) / T::CH;
+  __shared__ __attribute__((aligned(16))) char vpt[G == 1 ? VPR * 2 * D : 16];
+  __shared__ float stat[G == 1 ? 1 : kWaves * 32];
+  __shared__ float xchg[G == 1 ? 1 : kWaves * 64 * (D / 64)];
+  auto kst = [&](auto SC) __attribute__((always_inline)) {
+    constexpr int X = decltype(SC)::value;
+    return to_lds(X == 0 ? kst0 : X == 1 ? kst1 : X == 2 ? kst2 : kst3);
+  };
+  auto vst = [&](auto SC) __attribute__((always_inline)) {
+    constexpr int X = decltype(SC)::value;
+    return to_lds(X == 0 ? vst0 : X == 1 ? vst1 : X == 2 ? vst2 : vst3);
+  };
 
   // XCD-aware tile order: hardware deals workgroups round-robin over the 8
   // XCDs; remap so each XCD walks a contiguous run of tiles of one head and
@@ -93,53 +118,84 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
   const bool rowvalid = qvalid && kk >= 0 && kk > i - w2;
   const float qscale = s.scale * kLog2e;
 
-  // ---- main loop over 32-key blocks of the workgroup's window union ----
   const int jlo = i0 - w1 + 1;
   const int nb = (w1 + QW - 1 + 31) / 32;
   const int rsb = static_cast<int>(rs) * 2;
   const __amdgpu_buffer_rsrc_t rk = make_rsrc(k + base, head_bytes(N, rsb, D));
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(v + base, head_bytes(N, rsb, D));
-  f32x16_t acc[NDT];
-#pragma unroll
-  for (int dt = 0; dt < NDT; ++dt) acc[dt] = f32x16_t{};
-  // Running row maximum m (log2 units). The logit products start from -m_used
-  // in the accumulator, so they come out already shifted; m_used == m except
-  // before the first block and inside a block where m was raised.
-  float m = -INFINITY, l = 0.f, m_used = 0.f;
-  f32x16_t negm = f32x16_t{};
 
-  // K/V blocks are staged through registers: fetch loads this wavefront's
-  // share of a block (16 bytes per lane per load, the chunk that belongs at
-  // LDS offset 1024 k + 16 lane of the swizzled tile; rows outside [0, N)
-  // come back as zeros from the buffer range check), put writes it into a
-  // ring stage one block later.
+  // Per-lane LDS byte offsets inside a tile. K row fragment t: row c,
+  // columns 16t + 8h .. + 7. Transposed V fragment (dt, u): two
+  // ds_read_b64_tr_b16 at vo[dt][0] and vo[dt][1] plus 32 D u (16 rows on).
+  int ko[NT], vo[NDT][2];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) ko[t] = T::off(c, 2 * t + h);
+  {
+    const int grp = lane >> 4, sl = lane & 15;
+    const int r0 = 4 * (grp >> 1) + (sl >> 2);
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) {
+      const int col = 32 * dt + 16 * (grp & 1) + 4 * (sl & 3);
+      const int ch = col >> 3, within = (col & 7) * 2;
+      vo[dt][0] = T::off(r0, ch) + within;
+      vo[dt][1] = T::off(r0 + 8, ch) + within;
+    }
+  }
+  auto kfrag = [&](auto SC, int t) __attribute__((always_inline)) {
+    return lds_ld<u32x4_t>(kst(SC) + ko[t]);
+  };
+  auto vfrag = [&](auto SC, int dt, int u) __attribute__((always_inline)) {
+    const lds_char* p = vst(SC) + 32 * D * u;
+    const u32x2_t a = lds_tr16(p + vo[dt][0]);
+    const u32x2_t bb = lds_tr16(p + vo[dt][1]);
+    return u32x4_t{a[0], a[1], bb[0], bb[1]};
+  };
+
+  // Block loads: wavefront x-th share of a 32 x D tile is the 1 KB at
+  // 1024 (x kWaves + wave) of the tile, lane l supplying the 16-byte chunk at
+  // offset 16 l of it (row p / CH, swizzled chunk of p = 64 (x kWaves + wave)
+  // + l). The hardware writes lane l's chunk to the LDS address given plus
+  // 16 l. Rows outside [0, N) are loaded from the clamped row: they are
+  // masked (p = 0), and finite data keeps 0 * v finite.
   constexpr int SPW = (T::instrs + kWaves - 1) / kWaves;  // loads per tile per wavefront
-  u32x4_t skr[SPW], svr[SPW];
-  auto fetch = [&](int blk) {
+  int lrow[SPW], lcol[SPW];
+#pragma unroll
+  for (int x = 0; x < SPW; ++x) {
+    const int kx = x * kWaves + wave;
+    const int p = 64 * kx + lane;
+    lrow[x] = p / T::CH;
+    lcol[x] = 16 * ((p % T::CH) ^ T::swz(lrow[x]));
+  }
+  auto load_tile = [&](__amdgpu_buffer_rsrc_t r, lds_char* dst, int blk) __attribute__((always_inline)) {
     const int jb = jlo + 32 * blk;
 #pragma unroll
     for (int x = 0; x < SPW; ++x) {
       const int kx = x * kWaves + wave;
-      const int p = 64 * kx + lane;
-      const int row = p / T::CH, ch = (p % T::CH) ^ T::swz(row);
-      const int off = kx < T::instrs ? (jb + row) * rsb + 16 * ch : -1;
-      skr[x] = ldbuf128(rk, off);
-      svr[x] = ldbuf128(rv, off);
+      const int row = min(max(jb + lrow[x], 0), N - 1);
+      if (T::instrs % kWaves == 0 || kx < T::instrs) load_lds16(r, dst + 1024 * kx, row * rsb + lcol[x]);
     }
   };
-  auto put = [&](char* st) {
+  // Blocks 0-3 of K and 0-2 of V go out before the q~ loads, so their
+  // latencies overlap (blocks past the window only cost the loads).
+  load_tile(rk, kst(IC<0>{}), 0);
+  load_tile(rk, kst(IC<1>{}), 1);
+  load_tile(rk, kst(IC<2>{}), 2);
+  load_tile(rk, kst(IC<3>{}), 3);
+  load_tile(rv, vst(IC<0>{}), 0);
+  load_tile(rv, vst(IC<1>{}), 1);
+  load_tile(rv, vst(IC<2>{}), 2);
+  const __amdgpu_buffer_rsrc_t rvp = make_rsrc(vp + base, head_bytes(N, rsb, D));
+  if constexpr (G == 1) {
+    constexpr int VI = VPR * T::CH / 64;  // 64-lane loads of the v' tile
+    const int kk0 = i0 - 31;
 #pragma unroll
-    for (int x = 0; x < SPW; ++x) {
-      const int kx = x * kWaves + wave;
-      if (kx < T::instrs) {
-        *reinterpret_cast<u32x4_t*>(st + 1024 * kx + 16 * lane) = skr[x];
-        *reinterpret_cast<u32x4_t*>(st + T::bytes + 1024 * kx + 16 * lane) = svr[x];
-      }
+    for (int x = wave; x < VI; x += kWaves) {
+      const int p = 64 * x + lane, r = p / T::CH;
+      const int ch = (p % T::CH) ^ (r % T::CH);
+      const int row = min(max(kk0 + r, 0), N - 1);
+      load_lds16(rvp, to_lds(vpt) + 1024 * x, row * rsb + 16 * ch);
     }
-  };
-  // The first block's K/V loads go out before the q~ loads, so their
-  // latencies overlap.
-  fetch(0);
+  }
 
   // ---- modulated queries q~ = (scale*log2 e) * q_i o k'_k as B operands ----
   // (rows outside the window or the sequence load as zeros: offset -1)
@@ -160,97 +216,137 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
         qt[t][e] = pack_bf16x2(bf16_lo(qa[t][e]) * bf16_lo(ka[t][e]) * qscale,
                                bf16_hi(qa[t][e]) * bf16_hi(ka[t][e]) * qscale);
   }
-  put(smem);
-  if (nb > 1) fetch(1);
 
-  for (int blk = 0; blk < nb; ++blk) {
+  f32x16_t acc[NDT];
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt) acc[dt] = f32x16_t{};
+  // Running row maximum m and sum l (log2 units; logits come out of the
+  // products unshifted and p = 2^(s - m)). m starts finite so that a block
+  // masked entirely (s = -inf) before any valid one gives p = 0, not NaN;
+  // the first block with a valid column always raises it.
+  float m = -1e30f, l = 0.f;
+  f32x16_t sc[2];
+  u32x4_t kf[NT];
+  auto logits = [&](f32x16_t& dst) __attribute__((always_inline)) {
+    dst = mfma32(kf[0], qt[0], f32x16_t{});
+#pragma unroll
+    for (int t = 1; t < NT; ++t) dst = mfma32(kf[t], qt[t], dst);
+  };
+
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wavefront's block loads are in LDS
+  lds_barrier();
+#pragma unroll
+  for (int t = 0; t < NT; ++t) kf[t] = kfrag(IC<0>{}, t);
+  logits(sc[0]);
+#pragma unroll
+  for (int t = 0; t < NT; ++t) kf[t] = kfrag(IC<1>{}, t);
+
+  const bf16x2_t ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+  auto iteration = [&](auto SC, int blk) __attribute__((always_inline)) {
+    constexpr int S = decltype(SC)::value;  // ring stage of block blk
+    constexpr int cur = S & 1, nxt = cur ^ 1;
+    // K(blk + 2) (loaded in iteration blk - 2) and V(blk) (iteration
+    // blk - 3) must be in LDS for every wavefront: wait until at most the
+    // 3 SPW loads issued after K(blk + 2) are in flight, then synchronise.
+    wait_vmcnt<3 * SPW>();
     lds_barrier();
-    // Block blk + 1 goes into its stage (last read in block blk - 1, which
-    // every wavefront finished before the barrier), then block blk + 2 is
-    // fetched into the registers.
-    if (blk + 1 < nb) put(smem + ((blk + 1) % NS) * L::stageBytes);
-    if (blk + 2 < nb) fetch(blk + 2);
-    const char* kt = smem + (blk % NS) * L::stageBytes;
-    const char* vt = kt + T::bytes;
+    // K(blk + 4) replaces K(blk), read in iteration blk - 2; V(blk + 3)
+    // replaces V(blk - 1), read in iteration blk - 1.
+    if (blk + 4 < nb) load_tile(rk, kst(IC<S>{}), blk + 4);
+    if (blk + 3 < nb) load_tile(rv, vst(IC<(S + 3) % kStages>{}), blk + 3);
 
     // Valid block-local columns of this wavefront's query.
     const int lo = max(qs, -jlo) - 32 * blk;
     const int hi = min(qs + w1 - 1, N - 1 - jlo) - 32 * blk;
-    if (qvalid && hi >= 0 && lo <= 31 && lo <= hi) {
-      u32x4_t kf[NT];
-#pragma unroll
-      for (int t = 0; t < NT; ++t) kf[t] = frag_row_swz<D>(kt, c, h, t);
-      f32x16_t sacc = mfma32(kf[0], qt[0], negm);
-#pragma unroll
-      for (int t = 1; t < NT; ++t) sacc = mfma32(kf[t], qt[t], sacc);
-      const float m_blk = m_used;
-      float sv[16];
-#pragma unroll
-      for (int vv = 0; vv < 16; ++vv) sv[vv] = sacc[vv];
-      if (lo > 0 || hi < 31) {
-#pragma unroll
-        for (int vv = 0; vv < 16; ++vv) {
-          const int jl = acc_row(vv, h);
-          if (jl < lo || jl > hi) sv[vv] = -INFINITY;
-        }
-      }
-      float mx = fmaxf(sv[0], sv[1]);
-#pragma unroll
-      for (int vv = 2; vv < 16; vv += 2) mx = fmaxf(fmaxf(mx, sv[vv]), sv[vv + 1]);
-      mx = fmaxf(mx, swap_halves(mx)) + m_blk;
-      if (__builtin_amdgcn_ballot_w64(mx > m + kLazyRescale) != 0) {
-        const float mnew = fmaxf(m, mx);
-        const float alpha = fast_exp2(m - mnew);
-        l *= alpha;
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) acc[dt] *= alpha;
-        m = mnew;
-        m_used = mnew;
-        const float off = m_blk - mnew;
-#pragma unroll
-        for (int vv = 0; vv < 16; ++vv) {
-          sv[vv] += off;
-          negm[vv] = -mnew;
-        }
-      }
+    if (lo > 0 || hi < 31) {
 #pragma unroll
       for (int vv = 0; vv < 16; ++vv) {
-        sv[vv] = fast_exp2(sv[vv]);
-        l += sv[vv];
-      }
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const u32x4_t pf = pack_frag(sv, u);
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) acc[dt] = mfma32(frag_tr_swz<D>(vt, lane, dt, u), pf, acc[dt]);
+        const int jl = acc_row(vv, h);
+        if (jl < lo || jl > hi) sc[cur][vv] = -INFINITY;
       }
     }
+    float mx = fmaxf(sc[cur][0], sc[cur][1]);
+#pragma unroll
+    for (int vv = 2; vv < 16; vv += 2) mx = fmaxf(fmaxf(mx, sc[cur][vv]), sc[cur][vv + 1]);
+    mx = fmaxf(mx, swap_halves(mx));
+    if (__builtin_amdgcn_ballot_w64(mx > m + kLazyRescale) != 0) {
+      const float mnew = fmaxf(m, mx);
+      const float alpha = fast_exp2(m - mnew);
+      l *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) acc[dt] *= alpha;
+      m = mnew;
+    }
+    // P(blk) on the vector units while the matrix cores form S(blk + 1).
+    logits(sc[nxt]);
+    u32x4_t pf[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const unsigned pp = pack_bf16x2(fast_exp2(sc[cur][8 * u + 2 * e] - m), fast_exp2(sc[cur][8 * u + 2 * e + 1] - m));
+        pf[u][e] = pp;
+        l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pp), ones, l, false);
+      }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      u32x4_t vf[NDT];
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) vf[dt] = vfrag(SC, dt, u);
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) acc[dt] = mfma32(vf[dt], pf[u], acc[dt]);
+    }
+    // K fragments of block blk + 2 (stage written in iteration blk - 1).
+#pragma unroll
+    for (int t = 0; t < NT; ++t) kf[t] = kfrag(IC<(S + 2) % kStages>{}, t);
+  };
+  for (int b0 = 0; b0 < nb; b0 += kStages) {
+    iteration(IC<0>{}, b0);
+    if (b0 + 1 < nb) iteration(IC<1>{}, b0 + 1);
+    if (b0 + 2 < nb) iteration(IC<2>{}, b0 + 2);
+    if (b0 + 3 < nb) iteration(IC<3>{}, b0 + 3);
   }
   // ---- epilogue: merge the k-rows of each query (log-sum-exp), apply v'_k ----
   // v'_k of this lane's row in the accumulator layout (d = 32 dt + 8 (v/4) +
-  // 4 h + v%4), loaded first so the merge below covers their latency.
-  const __amdgpu_buffer_rsrc_t rvp = make_rsrc(vp + base, head_bytes(N, rsb, D));
+  // 4 h + v%4): from the LDS tile when w2 <= 32, else loaded here, before the
+  // merge below covers their latency.
   u32x2_t vpr[4 * NDT];
+  if constexpr (G == 1) {
+    const int r = qs + c;
+    const lds_char* vrow = to_lds(vpt) + r * 2 * D + 8 * h;
 #pragma unroll
-  for (int dt = 0; dt < NDT; ++dt)
+    for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-    for (int qd = 0; qd < 4; ++qd)
-      vpr[4 * dt + qd] = ldbuf64(rvp, rowvalid ? kk * rsb + 2 * (32 * dt + 8 * qd + 4 * h) : -1);
+      for (int qd = 0; qd < 4; ++qd) vpr[4 * dt + qd] = lds_ld<u32x2_t>(vrow + 16 * ((4 * dt + qd) ^ (r % T::CH)));
+  } else {
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int qd = 0; qd < 4; ++qd)
+        vpr[4 * dt + qd] = ldbuf64(rvp, rowvalid ? kk * rsb + 2 * (32 * dt + 8 * qd + 4 * h) : -1);
+  }
   const float lsum = l + swap_halves(l);
   const float lse2_row = rowvalid ? m + fast_log2(lsum) : -INFINITY;
-  if (h == 0) stat[wave * 32 + c] = lse2_row;
-  lds_barrier();  // also: every wavefront is past its last K/V stage reads
-  float mq = -INFINITY;
+  float mq, z;
+  if constexpr (G == 1) {
+    // All 32 rows of the query are in this wavefront.
+    mq = reduce32(lse2_row, [](float a, float bb) { return fmaxf(a, bb); });
+    z = reduce32(lse2_row == -INFINITY ? 0.f : fast_exp2(lse2_row - mq), [](float a, float bb) { return a + bb; });
+  } else {
+    if (h == 0) stat[wave * 32 + c] = lse2_row;
+    lds_barrier();
+    mq = -INFINITY;
 #pragma unroll
-  for (int gg = 0; gg < G; ++gg) mq = fmaxf(mq, stat[(qs * G + gg) * 32 + c]);
-  mq = max32(mq);
-  float z = 0.f;
+    for (int gg = 0; gg < G; ++gg) mq = fmaxf(mq, stat[(qs * G + gg) * 32 + c]);
+    mq = reduce32(mq, [](float a, float bb) { return fmaxf(a, bb); });
+    z = 0.f;
 #pragma unroll
-  for (int gg = 0; gg < G; ++gg) {
-    const float x = stat[(qs * G + gg) * 32 + c];
-    z += x == -INFINITY ? 0.f : fast_exp2(x - mq);
+    for (int gg = 0; gg < G; ++gg) {
+      const float x = stat[(qs * G + gg) * 32 + c];
+      z += x == -INFINITY ? 0.f : fast_exp2(x - mq);
+    }
+    z = reduce32(z, [](float a, float bb) { return a + bb; });
   }
-  z = sum32(z);
   const float lse2 = mq + fast_log2(z);
   const float wgt = rowvalid ? fast_exp2(m - lse2) : 0.f;
 
@@ -276,7 +372,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
   // j = 16 dt + 4 qd + e  <->  d = 32 dt + 8 qd + 4 h + e
   const int d0 = 32 * (j0 >> 4) + 8 * ((j0 >> 2) & 3) + 4 * h + (j0 & 3);
   if constexpr (G > 1) {
-    float* part = reinterpret_cast<float*>(smem) + wave * 64 * NO;
+    float* part = xchg + wave * 64 * NO;
 #pragma unroll
     for (int t = 0; t < NO; ++t) part[lane * NO + t] = xv[t];
     lds_barrier();
@@ -303,11 +399,10 @@ template <int D, int G>
 hipError_t launch(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
                   const void* vp, void* out, float* lse, hipStream_t st) {
   constexpr int QW = kWaves / G;
-  constexpr int NS = 2;
   const long tiles = (s.N + QW - 1) / QW;
   const long total = tiles * s.B * s.H;
   const long grid = ((total + 7) / 8) * 8;
-  hipLaunchKernelGGL((fwd_mfma_kernel<D, G, NS>), dim3(static_cast<unsigned>(grid)), dim3(kThreads), 0,
+  hipLaunchKernelGGL((fwd_mfma_kernel<D, G>), dim3(static_cast<unsigned>(grid)), dim3(kThreads), 0,
                      st, s, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                      static_cast<const uint16_t*>(kp), static_cast<const uint16_t*>(v),
                      static_cast<const uint16_t*>(vp), static_cast<uint16_t*>(out), lse);

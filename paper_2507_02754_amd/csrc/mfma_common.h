@@ -129,6 +129,14 @@ template <typename V>
 __device__ __forceinline__ void lds_st(lds_char* p, V v) {
   *reinterpret_cast<__attribute__((address_space(3))) V*>(p) = v;
 }
+// Buffer load of 16 bytes per lane straight into LDS: lane l's bytes go to
+// dst + 16 l (dst wave-uniform). Out-of-range offsets load zeros, as for
+// register loads. (The builtin exists only in the device pass.)
+__device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t r, lds_char* dst, int voff) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)(dst), 16, voff, 0, 0, 0);
+#endif
+}
 __device__ __forceinline__ u32x2_t lds_tr16(const lds_char* p) {
   const s16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t*)(p));
   return __builtin_bit_cast(u32x2_t, v);
@@ -199,6 +207,20 @@ __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(
 template <int CTRL>
 __device__ __forceinline__ float dpp_f(float x) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+
+// Reduction over the 32 lanes of each half-wavefront (lanes with the same
+// lane >> 5) without LDS: DPP lane ^ 1 and lane ^ 2 (quad permutations), the
+// mirror within 8 and within 16 lanes, then v_permlane16_swap for lane ^ 16.
+// Every lane of the half ends with the result.
+template <typename Op>
+__device__ __forceinline__ float reduce32(float x, Op op) {
+  x = op(x, dpp_f<0xB1>(x));   // quad_perm [1,0,3,2]
+  x = op(x, dpp_f<0x4E>(x));   // quad_perm [2,3,0,1]
+  x = op(x, dpp_f<0x141>(x));  // row_half_mirror
+  x = op(x, dpp_f<0x140>(x));  // row_mirror
+  auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return op(__uint_as_float(p[0]), __uint_as_float(p[1]));
 }
 
 // Sums v[j] over the 32 lanes of each half-wavefront (lanes with the same
