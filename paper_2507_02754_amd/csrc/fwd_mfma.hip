@@ -35,10 +35,12 @@
 // compiler's wait for a stage's loads does not also wait for the others. Within a wavefront all rows share one
 // query, so a block is fully valid or masked by column only; masked columns
 // are set to -inf before the maximum.
-// The running maximum is rescaled lazily: only when some row's block maximum
-// exceeds it by more than 2^8 (p stays <= 256, exact in fp32 and bf16 range),
-// which after the first blocks is rare. The row sum l adds the bf16-rounded
-// p that the P V product consumes, so O is a convex combination of V rows.
+// The running maximum m is raised lazily: P(n) is formed with the current m
+// and only if some row's block sum of p leaves (0, 2^16] (p far from fp32
+// overflow) is m raised to the block maximum and P(n) formed again; after the
+// first block with a valid column this is rare, and the per-block maximum is
+// not computed otherwise. The row sum l adds the bf16-rounded p that the P V
+// product consumes, so O is a convex combination of V rows.
 // Rows with k < 0 or k <= i - w2 get q~ = 0 and weight 0 in the merge.
 #include "mfma_common.h"
 
@@ -48,7 +50,7 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kStages = 4;
-constexpr float kLazyRescale = 8.0f;  // log2 headroom before the running max is raised
+constexpr float kPmax = 65536.0f;  // largest block row sum of p before the running max is raised
 
 template <int X>
 using IC = std::integral_constant<int, X>;
@@ -105,7 +107,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
   const int b = bh / s.H, hh = bh - b * s.H;
 
   const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63, c = lane & 31, h = lane >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, c = lane & 31, h = lane >> 5;
   const int qs = wave / G, g = wave % G;
   const size_t rs = static_cast<size_t>(s.H) * D;
   const size_t base = (static_cast<size_t>(b) * s.N * s.H + hh) * D;
@@ -168,11 +170,22 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
   }
   auto load_tile = [&](__amdgpu_buffer_rsrc_t r, lds_char* dst, int blk) __attribute__((always_inline)) {
     const int jb = jlo + 32 * blk;
+    if (jb >= 0 && jb + 31 < N) {
+      // Block inside the sequence: the block's row offset goes in the
+      // scalar offset, the lane's offset within the block is fixed.
 #pragma unroll
-    for (int x = 0; x < SPW; ++x) {
-      const int kx = x * kWaves + wave;
-      const int row = min(max(jb + lrow[x], 0), N - 1);
-      if (T::instrs % kWaves == 0 || kx < T::instrs) load_lds16(r, dst + 1024 * kx, row * rsb + lcol[x]);
+      for (int x = 0; x < SPW; ++x) {
+        const int kx = x * kWaves + wave;
+        if (T::instrs % kWaves == 0 || kx < T::instrs)
+          load_lds16(r, dst + 1024 * kx, lrow[x] * rsb + lcol[x], jb * rsb);
+      }
+    } else {
+#pragma unroll
+      for (int x = 0; x < SPW; ++x) {
+        const int kx = x * kWaves + wave;
+        const int row = min(max(jb + lrow[x], 0), N - 1);
+        if (T::instrs % kWaves == 0 || kx < T::instrs) load_lds16(r, dst + 1024 * kx, row * rsb + lcol[x]);
+      }
     }
   };
   // Blocks 0-3 of K and 0-2 of V go out before the q~ loads, so their
@@ -249,11 +262,17 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
     // blk - 3) must be in LDS for every wavefront: wait until at most the
     // 3 SPW loads issued after K(blk + 2) are in flight, then synchronise.
     wait_vmcnt<3 * SPW>();
-    lds_barrier();
+    lds_barrier_tracked();
     // K(blk + 4) replaces K(blk), read in iteration blk - 2; V(blk + 3)
     // replaces V(blk - 1), read in iteration blk - 1.
     if (blk + 4 < nb) load_tile(rk, kst(IC<S>{}), blk + 4);
     if (blk + 3 < nb) load_tile(rv, vst(IC<(S + 3) % kStages>{}), blk + 3);
+    // V(blk) fragments, in flight while S(blk + 1) and P(blk) are formed.
+    u32x4_t vf[2][NDT];
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) vf[u][dt] = vfrag(SC, dt, u);
 
     // Valid block-local columns of this wavefront's query.
     const int lo = max(qs, -jlo) - 32 * blk;
@@ -265,37 +284,45 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
         if (jl < lo || jl > hi) sc[cur][vv] = -INFINITY;
       }
     }
-    float mx = fmaxf(sc[cur][0], sc[cur][1]);
+    // P(blk) on the vector units while the matrix cores form S(blk + 1).
+    logits(sc[nxt]);
+    u32x4_t pf[2];
+    float lb = 0.f;
+    auto form_p = [&]() __attribute__((always_inline)) {
+      lb = 0.f;
 #pragma unroll
-    for (int vv = 2; vv < 16; vv += 2) mx = fmaxf(fmaxf(mx, sc[cur][vv]), sc[cur][vv + 1]);
-    mx = fmaxf(mx, swap_halves(mx));
-    if (__builtin_amdgcn_ballot_w64(mx > m + kLazyRescale) != 0) {
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const unsigned pp =
+              pack_bf16x2(fast_exp2(sc[cur][8 * u + 2 * e] - m), fast_exp2(sc[cur][8 * u + 2 * e + 1] - m));
+          pf[u][e] = pp;
+          lb = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pp), ones, lb, false);
+        }
+    };
+    form_p();
+    // The running maximum is raised only when some row's block sum leaves
+    // (0, kPmax] (always on the first block with a valid column, where
+    // m = -1e30 makes p = inf): then m becomes the block maximum, the state
+    // is rescaled and P(blk) is formed again.
+    if (__builtin_amdgcn_ballot_w64(!(lb <= kPmax)) != 0) {
+      float mx = fmaxf(sc[cur][0], sc[cur][1]);
+#pragma unroll
+      for (int vv = 2; vv < 16; vv += 2) mx = fmaxf(fmaxf(mx, sc[cur][vv]), sc[cur][vv + 1]);
+      mx = fmaxf(mx, swap_halves(mx));
       const float mnew = fmaxf(m, mx);
       const float alpha = fast_exp2(m - mnew);
       l *= alpha;
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt) acc[dt] *= alpha;
       m = mnew;
+      form_p();
     }
-    // P(blk) on the vector units while the matrix cores form S(blk + 1).
-    logits(sc[nxt]);
-    u32x4_t pf[2];
+    l += lb;
 #pragma unroll
     for (int u = 0; u < 2; ++u)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const unsigned pp = pack_bf16x2(fast_exp2(sc[cur][8 * u + 2 * e] - m), fast_exp2(sc[cur][8 * u + 2 * e + 1] - m));
-        pf[u][e] = pp;
-        l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pp), ones, l, false);
-      }
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      u32x4_t vf[NDT];
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) vf[dt] = vfrag(SC, dt, u);
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) acc[dt] = mfma32(vf[dt], pf[u], acc[dt]);
-    }
+      for (int dt = 0; dt < NDT; ++dt) acc[dt] = mfma32(vf[u][dt], pf[u], acc[dt]);
     // K fragments of block blk + 2 (stage written in iteration blk - 1).
 #pragma unroll
     for (int t = 0; t < NT; ++t) kf[t] = kfrag(IC<(S + 2) % kStages>{}, t);

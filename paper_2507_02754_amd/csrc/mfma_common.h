@@ -132,9 +132,9 @@ __device__ __forceinline__ void lds_st(lds_char* p, V v) {
 // Buffer load of 16 bytes per lane straight into LDS: lane l's bytes go to
 // dst + 16 l (dst wave-uniform). Out-of-range offsets load zeros, as for
 // register loads. (The builtin exists only in the device pass.)
-__device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t r, lds_char* dst, int voff) {
+__device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t r, lds_char* dst, int voff, int soff = 0) {
 #if defined(__HIP_DEVICE_COMPILE__)
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)(dst), 16, voff, 0, 0, 0);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)(dst), 16, voff, soff, 0, 0);
 #endif
 }
 __device__ __forceinline__ u32x2_t lds_tr16(const lds_char* p) {
@@ -203,6 +203,16 @@ struct FragTile {
 // accesses on their side of it, and without the vmcnt(0) wait that
 // __syncthreads adds, so global loads in flight stay in flight.
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// The same through builtins, so that the compiler's wait-count tracking knows
+// every LDS read issued before it has completed (it does not look inside the
+// inline assembly above and would otherwise wait again for them later).
+__device__ __forceinline__ void lds_barrier_tracked() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt and expcnt at their maxima
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 
 template <int CTRL>
 __device__ __forceinline__ float dpp_f(float x) {
