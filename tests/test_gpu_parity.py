@@ -68,6 +68,34 @@ def test_small_shapes_full(shape):
     P.check_grads([P.to64(g) for g in grads], g_ref, dt, str(shape))
 
 
+@pytest.mark.parametrize("d", [128, 64])
+def test_running_max_raised_mid_window(d):
+    """Keys alternate, 32 at a time, between blocks whose logits sit near -24
+    and blocks with logits ~N(0, 1): a window whose first block is a low one
+    sets the running maximum there and must raise it (by ~35 in log2 units,
+    rescaling the partial sums) when the next block arrives. The low blocks'
+    weights are ~e^-24 next to a normal block, so the bf16 rounding of their
+    large logits barely reaches the result."""
+    b, h, n, w1, w2 = 1, 2, 257, 96, 32
+    _announce(f"running max raised mid-window N={n} D={d} w1={w1} w2={w2}")
+    g = torch.Generator(device="cpu").manual_seed(7 + d)
+    shape = (b, n, h, d)
+    q = 1 + 0.1 * torch.randn(shape, generator=g)
+    kp = 1 + 0.1 * torch.randn(shape, generator=g)
+    k = torch.randn(shape, generator=g)
+    low = ((torch.arange(n) // 32) % 2 == 0).view(1, n, 1, 1)
+    k = torch.where(low, torch.full_like(k, -2.1 * (128 / d) ** 0.5), k)
+    v, vp, do = (torch.randn(shape, generator=g) for _ in range(3))
+    inputs = tuple(x.to(torch.bfloat16).contiguous() for x in (q, k, kp, v, vp, do))
+    scale = d ** -0.5
+    o, lse = P.gpu_forward(inputs, w1, w2, scale)
+    grads = P.gpu_backward(inputs, o, lse, w1, w2, scale)
+    o_ref, lse_ref, g_ref = P.full_oracle(inputs, w1, w2, scale)
+    assert lse_ref.min() < -15  # some queries see only low blocks
+    P.check_forward(P.to64(o), P.to64(lse), o_ref, lse_ref, "bf16", f"mid-window max D={d}")
+    P.check_grads([P.to64(g_) for g_ in grads], g_ref, "bf16", f"mid-window max D={d}")
+
+
 def _is_fast(w, which):
     return simplicial_attn_path_name(which, w.B, w.N, w.H, w.D, w.w1, w.w2, 1) != "generic"
 
