@@ -90,6 +90,9 @@ __global__ __launch_bounds__(kQThreads, 1) void bwd_query_kernel(
 
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // Roles alternate by wavefront. Wavefronts w and w + 4 of a 512-thread
+  // workgroup share a SIMD, so each SIMD holds two wavefronts of one role;
+  // pairing the two roles of a query on a SIMD instead measured slower here.
   const bool roleA = (wave & 1) == 0;
   const int qs = wave >> 1;  // query slot of this wavefront in a tile
   const int lane = tid & 63, c = lane & 31, h = lane >> 5;
