@@ -276,6 +276,10 @@ __global__ __launch_bounds__(kKeyThreads, 1) void bwd_key_kernel(
     // Iteration rb, tile slot S = rb % 4. The q~ half of tile rb + 2 is formed
     // from loads issued two iterations earlier (register set rb & 1).
     auto step = [&](int rb, auto slot, auto guard) __attribute__((always_inline)) {
+      // Wavefront priority 1 while computing, 0 at the barrier (measured
+      // faster: a wavefront that is computing issues ahead of one that is
+      // about to wait).
+      __builtin_amdgcn_s_setprio(1);
       constexpr int S = decltype(slot)::value;
       constexpr int S1 = (S + 1) % kSlots, S2 = (S + 2) % kSlots;
       constexpr bool kGuard = decltype(guard)::value != 0;
@@ -335,6 +339,7 @@ __global__ __launch_bounds__(kKeyThreads, 1) void bwd_key_kernel(
       fetch(rb + 4, ic<S & 1>{});
       pcur[0] = pnext[0];
       pcur[1] = pnext[1];
+      __builtin_amdgcn_s_setprio(0);
       lds_barrier();
     };
     run_loops(step);
@@ -364,6 +369,7 @@ __global__ __launch_bounds__(kKeyThreads, 1) void bwd_key_kernel(
       return df;
     };
     auto step = [&](int rb, auto slot, auto guard) __attribute__((always_inline)) {
+      __builtin_amdgcn_s_setprio(1);
       constexpr int S = decltype(slot)::value;
       constexpr int S1 = (S + 1) % kSlots, S2 = (S + 2) % kSlots;
       constexpr bool kGuard = decltype(guard)::value != 0;
@@ -431,6 +437,7 @@ __global__ __launch_bounds__(kKeyThreads, 1) void bwd_key_kernel(
       }
       fetch(rb + 3, ic<0>{});
       dpcur = dpnext;
+      __builtin_amdgcn_s_setprio(0);
       lds_barrier();
     };
     run_loops(step);

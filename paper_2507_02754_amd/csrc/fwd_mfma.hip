@@ -285,6 +285,10 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
       }
     }
     // P(blk) on the vector units while the matrix cores form S(blk + 1).
+    // From here to the end of the block this wavefront issues ahead of the
+    // other one on its SIMD while that one is at the barrier or issuing its
+    // loads (wavefront priority 1; back to 0 at the end of the block).
+    __builtin_amdgcn_s_setprio(1);
     logits(sc[nxt]);
     u32x4_t pf[2];
     float lb = 0.f;
@@ -326,6 +330,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
     // K fragments of block blk + 2 (stage written in iteration blk - 1).
 #pragma unroll
     for (int t = 0; t < NT; ++t) kf[t] = kfrag(IC<(S + 2) % kStages>{}, t);
+    __builtin_amdgcn_s_setprio(0);
   };
   for (int b0 = 0; b0 < nb; b0 += kStages) {
     iteration(IC<0>{}, b0);
