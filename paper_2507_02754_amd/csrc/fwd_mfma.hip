@@ -30,6 +30,13 @@
 //     P(n), while the matrix cores compute S(n+1) from K fragments that were
 //     read one iteration earlier,
 //   - accumulates P(n) V(n) while the K fragments of block n+2 are read.
+// With w2 <= 32 the prologue brings the workgroup's k' and q rows into a
+// staging tile with the same LDS-DMA loads and forms q~ from LDS (one 16-byte
+// load per row instead of per-wavefront register loads of overlapping rows),
+// waits only for K(0) and K(1) before the first products and issues V(1),
+// K(3), V(2) behind them; the staging tile then receives the v' rows. Tiles
+// whose key window lies inside the sequence skip the per-block bounds test:
+// the loop is bound by instruction issue, scalar instructions included.
 // The iteration is unrolled over the 4 ring stages so every LDS address is a
 // per-lane base plus an immediate; each stage is a separate LDS array so the
 // compiler's wait for a stage's loads does not also wait for the others. Within a wavefront all rows share one
@@ -79,10 +86,14 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
   using T = SwzTile<D>;
   __shared__ __attribute__((aligned(16))) char kst0[T::bytes], kst1[T::bytes], kst2[T::bytes], kst3[T::bytes];
   __shared__ __attribute__((aligned(16))) char vst0[T::bytes], vst1[T::bytes], vst2[T::bytes], vst3[T::bytes];
-  // v'_k rows kk0 .. kk0 + 34 of the workgroup's queries (w2 <= 32), rows of
-  // 2D bytes with the 16-byte chunk ch of row r at slot ch ^ (r % CH).
-  constexpr int VPR = ((35 * T::CH + 63) / 64 * 64) / T::CH;
-  __shared__ __attribute__((aligned(16))) char vpt[G == 1 ? VPR * 2 * D : 16];
+  // Staging tile (w2 <= 32): rows 0 .. KR-1 hold k'_k for k = i0-31 ... (35
+  // needed) and rows KR .. KR+3 the workgroup's q rows until q~ is formed;
+  // from the first iteration on rows 0 .. 34 hold v'_k of the same k for the
+  // epilogue. Rows of 2D bytes, 16-byte chunk ch of row r at slot ch ^ (r % CH).
+  constexpr int KI = (35 * T::CH + 63) / 64;  // 64-lane loads of 35 rows
+  constexpr int KR = KI * 64 / T::CH;         // rows they cover
+  constexpr int SR = KR + 64 / T::CH;         // + one 64-lane load of q rows
+  __shared__ __attribute__((aligned(16))) char stg[G == 1 ? SR * 2 * D : 16];
   __shared__ float stat[G == 1 ? 1 : kWaves * 32];
   __shared__ float xchg[G == 1 ? 1 : kWaves * 64 * (D / 64)];
   auto kst = [&](auto SC) __attribute__((always_inline)) {
@@ -168,9 +179,12 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
     lrow[x] = p / T::CH;
     lcol[x] = 16 * ((p % T::CH) ^ T::swz(lrow[x]));
   }
+  // Tiles whose whole key window lies inside the sequence (all but the first
+  // and last few of each head) skip the per-block bounds test.
+  const bool interior = jlo >= 0 && jlo + 32 * nb <= N;
   auto load_tile = [&](__amdgpu_buffer_rsrc_t r, lds_char* dst, int blk) __attribute__((always_inline)) {
     const int jb = jlo + 32 * blk;
-    if (jb >= 0 && jb + 31 < N) {
+    if (interior || (jb >= 0 && jb + 31 < N)) {
       // Block inside the sequence: the block's row offset goes in the
       // scalar offset, the lane's offset within the block is fixed.
 #pragma unroll
@@ -188,34 +202,48 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
       }
     }
   };
-  // Blocks 0-3 of K and 0-2 of V go out before the q~ loads, so their
-  // latencies overlap (blocks past the window only cost the loads).
-  load_tile(rk, kst(IC<0>{}), 0);
-  load_tile(rk, kst(IC<1>{}), 1);
-  load_tile(rk, kst(IC<2>{}), 2);
-  load_tile(rk, kst(IC<3>{}), 3);
-  load_tile(rv, vst(IC<0>{}), 0);
-  load_tile(rv, vst(IC<1>{}), 1);
-  load_tile(rv, vst(IC<2>{}), 2);
+  const __amdgpu_buffer_rsrc_t rq = make_rsrc(q + base, head_bytes(N, rsb, D));
+  const __amdgpu_buffer_rsrc_t rkp = make_rsrc(kp + base, head_bytes(N, rsb, D));
   const __amdgpu_buffer_rsrc_t rvp = make_rsrc(vp + base, head_bytes(N, rsb, D));
-  if constexpr (G == 1) {
-    constexpr int VI = VPR * T::CH / 64;  // 64-lane loads of the v' tile
-    const int kk0 = i0 - 31;
-#pragma unroll
-    for (int x = wave; x < VI; x += kWaves) {
-      const int p = 64 * x + lane, r = p / T::CH;
-      const int ch = (p % T::CH) ^ (r % T::CH);
-      const int row = min(max(kk0 + r, 0), N - 1);
-      load_lds16(rvp, to_lds(vpt) + 1024 * x, row * rsb + 16 * ch);
-    }
-  }
-
-  // ---- modulated queries q~ = (scale*log2 e) * q_i o k'_k as B operands ----
-  // (rows outside the window or the sequence load as zeros: offset -1)
+  const int kk0 = i0 - 31;  // first k of the staged k' / v' rows (w2 <= 32)
+  // 64-lane loads x of staging rows: row r of the 64 x 16 bytes is p / CH
+  // for p = 64 x + lane, its chunk goes to slot (p % CH) ^ (r % CH).
+  auto stage = [&](__amdgpu_buffer_rsrc_t r, int x, int row0) __attribute__((always_inline)) {
+    const int p = 64 * x + lane, rr = p / T::CH;
+    const int ch = (p % T::CH) ^ (rr % T::CH);
+    const int row = min(max(row0 + rr, 0), N - 1);
+    load_lds16(r, to_lds(stg) + 1024 * x, row * rsb + 16 * ch);
+  };
   u32x4_t qt[NT];
-  {
-    const __amdgpu_buffer_rsrc_t rq = make_rsrc(q + base, head_bytes(N, rsb, D));
-    const __amdgpu_buffer_rsrc_t rkp = make_rsrc(kp + base, head_bytes(N, rsb, D));
+  if constexpr (G == 1) {
+    // The workgroup's k' rows and q rows go to the staging tile, then the
+    // blocks the first products and iteration 0 need: K(0), K(1), V(0), K(2).
+    // V(1), K(3), V(2) follow once S(0) is under way, so that the wait of
+    // every iteration below (K(blk + 2) and V(blk) loaded) holds from the
+    // first one on. Blocks past the window only cost the loads.
+#pragma unroll
+    for (int x = wave; x < KI + 1; x += kWaves) {
+      if (x < KI)
+        stage(rkp, x, kk0);
+      else
+        stage(rq, x, i0 - KR);
+    }
+    load_tile(rk, kst(IC<0>{}), 0);
+    load_tile(rk, kst(IC<1>{}), 1);
+    load_tile(rv, vst(IC<0>{}), 0);
+    load_tile(rk, kst(IC<2>{}), 2);
+  } else {
+    // Blocks 0-3 of K and 0-2 of V go out before the q~ loads, so their
+    // latencies overlap (blocks past the window only cost the loads).
+    load_tile(rk, kst(IC<0>{}), 0);
+    load_tile(rk, kst(IC<1>{}), 1);
+    load_tile(rk, kst(IC<2>{}), 2);
+    load_tile(rk, kst(IC<3>{}), 3);
+    load_tile(rv, vst(IC<0>{}), 0);
+    load_tile(rv, vst(IC<1>{}), 1);
+    load_tile(rv, vst(IC<2>{}), 2);
+    // modulated queries q~ = (scale*log2 e) * q_i o k'_k as B operands
+    // (rows outside the window or the sequence load as zeros: offset -1)
     u32x4_t qa[NT], ka[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
@@ -246,11 +274,44 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
     for (int t = 1; t < NT; ++t) dst = mfma32(kf[t], qt[t], dst);
   };
 
-  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wavefront's block loads are in LDS
-  lds_barrier();
+  if constexpr (G == 1) {
+    // Staging rows, K(0) and K(1) in LDS for every wavefront; V(0) and K(2)
+    // may still be in flight.
+    wait_vmcnt<2 * SPW>();
+    lds_barrier_tracked();
+    // modulated queries q~ = (scale*log2 e) * q_i o k'_k as B operands, from
+    // the staged rows (local k' row qs + c, q row KR + qs); rows outside the
+    // window or the sequence are zero.
+    const int rr = qs + c, rq_ = KR + qs;
+    const lds_char* krow = to_lds(stg) + rr * 2 * D;
+    const lds_char* qrow = to_lds(stg) + rq_ * 2 * D;
+    const unsigned keep = rowvalid ? 0xFFFFFFFFu : 0u;
+    u32x4_t qa[NT], ka[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const int ch = 2 * t + h;
+      ka[t] = lds_ld<u32x4_t>(krow + 16 * (ch ^ (rr % T::CH)));
+      qa[t] = lds_ld<u32x4_t>(qrow + 16 * (ch ^ (rq_ % T::CH)));
+    }
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        qt[t][e] = keep & pack_bf16x2(bf16_lo(qa[t][e]) * bf16_lo(ka[t][e]) * qscale,
+                                      bf16_hi(qa[t][e]) * bf16_hi(ka[t][e]) * qscale);
+  } else {
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wavefront's block loads are in LDS
+    lds_barrier();
+  }
 #pragma unroll
   for (int t = 0; t < NT; ++t) kf[t] = kfrag(IC<0>{}, t);
+  __builtin_amdgcn_sched_barrier(0);  // all fragment reads ahead of the products
   logits(sc[0]);
+  if constexpr (G == 1) {
+    load_tile(rv, vst(IC<1>{}), 1);
+    load_tile(rk, kst(IC<3>{}), 3);
+    load_tile(rv, vst(IC<2>{}), 2);
+  }
 #pragma unroll
   for (int t = 0; t < NT; ++t) kf[t] = kfrag(IC<1>{}, t);
 
@@ -267,6 +328,14 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
     // replaces V(blk - 1), read in iteration blk - 1.
     if (blk + 4 < nb) load_tile(rk, kst(IC<S>{}), blk + 4);
     if (blk + 3 < nb) load_tile(rv, vst(IC<(S + 3) % kStages>{}), blk + 3);
+    if constexpr (G == 1 && S == 0) {
+      // v' rows into the staging tile, whose q and k' rows every wavefront
+      // has read before the barrier above.
+      if (blk == 0) {
+#pragma unroll
+        for (int x = wave; x < KI; x += kWaves) stage(rvp, x, kk0);
+      }
+    }
     // V(blk) fragments, in flight while S(blk + 1) and P(blk) are formed.
     u32x4_t vf[2][NDT];
 #pragma unroll
@@ -344,8 +413,15 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
   // merge below covers their latency.
   u32x2_t vpr[4 * NDT];
   if constexpr (G == 1) {
+    // The v' rows (issued in iteration 0) are in LDS for every wavefront
+    // once 3 SPW later loads have been waited for and a barrier passed,
+    // which iterations 1-3 do when the window has at least 7 blocks.
+    if (nb < 7) {
+      wait_vmcnt<0>();
+      lds_barrier_tracked();
+    }
     const int r = qs + c;
-    const lds_char* vrow = to_lds(vpt) + r * 2 * D + 8 * h;
+    const lds_char* vrow = to_lds(stg) + r * 2 * D + 8 * h;
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll

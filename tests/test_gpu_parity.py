@@ -96,6 +96,26 @@ def test_running_max_raised_mid_window(d):
     P.check_grads([P.to64(g_) for g_ in grads], g_ref, "bf16", f"mid-window max D={d}")
 
 
+@pytest.mark.parametrize("d,w1,w2", [(64, 200, 32), (128, 230, 32), (64, 300, 32), (128, 230, 17)])
+def test_forward_tile_runs(d, w1, w2):
+    """Many tiles per workgroup of the streaming forward (two workgroups per
+    CU, each walking a run of 4-query tiles with its K/V rings running on from
+    one tile into the next): 3 heads of 4096 queries, so one XCD's run of tiles
+    crosses a head boundary; w1 = 200, 230, 300 give 7, 8 and 10 key blocks
+    per tile (tile start stages cycling by 3, 0 and 2 mod 4). Sampled rows of
+    every head, the first rows of each head included."""
+    b, h, n = 1, 3, 4096
+    _announce(f"forward tile runs N={n} H={h} D={d} w1={w1} w2={w2} "
+              f"fwd={simplicial_attn_path_name(0, b, n, h, d, w1, w2, 1)}")
+    inputs = draw((b, n, h, d), seed=11 + d + w1 + w2, dtype=torch.bfloat16)
+    scale = d ** -0.5
+    o, lse = P.gpu_forward(inputs, w1, w2, scale)
+    rows = P.sample_rows(n, w1, w2, extra=40, seed=w1)
+    heads = [(0, x) for x in range(h)]
+    P.sampled_forward_check(inputs[:5], o, lse, w1, w2, scale, "bf16", heads, rows,
+                            f"tile runs D={d} w1={w1} w2={w2}")
+
+
 def _is_fast(w, which):
     return simplicial_attn_path_name(which, w.B, w.N, w.H, w.D, w.w1, w.w2, 1) != "generic"
 
