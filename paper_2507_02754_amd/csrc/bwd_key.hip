@@ -261,9 +261,13 @@ __global__ __launch_bounds__(kKeyThreads, 1) void bwd_key_kernel(
       const int i = j0 + rb / G;
       const bool colok = jme <= i && jme > i - w1 && jme < N;
       const float nl = nlse2 - (colok ? 0.f : __builtin_inff());
+      // p = 2^min(x, 0): at most 1, so rows formed as zeros (whose statistic
+      // may belong to another query) stay finite. Written as a [0, 1] clamp of
+      // 2^x, which the compiler folds into the exponential's clamp bit.
       float pr[16];
 #pragma unroll
-      for (int vv = 0; vv < 16; ++vv) pr[vv] = fast_exp2(fminf(__builtin_fmaf(sacc[vv], qscale, nl), 0.f));
+      for (int vv = 0; vv < 16; ++vv)
+        pr[vv] = __builtin_amdgcn_fmed3f(fast_exp2(__builtin_fmaf(sacc[vv], qscale, nl)), 0.f, 1.f);
 #pragma unroll
       for (int uu = 0; uu < 2; ++uu) {
         pf[uu] = pack_frag(pr, uu);
