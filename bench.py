@@ -95,8 +95,8 @@ def cpu_baseline(w, inputs, target_s):
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="long_bf16_n32k")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -172,8 +172,16 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     total_ms = start.elapsed_time(end)
-    ms = {p: sum(e[j].elapsed_time(e[j + 1]) for e in evs) / args.steps for j, p in enumerate(phases)}
+    per = {p: sorted(e[j].elapsed_time(e[j + 1]) for e in evs) for j, p in enumerate(phases)}
+    ms = {p: sum(v) / args.steps for p, v in per.items()}
     ms_step = total_ms / args.steps
+
+    def med(v):
+        n = len(v)
+        return v[n // 2] if n % 2 else 0.5 * (v[n // 2 - 1] + v[n // 2])
+
+    fwd_each = per["fwd"]
+    bwd_each = sorted(sum(e[j].elapsed_time(e[j + 1]) for j in (1, 2, 3)) for e in evs)
 
     unit = float(w.B) * w.H * w.N * w.w1 * w.w2 * w.D
     fwd_flops, bwd_flops = 4 * unit, 12 * unit
@@ -218,6 +226,8 @@ def main():
         "fwd_pct_peak": round(100 * fwd_tf / PEAK_BF16_TFLOPS, 2),
         "bwd_pct_peak": round(100 * bwd_tf / PEAK_BF16_TFLOPS, 2),
         "phase_ms": {p: round(ms[p], 4) for p in phases},
+        "fwd_ms_median_min": [round(med(fwd_each), 4), round(fwd_each[0], 4)],
+        "bwd_ms_median_min": [round(med(bwd_each), 4), round(bwd_each[0], 4)],
         "wall_s_timed": round(wall, 3),
         "roofline": roofline,
         "cpu_baseline": None,
