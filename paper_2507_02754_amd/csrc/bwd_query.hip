@@ -237,10 +237,13 @@ __global__ __launch_bounds__(kQThreads, 1) void bwd_query_kernel(
   // ring `ring` in QW phases: in phase p the wavefront of query slot qs adds
   // column slice (qs + p) % QW, so every slice of a ring row receives the
   // contributions in a fixed order.
-  auto ring_add = [&](float* ring, f32x16_t* x, bool rowvalid, int kk) __attribute__((always_inline)) {
+  // hook(IC<p>) runs in phase p before its barrier (register-only work that
+  // fills the wait).
+  auto ring_add = [&](float* ring, f32x16_t* x, bool rowvalid, int kk, auto hook) __attribute__((always_inline)) {
     const int aslot = (kk - kbase) % RB;
     float* rp = ring + aslot * L::rStride + 4 * h;
-    for (int p = 0; p < QW; ++p) {
+    auto phase = [&](auto PC) __attribute__((always_inline)) {
+      constexpr int p = decltype(PC)::value;
       const int sl = (qs + p) % QW;
 #pragma unroll
       for (int slc = 0; slc < QW; ++slc) {
@@ -268,8 +271,14 @@ __global__ __launch_bounds__(kQThreads, 1) void bwd_query_kernel(
             *reinterpret_cast<float4*>(rp + d0) = y;
           }
       }
+      hook(PC);
       lds_barrier();
-    }
+    };
+    static_assert(QW == 4, "four ring phases");
+    phase(std::integral_constant<int, 0>{});
+    phase(std::integral_constant<int, 1>{});
+    phase(std::integral_constant<int, 2>{});
+    phase(std::integral_constant<int, 3>{});
   };
 
   // Per-query statistic of this wavefront's query (A: LSE, B: Delta), loaded
@@ -389,7 +398,7 @@ __global__ __launch_bounds__(kQThreads, 1) void bwd_query_kernel(
           }
       }
       lds_barrier();  // matches B's barrier after its dq reduction
-      ring_add(ring_vp, au, rowvalid, kk);
+      ring_add(ring_vp, au, rowvalid, kk, [](auto) {});
       flush_tile(i0);
       lds_barrier();
     }
@@ -483,12 +492,13 @@ __global__ __launch_bounds__(kQThreads, 1) void bwd_query_kernel(
       }
       // ---- tile epilogue (B): dq_i, then scale q_i o dQ~_r into the dk' ring ----
       if (rowloader && tile + 1 < ntiles) row_put(i0 + QW, nrow);
+      // dq_i = scale * sum_k k'_k o dQ~_(i,k): every lane multiplies its
+      // accumulators (row c, d = 32 dt + 8 (v/4) + 4 h + v%4) by k'_k, then
+      // the sums over the 32 rows run across lanes in registers: the first
+      // level here, the other four in the ring phases below (their waits).
+      constexpr int NV = 16 * NDT;
+      float xv[NV];
       {
-        // dq_i = scale * sum_k k'_k o dQ~_(i,k): every lane multiplies its
-        // accumulators (row c, d = 32 dt + 8 (v/4) + 4 h + v%4) by k'_k, then
-        // the sums over the 32 rows run across lanes in registers.
-        constexpr int NV = 16 * NDT;
-        float xv[NV];
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
@@ -500,21 +510,7 @@ __global__ __launch_bounds__(kQThreads, 1) void bwd_query_kernel(
             xv[16 * dt + 4 * qd + 2] = bf16_lo(m[1]) * adq[dt][4 * qd + 2];
             xv[16 * dt + 4 * qd + 3] = bf16_hi(m[1]) * adq[dt][4 * qd + 3];
           }
-        reduce_lanes32<NV>(xv, lane);
-        constexpr int NO = NV / 32;  // sums per lane: columns j0 .. j0 + NO - 1
-        const int j0 = NV / 2 * ((c >> 4) & 1) + NV / 4 * ((c >> 3) & 1) + NV / 8 * ((c >> 2) & 1) +
-                       NV / 16 * ((c >> 1) & 1) + NV / 32 * (c & 1);
-        // j = 16 dt + 4 qd + e  <->  d = 32 dt + 8 qd + 4 h + e
-        const int d0 = 32 * (j0 >> 4) + 8 * ((j0 >> 2) & 3) + 4 * h + (j0 & 3);
-        if (qvalid) {
-          uint16_t* dst = dq + base + static_cast<size_t>(i) * rs + d0;
-          if constexpr (NO == 2) {
-            *reinterpret_cast<unsigned*>(dst) = pack_bf16x2(xv[0] * s.scale, xv[1] * s.scale);
-          } else {
-#pragma unroll
-            for (int t = 0; t < NO; ++t) dst[t] = f32_to_bf16(xv[t] * s.scale);
-          }
-        }
+        reduce_lanes32_level<NV, 0>(xv, lane);
         const char* qrow = qring + ((i - cs) % RQ) * 2 * D;  // q_i
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt)
@@ -529,7 +525,25 @@ __global__ __launch_bounds__(kQThreads, 1) void bwd_query_kernel(
           }
       }
       lds_barrier();  // every wavefront is past its reads of this tile's rows
-      ring_add(ring_kp, adq, rowvalid, kk);
+      ring_add(ring_kp, adq, rowvalid, kk, [&](auto PC) __attribute__((always_inline)) {
+        reduce_lanes32_level<NV, decltype(PC)::value + 1>(xv, lane);
+      });
+      {
+        constexpr int NO = NV / 32;  // sums per lane: columns j0 .. j0 + NO - 1
+        const int j0 = NV / 2 * ((c >> 4) & 1) + NV / 4 * ((c >> 3) & 1) + NV / 8 * ((c >> 2) & 1) +
+                       NV / 16 * ((c >> 1) & 1) + NV / 32 * (c & 1);
+        // j = 16 dt + 4 qd + e  <->  d = 32 dt + 8 qd + 4 h + e
+        const int d0 = 32 * (j0 >> 4) + 8 * ((j0 >> 2) & 3) + 4 * h + (j0 & 3);
+        if (qvalid) {
+          uint16_t* dst = dq + base + static_cast<size_t>(i) * rs + d0;
+          if constexpr (NO == 2) {
+            *reinterpret_cast<unsigned*>(dst) = pack_bf16x2(xv[0] * s.scale, xv[1] * s.scale);
+          } else {
+#pragma unroll
+            for (int t = 0; t < NO; ++t) dst[t] = f32_to_bf16(xv[t] * s.scale);
+          }
+        }
+      }
       flush_tile(i0);
       lds_barrier();
     }

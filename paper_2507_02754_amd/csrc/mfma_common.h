@@ -241,27 +241,38 @@ __device__ __forceinline__ float reduce32(float x, Op op) {
 // return v[0 .. NV/32 - 1] hold the sums of values j0 .. j0 + NV/32 - 1, with
 // j0 = sum over the bits b of c = lane & 31, from bit 4 down, of
 // bit * NV / 2^(step+1).
-template <int NV>
-__device__ __forceinline__ void reduce_lanes32(float* v, int lane) {
+// Level S (0..4) of the reduction below, so that callers can spread the
+// levels over other work; levels must run in order.
+template <int NV, int S>
+__device__ __forceinline__ void reduce_lanes32_level(float* v, int lane) {
   static_assert(NV >= 32 && NV % 32 == 0, "one value per lane at least");
   constexpr int N1 = NV / 2;
+  if constexpr (S == 0) {
 #pragma unroll
-  for (int j = 0; j < N1; ++j) {
-    auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v[j]), __float_as_uint(v[j + N1]), false, false);
-    v[j] = __uint_as_float(p[0]) + __uint_as_float(p[1]);
-  }
-  auto step = [&](auto ctrl, int n, int bit) __attribute__((always_inline)) {
-    constexpr int C = decltype(ctrl)::value;
+    for (int j = 0; j < N1; ++j) {
+      auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v[j]), __float_as_uint(v[j + N1]), false, false);
+      v[j] = __uint_as_float(p[0]) + __uint_as_float(p[1]);
+    }
+  } else {
+    // 0x140 row_mirror (lane ^ 15 within 16), 0x141 row_half_mirror (lane ^ 7
+    // within 8), 0x4E quad_perm [2,3,0,1], 0xB1 quad_perm [1,0,3,2]
+    constexpr int C = S == 1 ? 0x140 : S == 2 ? 0x141 : S == 3 ? 0x4E : 0xB1;
+    constexpr int bit = 16 >> S;
+    constexpr int n = N1 >> S;
 #pragma unroll
     for (int j = 0; j < n; ++j) {
       const float a = v[j] + dpp_f<C>(v[j]), b = v[j + n] + dpp_f<C>(v[j + n]);
       v[j] = (lane & bit) ? b : a;
     }
-  };
-  step(std::integral_constant<int, 0x140>{}, N1 / 2, 8);  // row_mirror: lane ^ 15 within 16
-  step(std::integral_constant<int, 0x141>{}, N1 / 4, 4);  // row_half_mirror: lane ^ 7 within 8
-  step(std::integral_constant<int, 0x4E>{}, N1 / 8, 2);   // quad_perm [2,3,0,1]
-  step(std::integral_constant<int, 0xB1>{}, N1 / 16, 1);  // quad_perm [1,0,3,2]
+  }
+}
+template <int NV>
+__device__ __forceinline__ void reduce_lanes32(float* v, int lane) {
+  reduce_lanes32_level<NV, 0>(v, lane);
+  reduce_lanes32_level<NV, 1>(v, lane);
+  reduce_lanes32_level<NV, 2>(v, lane);
+  reduce_lanes32_level<NV, 3>(v, lane);
+  reduce_lanes32_level<NV, 4>(v, lane);
 }
 
 // Accumulator register v of a 32x32 tile holds row 8*(v/4) + 4*h + (v%4).
