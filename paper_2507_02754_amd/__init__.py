@@ -2,9 +2,12 @@
 
 The compute lives in libsimplicial_attn.so (hand-written HIP, C ABI in
 include/simplicial_attn.h); this package is its thin Python binding plus the
-seeded synthetic workloads used by the tests and the benchmark.
+seeded synthetic workloads used by the tests and the benchmark, and a
+torch.autograd wrapper (`simplicial_attention`) over the forward and backward
+entry points.
 """
 
+from .autograd import SimplicialAttnFunction, simplicial_attention  # noqa: F401
 from .binding import (  # noqa: F401
     DTYPE_BF16,
     DTYPE_F32,

@@ -1,0 +1,50 @@
+"""torch.autograd wrapper of the library's forward and backward entry points.
+
+No arithmetic of its own: the forward is `simplicial_attn_fwd`, the backward
+is `simplicial_attn_bwd` (Section 7's split backward: Delta, the key-side and
+the query-side kernels), both called through the ctypes binding. Tensors are
+[B, N, H, D] on one GPU, bf16 or fp32; the window lengths and the scale are
+plain Python numbers (not differentiated).
+"""
+
+import torch
+
+from .binding import simplicial_attn_bwd, simplicial_attn_fwd
+
+__all__ = ["SimplicialAttnFunction", "simplicial_attention"]
+
+
+class SimplicialAttnFunction(torch.autograd.Function):
+    """(O, LSE) = 2-simplicial attention of (Q, K, K', V, V') with windows
+    (w1, w2) and logit scale `scale`; LSE is returned without a gradient."""
+
+    @staticmethod
+    def forward(ctx, q, k, kp, v, vp, w1, w2, scale):
+        q, k, kp, v, vp = (x.contiguous() for x in (q, k, kp, v, vp))
+        out, lse = simplicial_attn_fwd(q, k, kp, v, vp, w1, w2, scale)
+        ctx.save_for_backward(q, k, kp, v, vp, out, lse)
+        ctx.windows = (w1, w2, scale)
+        ctx.mark_non_differentiable(lse)
+        return out, lse
+
+    @staticmethod
+    @torch.autograd.function.once_differentiable
+    def backward(ctx, dout, _dlse):
+        q, k, kp, v, vp, out, lse = ctx.saved_tensors
+        w1, w2, scale = ctx.windows
+        if dout is None:
+            dout = torch.zeros_like(out)
+        grads = simplicial_attn_bwd(q, k, kp, v, vp, out, dout.to(out.dtype).contiguous(), lse,
+                                    w1, w2, scale)
+        return (*grads, None, None, None)
+
+
+def simplicial_attention(q, k, kp, v, vp, w1, w2, scale=None):
+    """O = 2-simplicial attention(Q, K, K', V, V') with autograd support.
+
+    `scale` defaults to 1/sqrt(D).
+    """
+    if scale is None:
+        scale = q.shape[-1] ** -0.5
+    out, _ = SimplicialAttnFunction.apply(q, k, kp, v, vp, int(w1), int(w2), float(scale))
+    return out

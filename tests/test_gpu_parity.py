@@ -141,6 +141,32 @@ def test_full_size_workloads_sampled(name):
                              key_rows, w.name)
 
 
+@pytest.mark.parametrize("shape", [(1, 2, 300, 128, 64, 32, "bf16"), (1, 1, 100, 64, 7, 5, "fp32")],
+                         ids=["bf16", "fp32"])
+def test_autograd_function(shape):
+    """Gradients through torch.autograd (loss = sum(O * dO)) equal the direct
+    backward call bit for bit and match the oracle; LSE carries no gradient."""
+    from paper_2507_02754_amd import simplicial_attention
+
+    b, h, n, d, w1, w2, dt = shape
+    _announce(f"autograd {shape}")
+    inputs = draw((b, n, h, d), seed=300 + n, dtype=torch.float32 if dt == "fp32" else torch.bfloat16)
+    scale = d ** -0.5
+    leaves = [x.to("cuda").requires_grad_(True) for x in inputs[:5]]
+    do = inputs[5].to("cuda")
+    o = simplicial_attention(*leaves, w1, w2, scale)
+    (o.float() * do.float()).sum().backward()
+    auto = [x.grad for x in leaves]
+    o_d, lse_d = P.gpu_forward(inputs, w1, w2, scale)
+    direct = P.gpu_backward(inputs, o_d, lse_d, w1, w2, scale)
+    assert torch.equal(o.detach(), o_d), "autograd forward differs from the direct call"
+    for name, g1, g2 in zip(("dq", "dk", "dkp", "dv", "dvp"), auto, direct):
+        assert torch.equal(g1, g2), f"{name}: autograd differs from the direct backward"
+    o_ref, lse_ref, g_ref = P.full_oracle(inputs, w1, w2, scale)
+    P.check_forward(P.to64(o.detach()), P.to64(lse_d), o_ref, lse_ref, dt, f"autograd {shape}")
+    P.check_grads([P.to64(g) for g in auto], g_ref, dt, f"autograd {shape}")
+
+
 def test_unit_windows_through_gpu():
     """w1 = w2 = 1: each query sees only the pair (i, i), so O = V o V',
     dV = dO o V' and dV' = dO o V (checked at the usual tolerance), while dQ, dK
