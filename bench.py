@@ -102,6 +102,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run one 1 GiB device-to-device copy first (HBM counter calibration)")
+    ap.add_argument("--gqa-kv-heads", type=int, default=0,
+                    help="also time the grouped-query forward and backward with this many "
+                         "K-side heads (reported under \"gqa\"; not part of the step)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this build runs the hot path on one GPU only; multi-GPU sharding "
@@ -114,6 +117,8 @@ def main():
     from paper_2507_02754_amd import (load_library, simplicial_attn_bwd_key_side,
                                       simplicial_attn_bwd_preprocess, simplicial_attn_bwd_query_side,
                                       simplicial_attn_bwd_workspace_size, simplicial_attn_fwd,
+                                      simplicial_attn_fwd_gqa, simplicial_attn_bwd_gqa,
+                                      simplicial_attn_bwd_gqa_workspace_size,
                                       simplicial_attn_path_name)
     from paper_2507_02754_amd.workloads import WORKLOADS, make_inputs
 
@@ -232,6 +237,41 @@ def main():
         "roofline": roofline,
         "cpu_baseline": None,
     }
+    if args.gqa_kv_heads:
+        # Grouped-query forward + backward at the same query shape, K, K', V, V'
+        # taken from the first Hkv heads of the inputs.
+        hkv = args.gqa_kv_heads
+        kv = [x[:, :, :hkv].contiguous() for x in (k, kp, v, vp)]
+        gkv = tuple(torch.empty_like(kv[0]) for _ in range(4))
+        gws = torch.empty(simplicial_attn_bwd_gqa_workspace_size(w.B, w.N, w.H, hkv, w.D, w.w1, w.w2,
+                                                                 w.torch_dtype),
+                          dtype=torch.uint8, device=dev)
+
+        def gqa_step(ev=None):
+            if ev:
+                ev[0].record()
+            simplicial_attn_fwd_gqa(q, *kv, w.w1, w.w2, w.scale, out=out, lse=lse)
+            if ev:
+                ev[1].record()
+            simplicial_attn_bwd_gqa(q, *kv, out, do, lse, w.w1, w.w2, w.scale, grads=(dq, *gkv),
+                                    workspace=gws)
+            if ev:
+                ev[2].record()
+
+        for _ in range(args.warmup):
+            gqa_step()
+        gev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+        torch.cuda.synchronize()
+        for i in range(args.steps):
+            gqa_step(gev[i])
+        torch.cuda.synchronize()
+        gf = sum(e[0].elapsed_time(e[1]) for e in gev) / args.steps
+        gb = sum(e[1].elapsed_time(e[2]) for e in gev) / args.steps
+        result["gqa"] = {"kv_heads": hkv, "fwd_ms": round(gf, 4), "bwd_ms": round(gb, 4),
+                         "fwd_tflops": round(fwd_flops / (gf * 1e-3) / 1e12, 2),
+                         "bwd_tflops": round(bwd_flops / (gb * 1e-3) / 1e12, 2),
+                         "step_tflops": round((fwd_flops + bwd_flops) / ((gf + gb) * 1e-3) / 1e12, 2)}
+        del kv, gkv, gws
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(w, inputs_cpu, args.cpu_seconds)

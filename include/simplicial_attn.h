@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define SIMPLICIAL_ATTN_ABI_VERSION 1
+#define SIMPLICIAL_ATTN_ABI_VERSION 2
 
 #define SA_DTYPE_F32 0
 #define SA_DTYPE_BF16 1
@@ -69,6 +69,23 @@ int simplicial_attn_fwd(const void* q, const void* k, const void* kp, const void
                         int32_t w2, float scale, int32_t dtype, void* stream);
 
 /*
+ * Forward pass with grouped-query attention (the layout of Section 6's
+ * production setting, where many query heads share one K/K'/V/V' head):
+ * query head h reads K-side head h / (H / Hkv). Same operation and conventions
+ * as simplicial_attn_fwd, except
+ *   q, out           [B, N, H, D]
+ *   k, kp, v, vp     [B, N, Hkv, D]
+ *   lse              [B, H, N]
+ *   Hkv              K-side heads, 1 <= Hkv <= H, H % Hkv == 0 (else SA_ERR_INVALID)
+ * Hkv == H is exactly simplicial_attn_fwd. The matching backward is
+ * simplicial_attn_bwd_gqa.
+ */
+int simplicial_attn_fwd_gqa(const void* q, const void* k, const void* kp, const void* v,
+                            const void* vp, void* out, float* lse, int64_t B, int64_t N, int64_t H,
+                            int64_t Hkv, int64_t D, int32_t w1, int32_t w2, float scale,
+                            int32_t dtype, void* stream);
+
+/*
  * Bytes of device workspace simplicial_attn_bwd needs for these sizes (the
  * per-query Delta = <dO_i, O_i> and the partial sums the backward reduces
  * deterministically). Returns 0 for arguments simplicial_attn_bwd would reject.
@@ -93,6 +110,36 @@ int simplicial_attn_bwd(const void* q, const void* k, const void* kp, const void
                         void* dkp, void* dv, void* dvp, void* workspace, size_t workspace_bytes,
                         int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1, int32_t w2,
                         float scale, int32_t dtype, void* stream);
+
+/*
+ * Backward with grouped-query attention, for the outputs of
+ * simplicial_attn_fwd_gqa. Every K-side element enters the logits of all the
+ * query heads of its group, so dK, dK', dV, dV' are the per-query-head
+ * gradients summed over the group (in fp32, query heads in ascending order,
+ * rounded once to dtype: bitwise deterministic).
+ *   q, out, dout, dq        [B, N, H, D], dtype
+ *   k, kp, v, vp            [B, N, Hkv, D], dtype
+ *   dk, dkp, dv, dvp        [B, N, Hkv, D], dtype, fully overwritten
+ *   lse                     [B, H, N] float32 from the forward
+ *   workspace               at least simplicial_attn_bwd_gqa_workspace_size()
+ *                           bytes, 16-byte aligned; contents on entry ignored.
+ *                           For Hkv < H it holds K, K', V, V' expanded to H
+ *                           heads and the per-query-head K-side gradients
+ *                           (8 tensors of B*N*H*D elements) besides what
+ *                           simplicial_attn_bwd needs.
+ *   Hkv                     as simplicial_attn_fwd_gqa (else SA_ERR_INVALID)
+ * Other arguments and errors as simplicial_attn_bwd; Hkv == H is exactly
+ * simplicial_attn_bwd. The workspace size function returns 0 for arguments
+ * the backward would reject.
+ */
+size_t simplicial_attn_bwd_gqa_workspace_size(int64_t B, int64_t N, int64_t H, int64_t Hkv,
+                                              int64_t D, int32_t w1, int32_t w2, int32_t dtype);
+int simplicial_attn_bwd_gqa(const void* q, const void* k, const void* kp, const void* v,
+                            const void* vp, const void* out, const void* dout, const float* lse,
+                            void* dq, void* dk, void* dkp, void* dv, void* dvp, void* workspace,
+                            size_t workspace_bytes, int64_t B, int64_t N, int64_t H, int64_t Hkv,
+                            int64_t D, int32_t w1, int32_t w2, float scale, int32_t dtype,
+                            void* stream);
 
 /*
  * The backward in three stages, for callers that schedule them themselves.

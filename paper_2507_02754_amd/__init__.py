@@ -15,11 +15,14 @@ from .binding import (  # noqa: F401
     load_library,
     simplicial_attn_abi_version,
     simplicial_attn_bwd,
+    simplicial_attn_bwd_gqa,
+    simplicial_attn_bwd_gqa_workspace_size,
     simplicial_attn_bwd_key_side,
     simplicial_attn_bwd_preprocess,
     simplicial_attn_bwd_query_side,
     simplicial_attn_bwd_workspace_size,
     simplicial_attn_error_string,
     simplicial_attn_fwd,
+    simplicial_attn_fwd_gqa,
     simplicial_attn_path_name,
 )

@@ -3,13 +3,16 @@
 No arithmetic of its own: the forward is `simplicial_attn_fwd`, the backward
 is `simplicial_attn_bwd` (Section 7's split backward: Delta, the key-side and
 the query-side kernels), both called through the ctypes binding. Tensors are
-[B, N, H, D] on one GPU, bf16 or fp32; the window lengths and the scale are
-plain Python numbers (not differentiated).
+[B, N, H, D] on one GPU, bf16 or fp32; when K, K', V, V' have fewer heads
+(Hkv dividing H: grouped-query attention) the `_gqa` entry points are used.
+The window lengths and the scale are plain Python numbers (not
+differentiated).
 """
 
 import torch
 
-from .binding import simplicial_attn_bwd, simplicial_attn_fwd
+from .binding import (simplicial_attn_bwd, simplicial_attn_bwd_gqa, simplicial_attn_fwd,
+                      simplicial_attn_fwd_gqa)
 
 __all__ = ["SimplicialAttnFunction", "simplicial_attention"]
 
@@ -21,7 +24,8 @@ class SimplicialAttnFunction(torch.autograd.Function):
     @staticmethod
     def forward(ctx, q, k, kp, v, vp, w1, w2, scale):
         q, k, kp, v, vp = (x.contiguous() for x in (q, k, kp, v, vp))
-        out, lse = simplicial_attn_fwd(q, k, kp, v, vp, w1, w2, scale)
+        fwd = simplicial_attn_fwd if k.shape[2] == q.shape[2] else simplicial_attn_fwd_gqa
+        out, lse = fwd(q, k, kp, v, vp, w1, w2, scale)
         ctx.save_for_backward(q, k, kp, v, vp, out, lse)
         ctx.windows = (w1, w2, scale)
         ctx.mark_non_differentiable(lse)
@@ -34,15 +38,17 @@ class SimplicialAttnFunction(torch.autograd.Function):
         w1, w2, scale = ctx.windows
         if dout is None:
             dout = torch.zeros_like(out)
-        grads = simplicial_attn_bwd(q, k, kp, v, vp, out, dout.to(out.dtype).contiguous(), lse,
-                                    w1, w2, scale)
+        bwd = simplicial_attn_bwd if k.shape[2] == q.shape[2] else simplicial_attn_bwd_gqa
+        grads = bwd(q, k, kp, v, vp, out, dout.to(out.dtype).contiguous(), lse, w1, w2, scale)
         return (*grads, None, None, None)
 
 
 def simplicial_attention(q, k, kp, v, vp, w1, w2, scale=None):
     """O = 2-simplicial attention(Q, K, K', V, V') with autograd support.
 
-    `scale` defaults to 1/sqrt(D).
+    q is [B, N, H, D]; k, kp, v, vp are [B, N, H, D] or, for grouped-query
+    attention, [B, N, Hkv, D] with H a multiple of Hkv. `scale` defaults to
+    1/sqrt(D).
     """
     if scale is None:
         scale = q.shape[-1] ** -0.5

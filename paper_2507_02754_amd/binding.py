@@ -17,7 +17,10 @@ __all__ = [
     "SimplicialAttnError",
     "load_library",
     "simplicial_attn_fwd",
+    "simplicial_attn_fwd_gqa",
     "simplicial_attn_bwd",
+    "simplicial_attn_bwd_gqa",
+    "simplicial_attn_bwd_gqa_workspace_size",
     "simplicial_attn_bwd_preprocess",
     "simplicial_attn_bwd_query_side",
     "simplicial_attn_bwd_key_side",
@@ -56,8 +59,14 @@ def load_library():
     vp, i64, i32, f32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_float
     lib.simplicial_attn_fwd.argtypes = [vp] * 7 + [i64] * 4 + [i32, i32, f32, i32, vp]
     lib.simplicial_attn_fwd.restype = ctypes.c_int
+    lib.simplicial_attn_fwd_gqa.argtypes = [vp] * 7 + [i64] * 5 + [i32, i32, f32, i32, vp]
+    lib.simplicial_attn_fwd_gqa.restype = ctypes.c_int
     lib.simplicial_attn_bwd.argtypes = [vp] * 14 + [ctypes.c_size_t] + [i64] * 4 + [i32, i32, f32, i32, vp]
     lib.simplicial_attn_bwd.restype = ctypes.c_int
+    lib.simplicial_attn_bwd_gqa.argtypes = [vp] * 14 + [ctypes.c_size_t] + [i64] * 5 + [i32, i32, f32, i32, vp]
+    lib.simplicial_attn_bwd_gqa.restype = ctypes.c_int
+    lib.simplicial_attn_bwd_gqa_workspace_size.argtypes = [i64] * 5 + [i32, i32, i32]
+    lib.simplicial_attn_bwd_gqa_workspace_size.restype = ctypes.c_size_t
     lib.simplicial_attn_bwd_preprocess.argtypes = [vp] * 3 + [ctypes.c_size_t] + [i64] * 4 + [i32, i32, i32, vp]
     lib.simplicial_attn_bwd_preprocess.restype = ctypes.c_int
     lib.simplicial_attn_bwd_query_side.argtypes = [vp] * 11 + [ctypes.c_size_t] + [i64] * 4 + [i32, i32, f32, i32, vp]
@@ -93,6 +102,12 @@ def simplicial_attn_path_name(which, B, N, H, D, w1, w2, dtype):
 def simplicial_attn_bwd_workspace_size(B, N, H, D, w1, w2, dtype):
     dt = _DTYPES.get(dtype, dtype)
     return int(load_library().simplicial_attn_bwd_workspace_size(B, N, H, D, int(w1), int(w2), int(dt)))
+
+
+def simplicial_attn_bwd_gqa_workspace_size(B, N, H, Hkv, D, w1, w2, dtype):
+    dt = _DTYPES.get(dtype, dtype)
+    return int(load_library().simplicial_attn_bwd_gqa_workspace_size(B, N, H, Hkv, D, int(w1), int(w2),
+                                                                      int(dt)))
 
 
 def _check_inputs(tensors, names):
@@ -145,6 +160,37 @@ def simplicial_attn_fwd(q, k, kp, v, vp, w1, w2, scale=None, out=None, lse=None)
         B, N, H, D, int(w1), int(w2), float(scale), dt, _stream(q.device))
     if rc != 0:
         raise SimplicialAttnError(rc, "simplicial_attn_fwd")
+    return out, lse
+
+
+def simplicial_attn_fwd_gqa(q, k, kp, v, vp, w1, w2, scale=None, out=None, lse=None):
+    """O, LSE = forward with grouped-query attention: q [B, N, H, D] and
+    k, kp, v, vp [B, N, Hkv, D] (H a multiple of Hkv; query head h reads head
+    h // (H // Hkv)). `scale` defaults to 1/sqrt(D). Returns (out [B, N, H, D],
+    lse [B, H, N] fp32)."""
+    (B, N, Hkv, D), dt = _check_inputs((k, kp, v, vp), ("k", "kp", "v", "vp"))
+    _check_inputs((q,), ("q",))
+    if q.dim() != 4 or q.shape[0] != B or q.shape[1] != N or q.shape[3] != D or q.dtype != k.dtype \
+            or q.device != k.device:
+        raise ValueError(f"q must be [B, N, H, D] = [{B}, {N}, H, {D}] with the dtype and device of k, "
+                         f"got {tuple(q.shape)} {q.dtype} {q.device}")
+    H = q.shape[2]
+    if scale is None:
+        scale = D ** -0.5
+    if out is None:
+        out = torch.empty_like(q)
+    else:
+        _check_inputs((q, out), ("q", "out"))
+    if lse is None:
+        lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+    elif lse.shape != (B, H, N) or lse.dtype != torch.float32 or not lse.is_contiguous() \
+            or lse.device != q.device:
+        raise ValueError("lse must be a contiguous float32 [B, H, N] tensor on the inputs' device")
+    rc = load_library().simplicial_attn_fwd_gqa(
+        _ptr(q), _ptr(k), _ptr(kp), _ptr(v), _ptr(vp), _ptr(out), _ptr(lse),
+        B, N, H, Hkv, D, int(w1), int(w2), float(scale), dt, _stream(q.device))
+    if rc != 0:
+        raise SimplicialAttnError(rc, "simplicial_attn_fwd_gqa")
     return out, lse
 
 
@@ -228,4 +274,35 @@ def simplicial_attn_bwd(q, k, kp, v, vp, out, dout, lse, w1, w2, scale=None, gra
         B, N, H, D, int(w1), int(w2), float(scale), dt, _stream(q.device))
     if rc != 0:
         raise SimplicialAttnError(rc, "simplicial_attn_bwd")
+    return grads
+
+
+def simplicial_attn_bwd_gqa(q, k, kp, v, vp, out, dout, lse, w1, w2, scale=None, grads=None,
+                            workspace=None):
+    """(dQ, dK, dK', dV, dV') for simplicial_attn_fwd_gqa: q, out, dout, dQ are
+    [B, N, H, D]; k, kp, v, vp and their gradients [B, N, Hkv, D]."""
+    (B, N, H, D), dt = _check_inputs((q, out, dout), ("q", "out", "dout"))
+    (Bk, Nk, Hkv, Dk), dtk = _check_inputs((k, kp, v, vp), ("k", "kp", "v", "vp"))
+    if (Bk, Nk, Dk) != (B, N, D) or dtk != dt or k.device != q.device:
+        raise ValueError(f"k, kp, v, vp must be [B, N, Hkv, D] = [{B}, {N}, Hkv, {D}] with the dtype "
+                         f"and device of q, got {tuple(k.shape)} {k.dtype} {k.device}")
+    if scale is None:
+        scale = D ** -0.5
+    if lse.shape != (B, H, N) or lse.dtype != torch.float32 or not lse.is_contiguous() \
+            or lse.device != q.device:
+        raise ValueError("lse must be a contiguous float32 [B, H, N] tensor on the inputs' device")
+    if grads is None:
+        grads = (torch.empty_like(q), *(torch.empty_like(k) for _ in range(4)))
+    else:
+        _check_inputs((q, grads[0]), ("q", "dq"))
+        _check_inputs((k, *grads[1:]), ("k", "dk", "dkp", "dv", "dvp"))
+    need = simplicial_attn_bwd_gqa_workspace_size(B, N, H, Hkv, D, w1, w2, dt)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
+    rc = load_library().simplicial_attn_bwd_gqa(
+        _ptr(q), _ptr(k), _ptr(kp), _ptr(v), _ptr(vp), _ptr(out), _ptr(dout), _ptr(lse),
+        *(_ptr(g) for g in grads), _ptr(workspace), ctypes.c_size_t(workspace.numel()),
+        B, N, H, Hkv, D, int(w1), int(w2), float(scale), dt, _stream(q.device))
+    if rc != 0:
+        raise SimplicialAttnError(rc, "simplicial_attn_bwd_gqa")
     return grads

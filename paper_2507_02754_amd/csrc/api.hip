@@ -53,6 +53,7 @@ Shape make_shape(int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1, int32_t
   s.w2 = static_cast<int>(w2 > N ? N : w2);
   s.scale = scale;
   s.dtype = dtype;
+  s.Hkv = s.H;
   return s;
 }
 
@@ -74,6 +75,29 @@ size_t workspace_bytes_for(int64_t B, int64_t N, int64_t H, int64_t D, int32_t w
   return ((static_cast<size_t>(B * H * N) * sizeof(float)) + 255) & ~size_t(255);
 }
 
+// Backward workspace with Hkv K-side heads: the per-head backward's workspace,
+// then (Hkv < H only) K, K', V, V' expanded to H heads and the per-query-head
+// dK, dK', dV', dV before the group sum, each [B, N, H, D] of the data type.
+struct GqaLayout {
+  size_t base, per_tensor, bytes;
+};
+
+GqaLayout gqa_layout(int64_t B, int64_t N, int64_t H, int64_t Hkv, int64_t D, int32_t w1,
+                     int32_t w2, int32_t dtype) {
+  GqaLayout l{0, 0, 0};
+  if (check_sizes(B, N, H, D, w1, w2, dtype) != SA_OK) return l;
+  if (Hkv <= 0 || Hkv > H || H % Hkv != 0) return l;
+  l.base = (workspace_bytes_for(B, N, H, D, w1, w2, dtype) + 255) & ~size_t(255);
+  if (Hkv == H) {
+    l.bytes = workspace_bytes_for(B, N, H, D, w1, w2, dtype);
+    return l;
+  }
+  const size_t esize = dtype == SA_DTYPE_BF16 ? 2 : 4;
+  l.per_tensor = (static_cast<size_t>(B * N * H * D) * esize + 255) & ~size_t(255);
+  l.bytes = l.base + 8 * l.per_tensor;
+  return l;
+}
+
 int to_status(hipError_t e) { return e == hipSuccess ? SA_OK : SA_ERR_HIP; }
 
 // Common validation of the backward entry points (pointers checked by callers).
@@ -84,6 +108,25 @@ int check_bwd(int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1, int32_t w2
   if (rc != SA_OK) return rc;
   if (workspace_bytes < workspace_bytes_for(B, N, H, D, w1, w2, dtype)) return SA_ERR_WORKSPACE;
   return SA_OK;
+}
+
+// Forward with Hkv K/V heads (Hkv == H: the plain forward).
+int forward(const void* q, const void* k, const void* kp, const void* v, const void* vp, void* out,
+            float* lse, int64_t B, int64_t N, int64_t H, int64_t Hkv, int64_t D, int32_t w1,
+            int32_t w2, float scale, int32_t dtype, void* stream) {
+  if (check_ptrs({q, k, kp, v, vp, out, lse}) != SA_OK) return SA_ERR_INVALID;
+  if (!isfinite(scale)) return SA_ERR_INVALID;
+  if (Hkv <= 0 || Hkv > H || H % Hkv != 0) return SA_ERR_INVALID;
+  const int rc = check_sizes(B, N, H, D, w1, w2, dtype);
+  if (rc != SA_OK) return rc;
+  Shape s = make_shape(B, N, H, D, w1, w2, scale, dtype);
+  s.Hkv = static_cast<int>(Hkv);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  switch (choose_path(0, B, N, H, D, w1, w2, dtype)) {
+    case Path::Generic: return to_status(sa::generic_fwd(s, q, k, kp, v, vp, out, lse, st));
+    case Path::Mfma: return to_status(sa::mfma_fwd(s, q, k, kp, v, vp, out, lse, st));
+    default: return SA_ERR_UNSUPPORTED;
+  }
 }
 
 int run_delta(const Shape& s, Path path, const void* out, const void* dout, void* workspace,
@@ -132,17 +175,14 @@ const char* simplicial_attn_path_name(int32_t which, int64_t B, int64_t N, int64
 int simplicial_attn_fwd(const void* q, const void* k, const void* kp, const void* v, const void* vp,
                         void* out, float* lse, int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1,
                         int32_t w2, float scale, int32_t dtype, void* stream) {
-  if (check_ptrs({q, k, kp, v, vp, out, lse}) != SA_OK) return SA_ERR_INVALID;
-  if (!isfinite(scale)) return SA_ERR_INVALID;
-  const int rc = check_sizes(B, N, H, D, w1, w2, dtype);
-  if (rc != SA_OK) return rc;
-  const Shape s = make_shape(B, N, H, D, w1, w2, scale, dtype);
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  switch (choose_path(0, B, N, H, D, w1, w2, dtype)) {
-    case Path::Generic: return to_status(sa::generic_fwd(s, q, k, kp, v, vp, out, lse, st));
-    case Path::Mfma: return to_status(sa::mfma_fwd(s, q, k, kp, v, vp, out, lse, st));
-    default: return SA_ERR_UNSUPPORTED;
-  }
+  return forward(q, k, kp, v, vp, out, lse, B, N, H, H, D, w1, w2, scale, dtype, stream);
+}
+
+int simplicial_attn_fwd_gqa(const void* q, const void* k, const void* kp, const void* v,
+                            const void* vp, void* out, float* lse, int64_t B, int64_t N, int64_t H,
+                            int64_t Hkv, int64_t D, int32_t w1, int32_t w2, float scale,
+                            int32_t dtype, void* stream) {
+  return forward(q, k, kp, v, vp, out, lse, B, N, H, Hkv, D, w1, w2, scale, dtype, stream);
 }
 
 size_t simplicial_attn_bwd_workspace_size(int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1,
@@ -206,6 +246,48 @@ int simplicial_attn_bwd(const void* q, const void* k, const void* kp, const void
   if (r != SA_OK) return r;
   return run_stage(s, path, BwdStage::Key, q, k, kp, v, vp, dout, lse, dk, dv, nullptr, workspace,
                    st);
+}
+
+size_t simplicial_attn_bwd_gqa_workspace_size(int64_t B, int64_t N, int64_t H, int64_t Hkv,
+                                              int64_t D, int32_t w1, int32_t w2, int32_t dtype) {
+  return gqa_layout(B, N, H, Hkv, D, w1, w2, dtype).bytes;
+}
+
+int simplicial_attn_bwd_gqa(const void* q, const void* k, const void* kp, const void* v,
+                            const void* vp, const void* out, const void* dout, const float* lse,
+                            void* dq, void* dk, void* dkp, void* dv, void* dvp, void* workspace,
+                            size_t workspace_bytes, int64_t B, int64_t N, int64_t H, int64_t Hkv,
+                            int64_t D, int32_t w1, int32_t w2, float scale, int32_t dtype,
+                            void* stream) {
+  if (check_ptrs({q, k, kp, v, vp, out, dout, lse, dq, dk, dkp, dv, dvp, workspace}) != SA_OK)
+    return SA_ERR_INVALID;
+  if (Hkv <= 0 || Hkv > H || H % Hkv != 0) return SA_ERR_INVALID;
+  const int rc = check_bwd(B, N, H, D, w1, w2, scale, dtype, workspace_bytes);
+  if (rc != SA_OK) return rc;
+  const GqaLayout l = gqa_layout(B, N, H, Hkv, D, w1, w2, dtype);
+  if (workspace_bytes < l.bytes) return SA_ERR_WORKSPACE;
+  if (Hkv == H)
+    return simplicial_attn_bwd(q, k, kp, v, vp, out, dout, lse, dq, dk, dkp, dv, dvp, workspace,
+                               workspace_bytes, B, N, H, D, w1, w2, scale, dtype, stream);
+  Shape s = make_shape(B, N, H, D, w1, w2, scale, dtype);
+  s.Hkv = static_cast<int>(Hkv);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  void* ex[4];  // K, K', V, V' expanded to H heads
+  void* gx[4];  // per-query-head dK, dK', dV, dV'
+  for (int t = 0; t < 4; ++t) {
+    ex[t] = ws + l.base + t * l.per_tensor;
+    gx[t] = ws + l.base + (4 + t) * l.per_tensor;
+  }
+  const void* src[4] = {k, kp, v, vp};
+  int r = to_status(sa::gqa_expand(s, src, ex, st));
+  if (r != SA_OK) return r;
+  r = simplicial_attn_bwd(q, ex[0], ex[1], ex[2], ex[3], out, dout, lse, dq, gx[0], gx[1], gx[2],
+                          gx[3], workspace, l.base, B, N, H, D, w1, w2, scale, dtype, stream);
+  if (r != SA_OK) return r;
+  const void* gsrc[4] = {gx[0], gx[1], gx[2], gx[3]};
+  void* gdst[4] = {dk, dkp, dv, dvp};
+  return to_status(sa::gqa_group_sum(s, gsrc, gdst, st));
 }
 
 }  // extern "C"

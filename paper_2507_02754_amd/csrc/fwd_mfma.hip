@@ -120,8 +120,13 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, c = lane & 31, h = lane >> 5;
   const int qs = wave / G, g = wave % G;
+  // Q-side tensors (q, out) have H heads; K-side ones (k, k', v, v') Hkv,
+  // query head hh reading K-side head hh / (H / Hkv) (grouped-query attention;
+  // Hkv == H otherwise).
   const size_t rs = static_cast<size_t>(s.H) * D;
   const size_t base = (static_cast<size_t>(b) * s.N * s.H + hh) * D;
+  const size_t rskv = static_cast<size_t>(s.Hkv) * D;
+  const size_t kvbase = (static_cast<size_t>(b) * s.N * s.Hkv + hh / (s.H / s.Hkv)) * D;
   const int N = s.N, w1 = s.w1, w2 = s.w2;
   const int i0 = tile * QW;
   const int i = i0 + qs;
@@ -133,9 +138,10 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
 
   const int jlo = i0 - w1 + 1;
   const int nb = (w1 + QW - 1 + 31) / 32;
-  const int rsb = static_cast<int>(rs) * 2;
-  const __amdgpu_buffer_rsrc_t rk = make_rsrc(k + base, head_bytes(N, rsb, D));
-  const __amdgpu_buffer_rsrc_t rv = make_rsrc(v + base, head_bytes(N, rsb, D));
+  const int rsbq = static_cast<int>(rs) * 2;     // bytes between rows of q, out
+  const int rsb = static_cast<int>(rskv) * 2;    // bytes between rows of k, k', v, v'
+  const __amdgpu_buffer_rsrc_t rk = make_rsrc(k + kvbase, head_bytes(N, rsb, D));
+  const __amdgpu_buffer_rsrc_t rv = make_rsrc(v + kvbase, head_bytes(N, rsb, D));
 
   // Per-lane LDS byte offsets inside a tile. K row fragment t: row c,
   // columns 16t + 8h .. + 7. Transposed V fragment (dt, u): two
@@ -202,17 +208,17 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
       }
     }
   };
-  const __amdgpu_buffer_rsrc_t rq = make_rsrc(q + base, head_bytes(N, rsb, D));
-  const __amdgpu_buffer_rsrc_t rkp = make_rsrc(kp + base, head_bytes(N, rsb, D));
-  const __amdgpu_buffer_rsrc_t rvp = make_rsrc(vp + base, head_bytes(N, rsb, D));
+  const __amdgpu_buffer_rsrc_t rq = make_rsrc(q + base, head_bytes(N, rsbq, D));
+  const __amdgpu_buffer_rsrc_t rkp = make_rsrc(kp + kvbase, head_bytes(N, rsb, D));
+  const __amdgpu_buffer_rsrc_t rvp = make_rsrc(vp + kvbase, head_bytes(N, rsb, D));
   const int kk0 = i0 - 31;  // first k of the staged k' / v' rows (w2 <= 32)
   // 64-lane loads x of staging rows: row r of the 64 x 16 bytes is p / CH
   // for p = 64 x + lane, its chunk goes to slot (p % CH) ^ (r % CH).
-  auto stage = [&](__amdgpu_buffer_rsrc_t r, int x, int row0) __attribute__((always_inline)) {
+  auto stage = [&](__amdgpu_buffer_rsrc_t r, int rstride, int x, int row0) __attribute__((always_inline)) {
     const int p = 64 * x + lane, rr = p / T::CH;
     const int ch = (p % T::CH) ^ (rr % T::CH);
     const int row = min(max(row0 + rr, 0), N - 1);
-    load_lds16(r, to_lds(stg) + 1024 * x, row * rsb + 16 * ch);
+    load_lds16(r, to_lds(stg) + 1024 * x, row * rstride + 16 * ch);
   };
   u32x4_t qt[NT];
   if constexpr (G == 1) {
@@ -224,9 +230,9 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
 #pragma unroll
     for (int x = wave; x < KI + 1; x += kWaves) {
       if (x < KI)
-        stage(rkp, x, kk0);
+        stage(rkp, rsb, x, kk0);
       else
-        stage(rq, x, i0 - KR);
+        stage(rq, rsbq, x, i0 - KR);
     }
     load_tile(rk, kst(IC<0>{}), 0);
     load_tile(rk, kst(IC<1>{}), 1);
@@ -247,7 +253,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
     u32x4_t qa[NT], ka[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
-      qa[t] = ldbuf128(rq, rowvalid ? i * rsb + 32 * t + 16 * h : -1);
+      qa[t] = ldbuf128(rq, rowvalid ? i * rsbq + 32 * t + 16 * h : -1);
       ka[t] = ldbuf128(rkp, rowvalid ? kk * rsb + 32 * t + 16 * h : -1);
     }
 #pragma unroll
@@ -333,7 +339,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
       // has read before the barrier above.
       if (blk == 0) {
 #pragma unroll
-        for (int x = wave; x < KI; x += kWaves) stage(rvp, x, kk0);
+        for (int x = wave; x < KI; x += kWaves) stage(rvp, rsb, x, kk0);
       }
     }
     // V(blk) fragments, in flight while S(blk + 1) and P(blk) are formed.

@@ -100,12 +100,14 @@ __device__ float block_sum_vec(float (&acc)[D], float* red /* [kWaves * D] */) {
   return r;
 }
 
-// Row pointer helper for [B, N, H, D] tensors: base of (b, 0, h, 0), stride H*D.
+// Row pointer helper for [B, N, heads, D] tensors: base of (b, 0, h, 0),
+// stride heads*D (heads = H for Q-side tensors, Hkv for K/V-side ones).
 struct Rows {
   size_t base, stride;
-  __device__ Rows(int b, int h, const Shape& s)
-      : base((static_cast<size_t>(b) * s.N * s.H + h) * s.D),
-        stride(static_cast<size_t>(s.H) * s.D) {}
+  __device__ Rows(int b, int h, const Shape& s) : Rows(b, h, s.H, s) {}
+  __device__ Rows(int b, int h, int heads, const Shape& s)
+      : base((static_cast<size_t>(b) * s.N * heads + h) * s.D),
+        stride(static_cast<size_t>(heads) * s.D) {}
   __device__ size_t at(int n) const { return base + static_cast<size_t>(n) * stride; }
 };
 
@@ -128,7 +130,8 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(Shape s, const T* __restr
   const int i = blockIdx.x % s.N;
   const int bh = blockIdx.x / s.N;
   const int b = bh / s.H, h = bh % s.H;
-  const Rows rows(b, h, s);
+  const Rows rows(b, h, s);                          // q, out
+  const Rows kvr(b, h / (s.H / s.Hkv), s.Hkv, s);    // k, k', v, v'
   __shared__ float qs[D];
   __shared__ float red[kWaves * D];
   __shared__ float sred[kWaves];
@@ -142,7 +145,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(Shape s, const T* __restr
   float m = -INFINITY;
   for (int p = threadIdx.x; p < np; p += kThreads) {
     const int j = j0 + p / nk, kk = k0 + p % nk;
-    m = fmaxf(m, tri<T, D>(qs, k + rows.at(j), kp + rows.at(kk)));
+    m = fmaxf(m, tri<T, D>(qs, k + kvr.at(j), kp + kvr.at(kk)));
   }
   m = block_max(m, sred);
 
@@ -152,10 +155,10 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(Shape s, const T* __restr
   for (int d = 0; d < D; ++d) acc[d] = 0.f;
   for (int p = threadIdx.x; p < np; p += kThreads) {
     const int j = j0 + p / nk, kk = k0 + p % nk;
-    const float e = expf(tri<T, D>(qs, k + rows.at(j), kp + rows.at(kk)) - m);
+    const float e = expf(tri<T, D>(qs, k + kvr.at(j), kp + kvr.at(kk)) - m);
     l += e;
-    const T* vj = v + rows.at(j);
-    const T* vk = vp + rows.at(kk);
+    const T* vj = v + kvr.at(j);
+    const T* vk = vp + kvr.at(kk);
 #pragma unroll
     for (int d = 0; d < D; ++d) acc[d] += e * ld(vj + d) * ld(vk + d);
   }

@@ -16,6 +16,10 @@ struct Shape {
   int w1, w2;
   float scale;
   int dtype;  // SA_DTYPE_*
+  // Heads of K, K', V, V' (grouped-query attention: query head h reads K/V
+  // head h / (H / Hkv)). Only the forward kernels and the GQA helpers below
+  // read it; the backward kernels run per query head with Hkv == H.
+  int Hkv;
 };
 
 // bf16 is carried as raw 16-bit patterns (uint16_t) in every kernel.
@@ -76,6 +80,17 @@ hipError_t mfma_bwd_query(const Shape& s, const BwdPlan& plan, const void* q, co
                           const void* kp, const void* v, const void* vp, const void* dout,
                           const float* lse, const float* delta, void* dq, void* dkp, void* dvp,
                           float* halo, hipStream_t st);
+
+// Grouped-query backward helpers (s.H query heads, s.Hkv K-side heads; the
+// four src/dst pointers are K, K', V, V' or their gradients).
+// gqa_expand: dst[t] [B, N, H, D] = src[t] [B, N, Hkv, D] with head h taken
+// from K-side head h / (H / Hkv).
+hipError_t gqa_expand(const Shape& s, const void* const src[4], void* const dst[4],
+                      hipStream_t st);
+// gqa_group_sum: dst[t] [B, N, Hkv, D] = fp32 sum over each group's query
+// heads (ascending) of src[t] [B, N, H, D], rounded once to the data type.
+hipError_t gqa_group_sum(const Shape& s, const void* const src[4], void* const dst[4],
+                         hipStream_t st);
 
 // Delta_i = <dO_i, O_i> for every query, [B, H, N] float32.
 hipError_t launch_delta(const Shape& s, const void* out, const void* dout, float* delta,

@@ -142,6 +142,70 @@ def full_oracle(inputs, w1, w2, scale, backward=True):
     return o, lse, grads
 
 
+def gqa_oracle_forward(q, kv, w1, w2, scale, heads=None, rows=None):
+    """Oracle forward with grouped-query attention: q [B, N, H, D], kv = (k, kp,
+    v, vp) each [B, N, Hkv, D]; query head h reads K-side head h // (H // Hkv).
+    Returns {(b, h): (o [N, D], lse [N])} for the requested heads (all if None),
+    computed on the given query rows (all if None)."""
+    B, N, H, D = q.shape
+    Hkv = kv[0].shape[2]
+    g = H // Hkv
+    heads = heads if heads is not None else [(b, h) for b in range(B) for h in range(H)]
+    res = {}
+    for (b, h) in heads:
+        qa = q[b, :, h, :].to(torch.float64).numpy()
+        ka = [x[b, :, h // g, :].to(torch.float64).numpy() for x in kv]
+        res[(b, h)] = orc.forward(qa, *ka, w1, w2, scale, queries=rows)
+    return res
+
+
+def gqa_oracle_backward(q, kv, do, w1, w2, scale, b_heads=None, queries=None):
+    """Oracle backward with grouped-query attention (chain rule over shared
+    K-side heads): per query head h, the oracle's gradients with K-side head
+    h // G; dQ stays per query head, dK, dK', dV, dV' of K-side head hk are the
+    fp64 sums over query heads hk*G .. hk*G + G - 1. `b_heads` restricts the
+    work to the listed (b, hk) K-side heads (all if None; others stay 0),
+    `queries` to the listed query rows (as the oracle's backward).
+    Returns dq [B, N, H, D] and dk, dkp, dv, dvp [B, N, Hkv, D] (fp64)."""
+    B, N, H, D = q.shape
+    Hkv = kv[0].shape[2]
+    g = H // Hkv
+    b_heads = b_heads if b_heads is not None else [(b, hk) for b in range(B) for hk in range(Hkv)]
+    dq = np.zeros((B, N, H, D))
+    dkv = [np.zeros((B, N, Hkv, D)) for _ in range(4)]
+    for (b, hk) in b_heads:
+        ka = [x[b, :, hk, :].to(torch.float64).numpy() for x in kv]
+        for h in range(hk * g, hk * g + g):
+            qa = q[b, :, h, :].to(torch.float64).numpy()
+            da = do[b, :, h, :].to(torch.float64).numpy()
+            gr = orc.backward(qa, *ka, da, w1, w2, scale, queries=queries)
+            dq[b, :, h, :] = gr[0]
+            for t in range(4):
+                dkv[t][b, :, hk, :] += gr[1 + t]
+    return dq, dkv
+
+
+def gqa_composite_backward(q, kv, out, do, lse, w1, w2, scale):
+    """The grouped-query backward composed from the library's per-head entry
+    point on the GPU: K, K', V, V' repeated per query head, the plain backward,
+    then each group's K-side gradients summed in fp32 in ascending head order
+    and rounded once. The library's GQA backward is specified to equal this bit
+    for bit."""
+    H, Hkv = q.shape[2], kv[0].shape[2]
+    g = H // Hkv
+    rep = [x.repeat_interleave(g, dim=2).contiguous() for x in kv]
+    grads = simplicial_attn_bwd(q, *rep, out, do, lse, w1, w2, scale)
+    torch.cuda.synchronize()
+    summed = []
+    for t in range(1, 5):
+        x = grads[t].unflatten(2, (Hkv, g))
+        acc = x[:, :, :, 0].float()
+        for j in range(1, g):
+            acc = acc + x[:, :, :, j].float()
+        summed.append(acc.to(grads[t].dtype).contiguous())
+    return (grads[0], *summed)
+
+
 def sample_rows(n, w1, w2, extra=4, seed=0):
     """Query rows spanning the clipped start, window edges, tile edges, middle and end."""
     cand = {0, 1, 2, w2 - 1, w2, w1 - 2, w1 - 1, w1, w1 + 1, 63, 64, 255, 256,

@@ -45,7 +45,9 @@ def declared_functions():
 
 def test_header_declares_the_expected_entry_points():
     assert declared_functions() == sorted([
-        "simplicial_attn_fwd", "simplicial_attn_bwd", "simplicial_attn_bwd_workspace_size",
+        "simplicial_attn_fwd", "simplicial_attn_fwd_gqa", "simplicial_attn_bwd",
+        "simplicial_attn_bwd_workspace_size", "simplicial_attn_bwd_gqa",
+        "simplicial_attn_bwd_gqa_workspace_size",
         "simplicial_attn_error_string", "simplicial_attn_abi_version", "simplicial_attn_path_name",
         "simplicial_attn_bwd_preprocess", "simplicial_attn_bwd_query_side",
         "simplicial_attn_bwd_key_side",
@@ -107,6 +109,72 @@ def test_forward_rejects_invalid_arguments(lib):
     assert _fwd(lib, D=256) == 2
     assert _fwd(lib, dtype=2) == 2
     assert _fwd(lib, dtype=-1) == 2
+
+
+def _fwd_gqa(lib, ptrs=None, B=1, N=64, H=4, Hkv=2, D=128, w1=16, w2=8, scale=0.1, dtype=1):
+    ptrs = ptrs or [A] * 7
+    return lib.simplicial_attn_fwd_gqa(*[ctypes.c_void_p(p) for p in ptrs], B, N, H, Hkv, D, w1, w2,
+                                       ctypes.c_float(scale), dtype, None)
+
+
+@only_without_gpu
+def test_gqa_forward_rejects_invalid_arguments(lib):
+    for i in range(7):
+        ptrs = [A] * 7
+        ptrs[i] = 0
+        assert _fwd_gqa(lib, ptrs) == 1, f"null pointer {i}"
+        ptrs[i] = MISALIGNED
+        assert _fwd_gqa(lib, ptrs) == 1, f"misaligned pointer {i}"
+    assert _fwd_gqa(lib, Hkv=0) == 1
+    assert _fwd_gqa(lib, Hkv=-2) == 1
+    assert _fwd_gqa(lib, H=4, Hkv=8) == 1   # more K-side heads than query heads
+    assert _fwd_gqa(lib, H=6, Hkv=4) == 1   # not a multiple
+    assert _fwd_gqa(lib, w1=0) == 1
+    assert _fwd_gqa(lib, scale=float("nan")) == 1
+    assert _fwd_gqa(lib, D=48) == 2
+    assert _fwd_gqa(lib, dtype=5) == 2
+
+
+def _bwd_gqa(lib, ptrs=None, ws_bytes=1 << 40, B=1, N=64, H=4, Hkv=2, D=128, w1=16, w2=8, scale=0.1,
+             dtype=1):
+    ptrs = ptrs or [A] * 14
+    return lib.simplicial_attn_bwd_gqa(*[ctypes.c_void_p(p) for p in ptrs], ctypes.c_size_t(ws_bytes),
+                                       B, N, H, Hkv, D, w1, w2, ctypes.c_float(scale), dtype, None)
+
+
+@only_without_gpu
+def test_gqa_backward_rejects_invalid_arguments(lib):
+    for i in range(14):
+        ptrs = [A] * 14
+        ptrs[i] = 0
+        assert _bwd_gqa(lib, ptrs) == 1, f"null pointer {i}"
+        ptrs[i] = MISALIGNED
+        assert _bwd_gqa(lib, ptrs) == 1, f"misaligned pointer {i}"
+    assert _bwd_gqa(lib, Hkv=0) == 1
+    assert _bwd_gqa(lib, H=4, Hkv=8) == 1
+    assert _bwd_gqa(lib, H=6, Hkv=4) == 1
+    assert _bwd_gqa(lib, w2=0) == 1
+    assert _bwd_gqa(lib, scale=float("inf")) == 1
+    assert _bwd_gqa(lib, D=40) == 2
+    need = binding.simplicial_attn_bwd_gqa_workspace_size(1, 64, 4, 2, 128, 16, 8, 1)
+    assert _bwd_gqa(lib, ws_bytes=need - 1) == 3
+    assert _bwd_gqa(lib, ws_bytes=0) == 3
+
+
+def test_gqa_workspace_size(lib):
+    f = binding.simplicial_attn_bwd_gqa_workspace_size
+    plain = binding.simplicial_attn_bwd_workspace_size
+    assert f(1, 64, 4, 3, 128, 16, 8, 1) == 0      # Hkv does not divide H
+    assert f(1, 64, 4, 0, 128, 16, 8, 1) == 0
+    assert f(1, 64, 4, 2, 48, 16, 8, 1) == 0
+    # Hkv == H: the plain backward's workspace
+    assert f(2, 8192, 8, 8, 128, 512, 32, 1) == plain(2, 8192, 8, 128, 512, 32, 1)
+    # Hkv < H: plus eight [B, N, H, D] tensors of the data type
+    for (b, n, h, hkv, d, w1, w2, dt, es) in [(1, 64, 4, 2, 128, 16, 8, 1, 2),
+                                              (2, 100, 6, 1, 32, 9, 5, 0, 4)]:
+        ws = f(b, n, h, hkv, d, w1, w2, dt)
+        assert ws >= plain(b, n, h, d, w1, w2, dt) + 8 * b * n * h * d * es
+        assert ws <= plain(b, n, h, d, w1, w2, dt) + 8 * (b * n * h * d * es + 255) + 255
 
 
 @only_without_gpu

@@ -116,6 +116,151 @@ def test_forward_tile_runs(d, w1, w2):
                             f"tile runs D={d} w1={w1} w2={w2}")
 
 
+GQA = [
+    # (B, H, Hkv, N, D, w1, w2, dtype)
+    (1, 4, 2, 300, 128, 64, 32, "bf16"),   # MFMA path, two query heads per K-side head
+    (2, 8, 1, 200, 64, 40, 32, "bf16"),    # head_dim 64, all query heads on one K-side head
+    (1, 4, 2, 333, 128, 96, 64, "bf16"),   # w2 = 64 (two wavefronts per query)
+    (1, 6, 3, 100, 64, 7, 5, "fp32"),      # generic path
+    (1, 3, 3, 129, 128, 33, 7, "bf16"),    # Hkv == H
+    (1, 64, 1, 96, 64, 40, 32, "bf16"),    # 64 query heads per K-side head (Section 6's ratio)
+]
+
+
+def _gqa_inputs(b, h, hkv, n, d, dt, seed):
+    tdt = torch.float32 if dt == "fp32" else torch.bfloat16
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    q = torch.randn((b, n, h, d), generator=g).to(tdt)
+    kv = [torch.randn((b, n, hkv, d), generator=g).to(tdt) for _ in range(4)]
+    do = torch.randn((b, n, h, d), generator=g).to(tdt)
+    return q, kv, do
+
+
+@pytest.mark.parametrize("shape", GQA, ids=[str(s) for s in GQA])
+def test_gqa_forward(shape):
+    """Grouped-query forward against the oracle (query head h reads K-side head
+    h // (H // Hkv)), and bit for bit against the plain forward on K, K', V, V'
+    repeated per query head."""
+    from paper_2507_02754_amd import simplicial_attn_fwd_gqa
+
+    b, h, hkv, n, d, w1, w2, dt = shape
+    _announce(f"gqa {shape}")
+    tdt = torch.float32 if dt == "fp32" else torch.bfloat16
+    g = torch.Generator(device="cpu").manual_seed(500 + n + h)
+    q = torch.randn((b, n, h, d), generator=g).to(tdt)
+    kv = [torch.randn((b, n, hkv, d), generator=g).to(tdt) for _ in range(4)]
+    scale = d ** -0.5
+    o, lse = simplicial_attn_fwd_gqa(q.cuda(), *(x.cuda() for x in kv), w1, w2, scale)
+    torch.cuda.synchronize()
+    rep = [x.repeat_interleave(h // hkv, dim=2).contiguous() for x in kv]
+    o_m, lse_m = simplicial_attn_fwd(q.cuda(), *(x.cuda() for x in rep), w1, w2, scale)
+    torch.cuda.synchronize()
+    assert torch.equal(o, o_m) and torch.equal(lse, lse_m), "GQA forward differs from repeated K/V"
+    ref = P.gqa_oracle_forward(q, kv, w1, w2, scale)
+    o_ref = np.stack([np.stack([ref[(bb, hh)][0] for hh in range(h)], axis=1) for bb in range(b)])
+    lse_ref = np.stack([np.stack([ref[(bb, hh)][1] for hh in range(h)]) for bb in range(b)])
+    P.check_forward(P.to64(o), P.to64(lse), o_ref, lse_ref, dt, f"gqa {shape}")
+
+
+@pytest.mark.parametrize("shape", GQA, ids=[str(s) for s in GQA])
+def test_gqa_backward(shape):
+    """Grouped-query backward: bit for bit the per-head backward on repeated
+    K, K', V, V' with each group's K-side gradients summed in fp32, and against
+    the oracle (chain rule over the shared K-side heads)."""
+    from paper_2507_02754_amd import simplicial_attn_bwd_gqa, simplicial_attn_fwd_gqa
+
+    b, h, hkv, n, d, w1, w2, dt = shape
+    _announce(f"gqa backward {shape}")
+    q, kv, do = _gqa_inputs(b, h, hkv, n, d, dt, 900 + n + h)
+    scale = d ** -0.5
+    qc, kvc, doc = q.cuda(), [x.cuda() for x in kv], do.cuda()
+    o, lse = simplicial_attn_fwd_gqa(qc, *kvc, w1, w2, scale)
+    grads = simplicial_attn_bwd_gqa(qc, *kvc, o, doc, lse, w1, w2, scale)
+    torch.cuda.synchronize()
+    assert grads[0].shape == q.shape and all(g_.shape == kv[0].shape for g_ in grads[1:])
+    comp = P.gqa_composite_backward(qc, kvc, o, doc, lse, w1, w2, scale)
+    for name, g1, g2 in zip(P.GRAD_NAMES, grads, comp):
+        assert torch.equal(g1, g2), f"{name}: GQA backward differs from the per-head composite"
+    dq_ref, dkv_ref = P.gqa_oracle_backward(q, kv, do, w1, w2, scale)
+    P.check_grads([P.to64(g_) for g_ in grads], [dq_ref, *dkv_ref], dt, f"gqa backward {shape}")
+
+
+def test_gqa_backward_full_size_sampled():
+    """16 query heads on 2 K-side heads, N = 4096, w1 = 512, w2 = 32: the whole
+    backward bit for bit against the per-head composite, and sampled rows of
+    K-side head 0 (all 8 of its query heads) against the oracle."""
+    from paper_2507_02754_amd import simplicial_attn_bwd_gqa, simplicial_attn_fwd_gqa
+
+    b, h, hkv, n, d, w1, w2 = 1, 16, 2, 4096, 128, 512, 32
+    _announce(f"gqa backward full size B={b} H={h} Hkv={hkv} N={n} D={d} w1={w1} w2={w2}")
+    q, kv, do = _gqa_inputs(b, h, hkv, n, d, "bf16", 78)
+    q = torch.nn.functional.normalize(q.float(), dim=-1).mul(d ** 0.5).to(torch.bfloat16)
+    kv[0] = torch.nn.functional.normalize(kv[0].float(), dim=-1).mul(d ** 0.5).to(torch.bfloat16)
+    scale = d ** -0.5
+    qc, kvc, doc = q.cuda(), [x.cuda() for x in kv], do.cuda()
+    o, lse = simplicial_attn_fwd_gqa(qc, *kvc, w1, w2, scale)
+    grads = simplicial_attn_bwd_gqa(qc, *kvc, o, doc, lse, w1, w2, scale)
+    torch.cuda.synchronize()
+    comp = P.gqa_composite_backward(qc, kvc, o, doc, lse, w1, w2, scale)
+    for name, g1, g2 in zip(P.GRAD_NAMES, grads, comp):
+        assert torch.equal(g1, g2), f"{name}: GQA backward differs from the per-head composite"
+    q_rows = P.sample_rows(n, w1, w2, extra=2, seed=5)
+    key_rows = [0, 1, w2, w1 - 1, n // 2, n - 1]
+    queries = set(q_rows)
+    for r in key_rows:
+        queries.update(range(r, min(n, r + w1)))
+    dq_ref, dkv_ref = P.gqa_oracle_backward(q, kv, do, w1, w2, scale, b_heads=[(0, 0)],
+                                            queries=sorted(queries))
+    got = [P.to64(grads[0])[0][q_rows][:, :h // hkv]] + \
+          [P.to64(g_)[0][key_rows][:, 0] for g_ in grads[1:]]
+    ref = [dq_ref[0][q_rows][:, :h // hkv]] + [r_[0][key_rows][:, 0] for r_ in dkv_ref]
+    P.check_grads(got, ref, "bf16", "gqa backward full size")
+
+
+def test_autograd_gqa():
+    """torch.autograd with fewer K-side heads routes to the GQA entry points:
+    gradients equal the direct GQA backward bit for bit."""
+    from paper_2507_02754_amd import (simplicial_attention, simplicial_attn_bwd_gqa,
+                                      simplicial_attn_fwd_gqa)
+
+    b, h, hkv, n, d, w1, w2 = 1, 4, 2, 200, 128, 64, 32
+    _announce("autograd gqa")
+    q, kv, do = _gqa_inputs(b, h, hkv, n, d, "bf16", 31)
+    scale = d ** -0.5
+    leaves = [x.cuda().requires_grad_(True) for x in (q, *kv)]
+    o = simplicial_attention(*leaves, w1, w2, scale)
+    (o.float() * do.cuda().float()).sum().backward()
+    o_d, lse_d = simplicial_attn_fwd_gqa(q.cuda(), *(x.cuda() for x in kv), w1, w2, scale)
+    direct = simplicial_attn_bwd_gqa(q.cuda(), *(x.cuda() for x in kv), o_d, do.cuda(), lse_d,
+                                     w1, w2, scale)
+    assert torch.equal(o.detach(), o_d)
+    for name, lf, g2 in zip(P.GRAD_NAMES, leaves, direct):
+        assert torch.equal(lf.grad, g2), f"{name}: autograd differs from the direct GQA backward"
+
+
+def test_gqa_forward_full_size_sampled():
+    """16 query heads on 2 K-side heads, N = 8192, w1 = 512, w2 = 32: sampled rows
+    of every query head against the oracle."""
+    from paper_2507_02754_amd import simplicial_attn_fwd_gqa
+
+    b, h, hkv, n, d, w1, w2 = 1, 16, 2, 8192, 128, 512, 32
+    _announce(f"gqa full size B={b} H={h} Hkv={hkv} N={n} D={d} w1={w1} w2={w2}")
+    g = torch.Generator(device="cpu").manual_seed(77)
+    q = torch.randn((b, n, h, d), generator=g).to(torch.bfloat16)
+    kv = [torch.randn((b, n, hkv, d), generator=g).to(torch.bfloat16) for _ in range(4)]
+    scale = d ** -0.5
+    o, lse = simplicial_attn_fwd_gqa(q.cuda(), *(x.cuda() for x in kv), w1, w2, scale)
+    torch.cuda.synchronize()
+    rows = P.sample_rows(n, w1, w2, extra=6, seed=3)
+    heads = [(0, hh) for hh in range(h)]
+    ref = P.gqa_oracle_forward(q, kv, w1, w2, scale, heads=heads, rows=rows)
+    o64, l64 = P.to64(o), P.to64(lse)
+    P.check_forward(np.concatenate([o64[0, rows, hh, :] for (_, hh) in heads]),
+                    np.concatenate([l64[0, hh, rows] for (_, hh) in heads]),
+                    np.concatenate([ref[k_][0][rows] for k_ in heads]),
+                    np.concatenate([ref[k_][1][rows] for k_ in heads]), "bf16", "gqa full size")
+
+
 def _is_fast(w, which):
     return simplicial_attn_path_name(which, w.B, w.N, w.H, w.D, w.w1, w.w2, 1) != "generic"
 
