@@ -177,6 +177,19 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
   // 16 l. Rows outside [0, N) are loaded from the clamped row: they are
   // masked (p = 0), and finite data keeps 0 * v finite.
   constexpr int SPW = (T::instrs + kWaves - 1) / kWaves;  // loads per tile per wavefront
+  // When the tile's loads do not divide evenly over the wavefronts (head_dim
+  // 64: 4 loads, 8 wavefronts), the wavefronts from T::instrs % kWaves on issue
+  // SPW - 1 per tile. Every vmcnt wait counts the issuing wavefront's own
+  // loads, so it takes that wavefront's count: a wavefront with no tile loads
+  // waits for all of its staging loads.
+  const bool full_share = T::instrs % kWaves == 0 || wave < T::instrs % kWaves;
+  auto wait_tiles = [&](auto NC) __attribute__((always_inline)) {
+    constexpr int n = decltype(NC)::value;  // tiles' loads that may stay in flight
+    if (full_share)
+      wait_vmcnt<n * SPW>();
+    else
+      wait_vmcnt<n * (SPW - 1)>();
+  };
   int lrow[SPW], lcol[SPW];
 #pragma unroll
   for (int x = 0; x < SPW; ++x) {
@@ -283,7 +296,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
   if constexpr (G == 1) {
     // Staging rows, K(0) and K(1) in LDS for every wavefront; V(0) and K(2)
     // may still be in flight.
-    wait_vmcnt<2 * SPW>();
+    wait_tiles(IC<2>{});
     lds_barrier_tracked();
     // modulated queries q~ = (scale*log2 e) * q_i o k'_k as B operands, from
     // the staged rows (local k' row qs + c, q row KR + qs); rows outside the
@@ -327,8 +340,8 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
     constexpr int cur = S & 1, nxt = cur ^ 1;
     // K(blk + 2) (loaded in iteration blk - 2) and V(blk) (iteration
     // blk - 3) must be in LDS for every wavefront: wait until at most the
-    // 3 SPW loads issued after K(blk + 2) are in flight, then synchronise.
-    wait_vmcnt<3 * SPW>();
+    // 3 tiles' loads issued after K(blk + 2) are in flight, then synchronise.
+    wait_tiles(IC<3>{});
     lds_barrier_tracked();
     // K(blk + 4) replaces K(blk), read in iteration blk - 2; V(blk + 3)
     // replaces V(blk - 1), read in iteration blk - 1.
@@ -420,8 +433,9 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
   u32x2_t vpr[4 * NDT];
   if constexpr (G == 1) {
     // The v' rows (issued in iteration 0) are in LDS for every wavefront
-    // once 3 SPW later loads have been waited for and a barrier passed,
-    // which iterations 1-3 do when the window has at least 7 blocks.
+    // once 3 tiles' later loads have been waited for and a barrier passed,
+    // which iterations 1-3 do when the window has at least 7 blocks (a
+    // wavefront without tile loads waits for all of its loads there).
     if (nb < 7) {
       wait_vmcnt<0>();
       lds_barrier_tracked();
