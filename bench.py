@@ -105,6 +105,9 @@ def main():
     ap.add_argument("--gqa-kv-heads", type=int, default=0,
                     help="also time the grouped-query forward and backward with this many "
                          "K-side heads (reported under \"gqa\"; not part of the step)")
+    ap.add_argument("--det", action="store_true",
+                    help="also time the determinant-logit forward and backward (Section 5) at "
+                         "B=1, H=16, N=4096, D=128, w1=512, w2=32 (reported under \"det\")")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this build runs the hot path on one GPU only; multi-GPU sharding "
@@ -119,6 +122,7 @@ def main():
                                       simplicial_attn_bwd_workspace_size, simplicial_attn_fwd,
                                       simplicial_attn_fwd_gqa, simplicial_attn_bwd_gqa,
                                       simplicial_attn_bwd_gqa_workspace_size,
+                                      simplicial_attn_det_bwd, simplicial_attn_det_fwd,
                                       simplicial_attn_path_name)
     from paper_2507_02754_amd.workloads import WORKLOADS, make_inputs
 
@@ -272,6 +276,43 @@ def main():
                          "bwd_tflops": round(bwd_flops / (gb * 1e-3) / 1e12, 2),
                          "step_tflops": round((fwd_flops + bwd_flops) / ((gf + gb) * 1e-3) / 1e12, 2)}
         del kv, gkv, gws
+    if args.det:
+        # Determinant logits run on the plain fp32 kernels: timed on a 4096-token
+        # sequence (the windows and head shape of the main workload).
+        db, dh, dn = 1, 16, 4096
+        g = torch.Generator(device="cpu").manual_seed(11)
+        dq_, dk_, dkp_, dv_, dvp_, ddo = (torch.randn((db, dn, dh, w.D), generator=g)
+                                          .to(w.torch_dtype).to(dev) for _ in range(6))
+        dws = torch.empty(simplicial_attn_bwd_workspace_size(db, dn, dh, w.D, w.w1, w.w2, w.torch_dtype),
+                          dtype=torch.uint8, device=dev)
+        de = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        dsteps = 3
+        for it in range(dsteps + 1):  # one warm-up step, then dsteps timed
+            if it == 1:
+                de[0].record()
+            o_, l_ = simplicial_attn_det_fwd(dq_, dk_, dkp_, dv_, dvp_, w.w1, w.w2, w.scale)
+            simplicial_attn_det_bwd(dq_, dk_, dkp_, dv_, dvp_, o_, ddo, l_, w.w1, w.w2, w.scale,
+                                    workspace=dws)
+        de[1].record()
+        torch.cuda.synchronize()
+        whole = de[0].elapsed_time(de[1]) / dsteps
+        # forward / backward split from one more step
+        t_f = torch.cuda.Event(enable_timing=True)
+        t_b = torch.cuda.Event(enable_timing=True)
+        t_e = torch.cuda.Event(enable_timing=True)
+        t_f.record()
+        o_, l_ = simplicial_attn_det_fwd(dq_, dk_, dkp_, dv_, dvp_, w.w1, w.w2, w.scale)
+        t_b.record()
+        simplicial_attn_det_bwd(dq_, dk_, dkp_, dv_, dvp_, o_, ddo, l_, w.w1, w.w2, w.scale,
+                                workspace=dws)
+        t_e.record()
+        torch.cuda.synchronize()
+        dunit = float(db) * dh * dn * w.w1 * w.w2 * w.D
+        result["det"] = {"config": {"B": db, "H": dh, "N": dn, "D": w.D, "w1": w.w1, "w2": w.w2},
+                         "step_ms": round(whole, 3), "fwd_ms": round(t_f.elapsed_time(t_b), 3),
+                         "bwd_ms": round(t_b.elapsed_time(t_e), 3),
+                         "nominal_tflops": round(16 * dunit / (whole * 1e-3) / 1e12, 2),
+                         "kernels": "generic (plain fp32)"}
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(w, inputs_cpu, args.cpu_seconds)

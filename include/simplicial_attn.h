@@ -112,6 +112,28 @@ int simplicial_attn_bwd(const void* q, const void* k, const void* kp, const void
                         float scale, int32_t dtype, void* stream);
 
 /*
+ * Forward and backward with the determinant logits of Section 5, Eq. (logits)
+ * (rotation-invariant, so usable with position rotations applied to Q, K, K'):
+ *   A_ijk = scale * sum_l det([q_i^(l); k_j^(l); k'_k^(l)])
+ * over the 3-component chunks l = 0 .. floor(D/3) - 1 (components 3l .. 3l+2);
+ * for D not a multiple of 3 the D mod 3 trailing components enter no logit and
+ * get zero dQ, dK, dK'. Softmax, output, windows, arguments, layouts, workspace
+ * (simplicial_attn_bwd_workspace_size) and errors are those of
+ * simplicial_attn_fwd / simplicial_attn_bwd. Both run on the plain fp32
+ * kernels (bf16 data is converted on load and rounded on store) for every
+ * supported shape.
+ */
+int simplicial_attn_det_fwd(const void* q, const void* k, const void* kp, const void* v,
+                            const void* vp, void* out, float* lse, int64_t B, int64_t N, int64_t H,
+                            int64_t D, int32_t w1, int32_t w2, float scale, int32_t dtype,
+                            void* stream);
+int simplicial_attn_det_bwd(const void* q, const void* k, const void* kp, const void* v,
+                            const void* vp, const void* out, const void* dout, const float* lse,
+                            void* dq, void* dk, void* dkp, void* dv, void* dvp, void* workspace,
+                            size_t workspace_bytes, int64_t B, int64_t N, int64_t H, int64_t D,
+                            int32_t w1, int32_t w2, float scale, int32_t dtype, void* stream);
+
+/*
  * Backward with grouped-query attention, for the outputs of
  * simplicial_attn_fwd_gqa. Every K-side element enters the logits of all the
  * query heads of its group, so dK, dK', dV, dV' are the per-query-head

@@ -17,6 +17,8 @@ from .binding import (  # noqa: F401
     simplicial_attn_bwd,
     simplicial_attn_bwd_gqa,
     simplicial_attn_bwd_gqa_workspace_size,
+    simplicial_attn_det_bwd,
+    simplicial_attn_det_fwd,
     simplicial_attn_bwd_key_side,
     simplicial_attn_bwd_preprocess,
     simplicial_attn_bwd_query_side,

@@ -20,6 +20,8 @@ __all__ = [
     "simplicial_attn_fwd_gqa",
     "simplicial_attn_bwd",
     "simplicial_attn_bwd_gqa",
+    "simplicial_attn_det_fwd",
+    "simplicial_attn_det_bwd",
     "simplicial_attn_bwd_gqa_workspace_size",
     "simplicial_attn_bwd_preprocess",
     "simplicial_attn_bwd_query_side",
@@ -63,6 +65,10 @@ def load_library():
     lib.simplicial_attn_fwd_gqa.restype = ctypes.c_int
     lib.simplicial_attn_bwd.argtypes = [vp] * 14 + [ctypes.c_size_t] + [i64] * 4 + [i32, i32, f32, i32, vp]
     lib.simplicial_attn_bwd.restype = ctypes.c_int
+    lib.simplicial_attn_det_fwd.argtypes = lib.simplicial_attn_fwd.argtypes
+    lib.simplicial_attn_det_fwd.restype = ctypes.c_int
+    lib.simplicial_attn_det_bwd.argtypes = lib.simplicial_attn_bwd.argtypes
+    lib.simplicial_attn_det_bwd.restype = ctypes.c_int
     lib.simplicial_attn_bwd_gqa.argtypes = [vp] * 14 + [ctypes.c_size_t] + [i64] * 5 + [i32, i32, f32, i32, vp]
     lib.simplicial_attn_bwd_gqa.restype = ctypes.c_int
     lib.simplicial_attn_bwd_gqa_workspace_size.argtypes = [i64] * 5 + [i32, i32, i32]
@@ -143,6 +149,16 @@ def simplicial_attn_fwd(q, k, kp, v, vp, w1, w2, scale=None, out=None, lse=None)
 
     `scale` defaults to 1/sqrt(D). Returns (out [B, N, H, D], lse [B, H, N] fp32).
     """
+    return _fwd("simplicial_attn_fwd", q, k, kp, v, vp, w1, w2, scale, out, lse)
+
+
+def simplicial_attn_det_fwd(q, k, kp, v, vp, w1, w2, scale=None, out=None, lse=None):
+    """Forward with the determinant logits of Section 5 (arguments and results
+    as simplicial_attn_fwd)."""
+    return _fwd("simplicial_attn_det_fwd", q, k, kp, v, vp, w1, w2, scale, out, lse)
+
+
+def _fwd(entry, q, k, kp, v, vp, w1, w2, scale, out, lse):
     (B, N, H, D), dt = _check_inputs((q, k, kp, v, vp), ("q", "k", "kp", "v", "vp"))
     if scale is None:
         scale = D ** -0.5
@@ -155,11 +171,11 @@ def simplicial_attn_fwd(q, k, kp, v, vp, w1, w2, scale=None, out=None, lse=None)
     elif lse.shape != (B, H, N) or lse.dtype != torch.float32 or not lse.is_contiguous() \
             or lse.device != q.device:
         raise ValueError("lse must be a contiguous float32 [B, H, N] tensor on the inputs' device")
-    rc = load_library().simplicial_attn_fwd(
+    rc = getattr(load_library(), entry)(
         _ptr(q), _ptr(k), _ptr(kp), _ptr(v), _ptr(vp), _ptr(out), _ptr(lse),
         B, N, H, D, int(w1), int(w2), float(scale), dt, _stream(q.device))
     if rc != 0:
-        raise SimplicialAttnError(rc, "simplicial_attn_fwd")
+        raise SimplicialAttnError(rc, entry)
     return out, lse
 
 
@@ -256,6 +272,19 @@ def simplicial_attn_bwd_key_side(q, k, kp, v, vp, dout, lse, w1, w2, workspace, 
 def simplicial_attn_bwd(q, k, kp, v, vp, out, dout, lse, w1, w2, scale=None, grads=None,
                         workspace=None):
     """(dQ, dK, dK', dV, dV') = backward(...); `out`/`lse` come from the forward."""
+    return _bwd("simplicial_attn_bwd", q, k, kp, v, vp, out, dout, lse, w1, w2, scale, grads,
+                workspace)
+
+
+def simplicial_attn_det_bwd(q, k, kp, v, vp, out, dout, lse, w1, w2, scale=None, grads=None,
+                            workspace=None):
+    """Backward with the determinant logits of Section 5 (arguments and results
+    as simplicial_attn_bwd; `out`/`lse` from simplicial_attn_det_fwd)."""
+    return _bwd("simplicial_attn_det_bwd", q, k, kp, v, vp, out, dout, lse, w1, w2, scale, grads,
+                workspace)
+
+
+def _bwd(entry, q, k, kp, v, vp, out, dout, lse, w1, w2, scale, grads, workspace):
     (B, N, H, D), dt = _check_inputs((q, k, kp, v, vp, out, dout),
                                      ("q", "k", "kp", "v", "vp", "out", "dout"))
     if scale is None:
@@ -268,12 +297,12 @@ def simplicial_attn_bwd(q, k, kp, v, vp, out, dout, lse, w1, w2, scale=None, gra
     else:
         _check_inputs((q, *grads), ("q", "dq", "dk", "dkp", "dv", "dvp"))
     workspace = _workspace(workspace, B, N, H, D, w1, w2, dt, q.device)
-    rc = load_library().simplicial_attn_bwd(
+    rc = getattr(load_library(), entry)(
         _ptr(q), _ptr(k), _ptr(kp), _ptr(v), _ptr(vp), _ptr(out), _ptr(dout), _ptr(lse),
         *(_ptr(g) for g in grads), _ptr(workspace), ctypes.c_size_t(workspace.numel()),
         B, N, H, D, int(w1), int(w2), float(scale), dt, _stream(q.device))
     if rc != 0:
-        raise SimplicialAttnError(rc, "simplicial_attn_bwd")
+        raise SimplicialAttnError(rc, entry)
     return grads
 
 

@@ -54,6 +54,7 @@ Shape make_shape(int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1, int32_t
   s.scale = scale;
   s.dtype = dtype;
   s.Hkv = s.H;
+  s.form = 0;
   return s;
 }
 
@@ -246,6 +247,40 @@ int simplicial_attn_bwd(const void* q, const void* k, const void* kp, const void
   if (r != SA_OK) return r;
   return run_stage(s, path, BwdStage::Key, q, k, kp, v, vp, dout, lse, dk, dv, nullptr, workspace,
                    st);
+}
+
+int simplicial_attn_det_fwd(const void* q, const void* k, const void* kp, const void* v,
+                            const void* vp, void* out, float* lse, int64_t B, int64_t N, int64_t H,
+                            int64_t D, int32_t w1, int32_t w2, float scale, int32_t dtype,
+                            void* stream) {
+  if (check_ptrs({q, k, kp, v, vp, out, lse}) != SA_OK) return SA_ERR_INVALID;
+  if (!isfinite(scale)) return SA_ERR_INVALID;
+  const int rc = check_sizes(B, N, H, D, w1, w2, dtype);
+  if (rc != SA_OK) return rc;
+  Shape s = make_shape(B, N, H, D, w1, w2, scale, dtype);
+  s.form = 1;
+  return to_status(sa::generic_fwd(s, q, k, kp, v, vp, out, lse, static_cast<hipStream_t>(stream)));
+}
+
+int simplicial_attn_det_bwd(const void* q, const void* k, const void* kp, const void* v,
+                            const void* vp, const void* out, const void* dout, const float* lse,
+                            void* dq, void* dk, void* dkp, void* dv, void* dvp, void* workspace,
+                            size_t workspace_bytes, int64_t B, int64_t N, int64_t H, int64_t D,
+                            int32_t w1, int32_t w2, float scale, int32_t dtype, void* stream) {
+  if (check_ptrs({q, k, kp, v, vp, out, dout, lse, dq, dk, dkp, dv, dvp, workspace}) != SA_OK)
+    return SA_ERR_INVALID;
+  const int rc = check_bwd(B, N, H, D, w1, w2, scale, dtype, workspace_bytes);
+  if (rc != SA_OK) return rc;
+  Shape s = make_shape(B, N, H, D, w1, w2, scale, dtype);
+  s.form = 1;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  int r = run_delta(s, Path::Generic, out, dout, workspace, st);
+  if (r != SA_OK) return r;
+  r = run_stage(s, Path::Generic, BwdStage::Query, q, k, kp, v, vp, dout, lse, dq, dkp, dvp,
+                workspace, st);
+  if (r != SA_OK) return r;
+  return run_stage(s, Path::Generic, BwdStage::Key, q, k, kp, v, vp, dout, lse, dk, dv, nullptr,
+                   workspace, st);
 }
 
 size_t simplicial_attn_bwd_gqa_workspace_size(int64_t B, int64_t N, int64_t H, int64_t Hkv,

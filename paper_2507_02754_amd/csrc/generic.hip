@@ -119,8 +119,51 @@ __device__ __forceinline__ float tri(const float* a, const T* x, const T* y) {
   return s;
 }
 
-// ---------------------------------------------------------------- forward ---
+// Determinant logits (Section 5, Eq. (logits)): sum over the 3-component
+// chunks c of det([a_c; x_c; y_c]) = a_c . (x_c cross y_c); the D mod 3
+// trailing components take no part.
 template <typename T, int D>
+__device__ __forceinline__ float tri_det(const float* a, const T* x, const T* y) {
+  float s = 0.f;
+  for (int c = 0; c + 2 < D; c += 3) {
+    const float x0 = ld(x + c), x1 = ld(x + c + 1), x2 = ld(x + c + 2);
+    const float y0 = ld(y + c), y1 = ld(y + c + 1), y2 = ld(y + c + 2);
+    s += a[c] * (x1 * y2 - x2 * y1) + a[c + 1] * (x2 * y0 - x0 * y2) + a[c + 2] * (x0 * y1 - x1 * y0);
+  }
+  return s;
+}
+
+// Logit of form FORM (0: trilinear, Eq. (3d-attention); 1: determinant) with
+// operands in the order (a, x, y) of the form.
+template <typename T, int D, int FORM>
+__device__ __forceinline__ float logit3(const float* a, const T* x, const T* y) {
+  if constexpr (FORM == 0)
+    return tri<T, D>(a, x, y);
+  else
+    return tri_det<T, D>(a, x, y);
+}
+
+// acc += w * dA/da for A = form(a, x, y): x o y (trilinear) or, per chunk,
+// x cross y (determinant; trailing components get nothing).
+template <typename T, int D, int FORM>
+__device__ __forceinline__ void add_partial(float (&acc)[D], float w, const T* x, const T* y) {
+  if constexpr (FORM == 0) {
+#pragma unroll
+    for (int d = 0; d < D; ++d) acc[d] += w * ld(x + d) * ld(y + d);
+  } else {
+#pragma unroll
+    for (int c = 0; c + 2 < D; c += 3) {
+      const float x0 = ld(x + c), x1 = ld(x + c + 1), x2 = ld(x + c + 2);
+      const float y0 = ld(y + c), y1 = ld(y + c + 1), y2 = ld(y + c + 2);
+      acc[c] += w * (x1 * y2 - x2 * y1);
+      acc[c + 1] += w * (x2 * y0 - x0 * y2);
+      acc[c + 2] += w * (x0 * y1 - x1 * y0);
+    }
+  }
+}
+
+// ---------------------------------------------------------------- forward ---
+template <typename T, int D, int FORM>
 __global__ __launch_bounds__(kThreads) void fwd_kernel(Shape s, const T* __restrict__ q,
                                                        const T* __restrict__ k,
                                                        const T* __restrict__ kp,
@@ -145,7 +188,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(Shape s, const T* __restr
   float m = -INFINITY;
   for (int p = threadIdx.x; p < np; p += kThreads) {
     const int j = j0 + p / nk, kk = k0 + p % nk;
-    m = fmaxf(m, tri<T, D>(qs, k + kvr.at(j), kp + kvr.at(kk)));
+    m = fmaxf(m, logit3<T, D, FORM>(qs, k + kvr.at(j), kp + kvr.at(kk)));
   }
   m = block_max(m, sred);
 
@@ -155,7 +198,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(Shape s, const T* __restr
   for (int d = 0; d < D; ++d) acc[d] = 0.f;
   for (int p = threadIdx.x; p < np; p += kThreads) {
     const int j = j0 + p / nk, kk = k0 + p % nk;
-    const float e = expf(tri<T, D>(qs, k + kvr.at(j), kp + kvr.at(kk)) - m);
+    const float e = expf(logit3<T, D, FORM>(qs, k + kvr.at(j), kp + kvr.at(kk)) - m);
     l += e;
     const T* vj = v + kvr.at(j);
     const T* vk = vp + kvr.at(kk);
@@ -184,7 +227,7 @@ __global__ void delta_kernel(Shape s, const T* __restrict__ out, const T* __rest
 }
 
 // --------------------------------------------------------------------- dQ ---
-template <typename T, int D>
+template <typename T, int D, int FORM>
 __global__ __launch_bounds__(kThreads) void dq_kernel(Shape s, const T* __restrict__ q,
                                                       const T* __restrict__ k,
                                                       const T* __restrict__ kp,
@@ -219,11 +262,10 @@ __global__ __launch_bounds__(kThreads) void dq_kernel(Shape s, const T* __restri
     const int j = j0 + p / nk, kk = k0 + p % nk;
     const T* kj = k + rows.at(j);
     const T* kk_ = kp + rows.at(kk);
-    const float pr = expf(tri<T, D>(qs, kj, kk_) - lse_i);
+    const float pr = expf(logit3<T, D, FORM>(qs, kj, kk_) - lse_i);
     const float dp = tri<T, D>(ds_, v + rows.at(j), vp + rows.at(kk));
     const float dsv = pr * (dp - delta_i);
-#pragma unroll
-    for (int d = 0; d < D; ++d) acc[d] += dsv * ld(kj + d) * ld(kk_ + d);
+    add_partial<T, D, FORM>(acc, dsv, kj, kk_);
   }
   const float g = block_sum_vec<D>(acc, red);
   if (threadIdx.x < D) st(dq + rows.at(i) + threadIdx.x, g * s.scale);
@@ -233,8 +275,10 @@ __global__ __launch_bounds__(kThreads) void dq_kernel(Shape s, const T* __restri
 // One workgroup per key row r of the K/V side (SIDE 0: window w1, partner
 // window w2) or of the K'/V' side (SIDE 1: window w2, partner window w1). The
 // pairs touching r are (i, o) with i in [r, r + w_self) and o in (i - w_other, i].
-// MODE 0 produces the key gradient, MODE 1 the value gradient.
-template <typename T, int D, int SIDE, int MODE>
+// MODE 0 produces the key gradient, MODE 1 the value gradient. For the
+// determinant form (FORM 1) the operand order follows the cyclic identities
+// q . (k x k') = k . (k' x q) = k' . (q x k).
+template <typename T, int D, int SIDE, int MODE, int FORM>
 __global__ __launch_bounds__(kThreads) void keyside_kernel(
     Shape s, const T* __restrict__ q, const T* __restrict__ kself, const T* __restrict__ kother,
     const T* __restrict__ vself, const T* __restrict__ vother, const T* __restrict__ dout,
@@ -268,12 +312,16 @@ __global__ __launch_bounds__(kThreads) void keyside_kernel(
     const T* ko = kother + rows.at(o);
     const T* doi = dout + rows.at(i);
     const T* vo = vother + rows.at(o);
-    const float pr = expf(tri<T, D>(kr, qi, ko) - lse[stat + i]);
+    const float a = FORM == 0 || SIDE == 1 ? logit3<T, D, FORM>(kr, qi, ko)
+                                           : logit3<T, D, FORM>(kr, ko, qi);
+    const float pr = expf(a - lse[stat + i]);
     if (MODE == 0) {
       const float dp = tri<T, D>(vr, doi, vo);
       const float dsv = pr * (dp - delta[stat + i]);
-#pragma unroll
-      for (int d = 0; d < D; ++d) acc[d] += dsv * ld(qi + d) * ld(ko + d);
+      if (FORM == 0 || SIDE == 1)
+        add_partial<T, D, FORM>(acc, dsv, qi, ko);
+      else
+        add_partial<T, D, FORM>(acc, dsv, ko, qi);
     } else {
 #pragma unroll
       for (int d = 0; d < D; ++d) acc[d] += pr * ld(doi + d) * ld(vo + d);
@@ -283,14 +331,42 @@ __global__ __launch_bounds__(kThreads) void keyside_kernel(
   if (threadIdx.x < D) st(grad + rows.at(r) + threadIdx.x, MODE == 0 ? g * s.scale : g);
 }
 
-template <typename T, int D>
-hipError_t fwd_t(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
+template <typename T, int D, int FORM>
+hipError_t fwd_f(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
                  const void* vp, void* out, float* lse, hipStream_t st) {
   const unsigned grid = static_cast<unsigned>(s.N) * s.B * s.H;
-  hipLaunchKernelGGL((fwd_kernel<T, D>), dim3(grid), dim3(kThreads), 0, st, s,
+  hipLaunchKernelGGL((fwd_kernel<T, D, FORM>), dim3(grid), dim3(kThreads), 0, st, s,
                      static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(kp),
                      static_cast<const T*>(v), static_cast<const T*>(vp), static_cast<T*>(out),
                      lse);
+  return hipGetLastError();
+}
+
+template <typename T, int D>
+hipError_t fwd_t(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
+                 const void* vp, void* out, float* lse, hipStream_t st) {
+  return s.form == 0 ? fwd_f<T, D, 0>(s, q, k, kp, v, vp, out, lse, st)
+                     : fwd_f<T, D, 1>(s, q, k, kp, v, vp, out, lse, st);
+}
+
+template <typename T, int D, int FORM>
+hipError_t bwd_stage_f(const Shape& s, BwdStage stage, const T* q, const T* k, const T* kp,
+                       const T* v, const T* vp, const T* dout, const float* lse,
+                       const float* delta, void* g0, void* g1, void* g2, hipStream_t st) {
+  const unsigned grid = static_cast<unsigned>(s.N) * s.B * s.H;
+  if (stage == BwdStage::Query) {
+    hipLaunchKernelGGL((dq_kernel<T, D, FORM>), dim3(grid), dim3(kThreads), 0, st, s, q, k, kp, v,
+                       vp, dout, lse, delta, static_cast<T*>(g0));
+    hipLaunchKernelGGL((keyside_kernel<T, D, 1, 0, FORM>), dim3(grid), dim3(kThreads), 0, st, s, q,
+                       kp, k, vp, v, dout, lse, delta, static_cast<T*>(g1));
+    hipLaunchKernelGGL((keyside_kernel<T, D, 1, 1, FORM>), dim3(grid), dim3(kThreads), 0, st, s, q,
+                       kp, k, vp, v, dout, lse, delta, static_cast<T*>(g2));
+  } else {
+    hipLaunchKernelGGL((keyside_kernel<T, D, 0, 0, FORM>), dim3(grid), dim3(kThreads), 0, st, s, q,
+                       k, kp, v, vp, dout, lse, delta, static_cast<T*>(g0));
+    hipLaunchKernelGGL((keyside_kernel<T, D, 0, 1, FORM>), dim3(grid), dim3(kThreads), 0, st, s, q,
+                       k, kp, v, vp, dout, lse, delta, static_cast<T*>(g1));
+  }
   return hipGetLastError();
 }
 
@@ -304,21 +380,9 @@ hipError_t bwd_stage_t(const Shape& s, BwdStage stage, const void* q_, const voi
   const T* v = static_cast<const T*>(v_);
   const T* vp = static_cast<const T*>(vp_);
   const T* dout = static_cast<const T*>(dout_);
-  const unsigned grid = static_cast<unsigned>(s.N) * s.B * s.H;
-  if (stage == BwdStage::Query) {
-    hipLaunchKernelGGL((dq_kernel<T, D>), dim3(grid), dim3(kThreads), 0, st, s, q, k, kp, v, vp,
-                       dout, lse, delta, static_cast<T*>(g0));
-    hipLaunchKernelGGL((keyside_kernel<T, D, 1, 0>), dim3(grid), dim3(kThreads), 0, st, s, q, kp, k,
-                       vp, v, dout, lse, delta, static_cast<T*>(g1));
-    hipLaunchKernelGGL((keyside_kernel<T, D, 1, 1>), dim3(grid), dim3(kThreads), 0, st, s, q, kp, k,
-                       vp, v, dout, lse, delta, static_cast<T*>(g2));
-  } else {
-    hipLaunchKernelGGL((keyside_kernel<T, D, 0, 0>), dim3(grid), dim3(kThreads), 0, st, s, q, k, kp,
-                       v, vp, dout, lse, delta, static_cast<T*>(g0));
-    hipLaunchKernelGGL((keyside_kernel<T, D, 0, 1>), dim3(grid), dim3(kThreads), 0, st, s, q, k, kp,
-                       v, vp, dout, lse, delta, static_cast<T*>(g1));
-  }
-  return hipGetLastError();
+  return s.form == 0
+             ? bwd_stage_f<T, D, 0>(s, stage, q, k, kp, v, vp, dout, lse, delta, g0, g1, g2, st)
+             : bwd_stage_f<T, D, 1>(s, stage, q, k, kp, v, vp, dout, lse, delta, g0, g1, g2, st);
 }
 
 }  // namespace

@@ -20,6 +20,9 @@ struct Shape {
   // head h / (H / Hkv)). Only the forward kernels and the GQA helpers below
   // read it; the backward kernels run per query head with Hkv == H.
   int Hkv;
+  // Logit form: 0 trilinear (Section 4), 1 sum of 3 x 3 determinants over
+  // 3-component chunks (Section 5; generic path only).
+  int form;
 };
 
 // bf16 is carried as raw 16-bit patterns (uint16_t) in every kernel.

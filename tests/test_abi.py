@@ -47,7 +47,7 @@ def test_header_declares_the_expected_entry_points():
     assert declared_functions() == sorted([
         "simplicial_attn_fwd", "simplicial_attn_fwd_gqa", "simplicial_attn_bwd",
         "simplicial_attn_bwd_workspace_size", "simplicial_attn_bwd_gqa",
-        "simplicial_attn_bwd_gqa_workspace_size",
+        "simplicial_attn_bwd_gqa_workspace_size", "simplicial_attn_det_fwd", "simplicial_attn_det_bwd",
         "simplicial_attn_error_string", "simplicial_attn_abi_version", "simplicial_attn_path_name",
         "simplicial_attn_bwd_preprocess", "simplicial_attn_bwd_query_side",
         "simplicial_attn_bwd_key_side",
@@ -175,6 +175,26 @@ def test_gqa_workspace_size(lib):
         ws = f(b, n, h, hkv, d, w1, w2, dt)
         assert ws >= plain(b, n, h, d, w1, w2, dt) + 8 * b * n * h * d * es
         assert ws <= plain(b, n, h, d, w1, w2, dt) + 8 * (b * n * h * d * es + 255) + 255
+
+
+@only_without_gpu
+def test_determinant_entry_points_reject_invalid_arguments(lib):
+    fd = lambda ptrs=None, B=1, N=64, H=2, D=128, w1=16, w2=8, scale=0.1, dtype=1: \
+        lib.simplicial_attn_det_fwd(*[ctypes.c_void_p(p) for p in (ptrs or [A] * 7)], B, N, H, D, w1,
+                                    w2, ctypes.c_float(scale), dtype, None)
+    bd = lambda ptrs=None, ws=1 << 30, D=128, w1=16: lib.simplicial_attn_det_bwd(
+        *[ctypes.c_void_p(p) for p in (ptrs or [A] * 14)], ctypes.c_size_t(ws), 1, 64, 2, D, w1, 8,
+        ctypes.c_float(0.1), 1, None)
+    for i in range(7):
+        ptrs = [A] * 7
+        ptrs[i] = 0
+        assert fd(ptrs) == 1
+    for i in range(14):
+        ptrs = [A] * 14
+        ptrs[i] = MISALIGNED
+        assert bd(ptrs) == 1
+    assert fd(w1=0) == 1 and fd(scale=float("nan")) == 1 and fd(D=48) == 2 and fd(dtype=3) == 2
+    assert bd(w1=0) == 1 and bd(D=40) == 2 and bd(ws=0) == 3
 
 
 @only_without_gpu

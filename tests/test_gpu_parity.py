@@ -238,6 +238,48 @@ def test_autograd_gqa():
         assert torch.equal(lf.grad, g2), f"{name}: autograd differs from the direct GQA backward"
 
 
+DET = [
+    # (B, H, N, D, w1, w2, dtype): determinant logits (Section 5), plain fp32 kernels
+    (1, 2, 100, 16, 7, 5, "fp32"),      # 5 chunks + 1 unused component
+    (1, 2, 130, 64, 33, 7, "fp32"),     # 21 chunks + 1
+    (2, 1, 77, 32, 20, 32, "bf16"),     # w2 longer than w1
+    (1, 2, 150, 128, 40, 16, "bf16"),   # 42 chunks + 2
+    (1, 1, 40, 16, 1, 1, "fp32"),       # unit windows
+    (1, 1, 1, 64, 8, 8, "fp32"),        # one query
+]
+
+
+@pytest.mark.parametrize("shape", DET, ids=[str(s) for s in DET])
+def test_determinant_form(shape):
+    """simplicial_attn_det_fwd / _bwd against the determinant oracle, every element."""
+    from oracle import determinant_oracle as dor
+    from paper_2507_02754_amd import simplicial_attn_det_bwd, simplicial_attn_det_fwd
+
+    b, h, n, d, w1, w2, dt = shape
+    _announce(f"determinant form {shape}")
+    inputs = draw((b, n, h, d), seed=700 + n + d, dtype=torch.float32 if dt == "fp32" else torch.bfloat16)
+    scale = d ** -0.5
+    dev = [x.cuda() for x in inputs]
+    o, lse = simplicial_attn_det_fwd(*dev[:5], w1, w2, scale)
+    grads = simplicial_attn_det_bwd(*dev[:5], o, dev[5], lse, w1, w2, scale)
+    torch.cuda.synchronize()
+    o_ref = np.zeros((b, n, h, d))
+    lse_ref = np.zeros((b, h, n))
+    g_ref = [np.zeros((b, n, h, d)) for _ in range(5)]
+    for bb in range(b):
+        for hh in range(h):
+            arrs = P.head_arrays(inputs, bb, hh)
+            o_ref[bb, :, hh], lse_ref[bb, hh] = dor.forward(*arrs[:5], w1, w2, scale)
+            for t, g_ in enumerate(dor.backward(*arrs, w1, w2, scale)):
+                g_ref[t][bb, :, hh] = g_
+    P.check_forward(P.to64(o), P.to64(lse), o_ref, lse_ref, dt, f"det {shape}")
+    P.check_grads([P.to64(g_) for g_ in grads], g_ref, dt, f"det {shape}")
+    # the D mod 3 trailing components get no Q, K, K' gradient
+    tail = 3 * (d // 3)
+    for g_ in grads[:3]:
+        assert torch.count_nonzero(g_[..., tail:]) == 0
+
+
 def test_gqa_forward_full_size_sampled():
     """16 query heads on 2 K-side heads, N = 8192, w1 = 512, w2 = 32: sampled rows
     of every query head against the oracle."""
