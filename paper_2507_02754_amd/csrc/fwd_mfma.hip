@@ -177,18 +177,12 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
   // 16 l. Rows outside [0, N) are loaded from the clamped row: they are
   // masked (p = 0), and finite data keeps 0 * v finite.
   constexpr int SPW = (T::instrs + kWaves - 1) / kWaves;  // loads per tile per wavefront
-  // When the tile's loads do not divide evenly over the wavefronts (head_dim
-  // 64: 4 loads, 8 wavefronts), the wavefronts from T::instrs % kWaves on issue
-  // SPW - 1 per tile. Every vmcnt wait counts the issuing wavefront's own
-  // loads, so it takes that wavefront's count: a wavefront with no tile loads
-  // waits for all of its staging loads.
-  const bool full_share = T::instrs % kWaves == 0 || wave < T::instrs % kWaves;
+  // Every wavefront issues exactly SPW loads per tile (head_dim 64: 4 loads,
+  // 128: 8, over 4 wavefronts), so each vmcnt wait below, which counts the
+  // issuing wavefront's own loads, holds for every wavefront.
+  static_assert(T::instrs % kWaves == 0, "tile loads must divide evenly over the wavefronts");
   auto wait_tiles = [&](auto NC) __attribute__((always_inline)) {
-    constexpr int n = decltype(NC)::value;  // tiles' loads that may stay in flight
-    if (full_share)
-      wait_vmcnt<n * SPW>();
-    else
-      wait_vmcnt<n * (SPW - 1)>();
+    wait_vmcnt<decltype(NC)::value * SPW>();  // that many tiles' loads may stay in flight
   };
   int lrow[SPW], lcol[SPW];
 #pragma unroll
@@ -434,8 +428,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
   if constexpr (G == 1) {
     // The v' rows (issued in iteration 0) are in LDS for every wavefront
     // once 3 tiles' later loads have been waited for and a barrier passed,
-    // which iterations 1-3 do when the window has at least 7 blocks (a
-    // wavefront without tile loads waits for all of its loads there).
+    // which iterations 1-3 do when the window has at least 7 blocks.
     if (nb < 7) {
       wait_vmcnt<0>();
       lds_barrier_tracked();
