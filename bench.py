@@ -277,8 +277,9 @@ def main():
                          "step_tflops": round((fwd_flops + bwd_flops) / ((gf + gb) * 1e-3) / 1e12, 2)}
         del kv, gkv, gws
     if args.det:
-        # Determinant logits run on the plain fp32 kernels: timed on a 4096-token
-        # sequence (the windows and head shape of the main workload).
+        # Determinant logits (forward on the MFMA kernel, backward on the plain
+        # fp32 kernels): timed on a 4096-token sequence with the windows and
+        # head shape of the main workload.
         db, dh, dn = 1, 16, 4096
         g = torch.Generator(device="cpu").manual_seed(11)
         dq_, dk_, dkp_, dv_, dvp_, ddo = (torch.randn((db, dn, dh, w.D), generator=g)
@@ -312,7 +313,7 @@ def main():
                          "step_ms": round(whole, 3), "fwd_ms": round(t_f.elapsed_time(t_b), 3),
                          "bwd_ms": round(t_b.elapsed_time(t_e), 3),
                          "nominal_tflops": round(16 * dunit / (whole * 1e-3) / 1e12, 2),
-                         "kernels": "generic (plain fp32)"}
+                         "kernels": "forward: MFMA kernel (w2 <= 32); backward: plain fp32 kernels"}
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(w, inputs_cpu, args.cpu_seconds)

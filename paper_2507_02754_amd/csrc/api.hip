@@ -259,7 +259,9 @@ int simplicial_attn_det_fwd(const void* q, const void* k, const void* kp, const 
   if (rc != SA_OK) return rc;
   Shape s = make_shape(B, N, H, D, w1, w2, scale, dtype);
   s.form = 1;
-  return to_status(sa::generic_fwd(s, q, k, kp, v, vp, out, lse, static_cast<hipStream_t>(stream)));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (sa::mfma_fwd_supported(s)) return to_status(sa::mfma_fwd(s, q, k, kp, v, vp, out, lse, st));
+  return to_status(sa::generic_fwd(s, q, k, kp, v, vp, out, lse, st));
 }
 
 int simplicial_attn_det_bwd(const void* q, const void* k, const void* kp, const void* v,

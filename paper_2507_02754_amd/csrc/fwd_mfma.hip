@@ -71,7 +71,9 @@ __device__ __forceinline__ void wait_vmcnt() {
 }
 
 
-template <int D, int G>
+// FORM 0: trilinear logits (Section 4); FORM 1: determinant logits (Section 5,
+// w2 <= 32 only), which differ only in the modulated query formed below.
+template <int D, int G, int FORM>
 __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const uint16_t* __restrict__ q,
                                                                const uint16_t* __restrict__ k,
                                                                const uint16_t* __restrict__ kp,
@@ -299,19 +301,67 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
     const lds_char* krow = to_lds(stg) + rr * 2 * D;
     const lds_char* qrow = to_lds(stg) + rq_ * 2 * D;
     const unsigned keep = rowvalid ? 0xFFFFFFFFu : 0u;
-    u32x4_t qa[NT], ka[NT];
+    if constexpr (FORM == 0) {
+      u32x4_t qa[NT], ka[NT];
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      const int ch = 2 * t + h;
-      ka[t] = lds_ld<u32x4_t>(krow + 16 * (ch ^ (rr % T::CH)));
-      qa[t] = lds_ld<u32x4_t>(qrow + 16 * (ch ^ (rq_ % T::CH)));
+      for (int t = 0; t < NT; ++t) {
+        const int ch = 2 * t + h;
+        ka[t] = lds_ld<u32x4_t>(krow + 16 * (ch ^ (rr % T::CH)));
+        qa[t] = lds_ld<u32x4_t>(qrow + 16 * (ch ^ (rq_ % T::CH)));
+      }
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          qt[t][e] = keep & pack_bf16x2(bf16_lo(qa[t][e]) * bf16_lo(ka[t][e]) * qscale,
+                                        bf16_hi(qa[t][e]) * bf16_hi(ka[t][e]) * qscale);
+    } else {
+      // Determinant logits: per 3-component chunk, det([q; k; k']) =
+      // k . (k' x q), so q~ = (scale log2 e) * (k'_k x q_i) chunk by chunk and
+      // <q~, k_j> is the logit. The lane's fragment t holds components
+      // 8 ch .. 8 ch + 7 (ch = 2t + h); a chunk reaches at most 2 components
+      // into the neighbouring 16-byte slots, read as 4-byte words (clamped at
+      // the row ends, where they are not used). Components past the last whole
+      // chunk (D mod 3 of them) are 0.
+      constexpr int DC = 3 * (D / 3);
+      const int swk = rr % T::CH, swq = rq_ % T::CH;
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        const int ch = 2 * t + h;
+        const int chp = ch > 0 ? ch - 1 : 0, chn = ch < T::CH - 1 ? ch + 1 : ch;
+        const u32x4_t kc = lds_ld<u32x4_t>(krow + 16 * (ch ^ swk));
+        const u32x4_t qc = lds_ld<u32x4_t>(qrow + 16 * (ch ^ swq));
+        const unsigned kw[2] = {lds_ld<unsigned>(krow + 16 * (chp ^ swk) + 12),
+                                lds_ld<unsigned>(krow + 16 * (chn ^ swk))};
+        const unsigned qw[2] = {lds_ld<unsigned>(qrow + 16 * (chp ^ swq) + 12),
+                                lds_ld<unsigned>(qrow + 16 * (chn ^ swq))};
+        // window x = 0 .. 11 holds components 8 ch - 2 .. 8 ch + 9
+        float fk[12], fq[12];
+        fk[0] = bf16_lo(kw[0]), fk[1] = bf16_hi(kw[0]), fk[10] = bf16_lo(kw[1]), fk[11] = bf16_hi(kw[1]);
+        fq[0] = bf16_lo(qw[0]), fq[1] = bf16_hi(qw[0]), fq[10] = bf16_lo(qw[1]), fq[11] = bf16_hi(qw[1]);
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          fk[2 + 2 * w] = bf16_lo(kc[w]), fk[3 + 2 * w] = bf16_hi(kc[w]);
+          fq[2 + 2 * w] = bf16_lo(qc[w]), fq[3 + 2 * w] = bf16_hi(qc[w]);
+        }
+        // component e of the fragment sits at position m of its chunk, which
+        // starts at window index e + 2 - m; m = (8 ch + e) mod 3 = (t + 2h + e) mod 3.
+        auto cross = [&](int e, int m) __attribute__((always_inline)) {
+          const int b = e + 2 - m;
+          return m == 0 ? fk[b + 1] * fq[b + 2] - fk[b + 2] * fq[b + 1]
+               : m == 1 ? fk[b + 2] * fq[b] - fk[b] * fq[b + 2]
+                        : fk[b] * fq[b + 1] - fk[b + 1] * fq[b];
+        };
+        float cr[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float x = h == 0 ? cross(e, (t + e) % 3) : cross(e, (t + 2 + e) % 3);
+          cr[e] = 8 * ch + e < DC ? x * qscale : 0.f;
+        }
+#pragma unroll
+        for (int w = 0; w < 4; ++w) qt[t][w] = keep & pack_bf16x2(cr[2 * w], cr[2 * w + 1]);
+      }
     }
-#pragma unroll
-    for (int t = 0; t < NT; ++t)
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        qt[t][e] = keep & pack_bf16x2(bf16_lo(qa[t][e]) * bf16_lo(ka[t][e]) * qscale,
-                                      bf16_hi(qa[t][e]) * bf16_hi(ka[t][e]) * qscale);
   } else {
     __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wavefront's block loads are in LDS
     lds_barrier();
@@ -516,14 +566,14 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
   }
 }
 
-template <int D, int G>
+template <int D, int G, int FORM = 0>
 hipError_t launch(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
                   const void* vp, void* out, float* lse, hipStream_t st) {
   constexpr int QW = kWaves / G;
   const long tiles = (s.N + QW - 1) / QW;
   const long total = tiles * s.B * s.H;
   const long grid = ((total + 7) / 8) * 8;
-  hipLaunchKernelGGL((fwd_mfma_kernel<D, G>), dim3(static_cast<unsigned>(grid)), dim3(kThreads), 0,
+  hipLaunchKernelGGL((fwd_mfma_kernel<D, G, FORM>), dim3(static_cast<unsigned>(grid)), dim3(kThreads), 0,
                      st, s, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                      static_cast<const uint16_t*>(kp), static_cast<const uint16_t*>(v),
                      static_cast<const uint16_t*>(vp), static_cast<uint16_t*>(out), lse);
@@ -535,12 +585,17 @@ hipError_t launch(const Shape& s, const void* q, const void* k, const void* kp, 
 bool mfma_fwd_supported(const Shape& s) {
   // Per-head byte offsets are 32-bit in the buffer loads.
   const bool fits = static_cast<long long>(s.N) * s.H * s.D * 2 < (1ll << 31);
-  return s.dtype == 1 && (s.D == 64 || s.D == 128) && s.w2 <= 64 && fits;
+  return s.dtype == 1 && (s.D == 64 || s.D == 128) && s.w2 <= (s.form == 1 ? 32 : 64) && fits;
 }
 
 hipError_t mfma_fwd(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
                     const void* vp, void* out, float* lse, hipStream_t st) {
   const int G = s.w2 <= 32 ? 1 : 2;
+  if (s.form == 1) {  // determinant logits: w2 <= 32 only (mfma_fwd_supported)
+    if (G != 1) return hipErrorInvalidValue;
+    return s.D == 128 ? launch<128, 1, 1>(s, q, k, kp, v, vp, out, lse, st)
+                      : launch<64, 1, 1>(s, q, k, kp, v, vp, out, lse, st);
+  }
   if (s.D == 128) return G == 1 ? launch<128, 1>(s, q, k, kp, v, vp, out, lse, st)
                                 : launch<128, 2>(s, q, k, kp, v, vp, out, lse, st);
   if (s.D == 64) return G == 1 ? launch<64, 1>(s, q, k, kp, v, vp, out, lse, st)

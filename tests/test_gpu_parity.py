@@ -243,7 +243,10 @@ DET = [
     (1, 2, 100, 16, 7, 5, "fp32"),      # 5 chunks + 1 unused component
     (1, 2, 130, 64, 33, 7, "fp32"),     # 21 chunks + 1
     (2, 1, 77, 32, 20, 32, "bf16"),     # w2 longer than w1
-    (1, 2, 150, 128, 40, 16, "bf16"),   # 42 chunks + 2
+    (1, 2, 150, 128, 40, 16, "bf16"),   # 42 chunks + 2 (MFMA forward)
+    (1, 2, 300, 128, 64, 32, "bf16"),   # MFMA forward, several tiles
+    (1, 3, 257, 64, 100, 17, "bf16"),   # MFMA forward, head_dim 64 (21 chunks + 1)
+    (2, 1, 100, 64, 7, 5, "bf16"),      # MFMA forward, short windows
     (1, 1, 40, 16, 1, 1, "fp32"),       # unit windows
     (1, 1, 1, 64, 8, 8, "fp32"),        # one query
 ]
@@ -278,6 +281,32 @@ def test_determinant_form(shape):
     tail = 3 * (d // 3)
     for g_ in grads[:3]:
         assert torch.count_nonzero(g_[..., tail:]) == 0
+
+
+def test_determinant_forward_full_size_sampled():
+    """Determinant forward on the MFMA kernel at B=1, H=4, N=8192, D=128,
+    w1=512, w2=32: sampled rows of every head against the determinant oracle."""
+    from oracle import determinant_oracle as dor
+    from paper_2507_02754_amd import simplicial_attn_det_fwd
+
+    b, h, n, d, w1, w2 = 1, 4, 8192, 128, 512, 32
+    _announce(f"determinant forward full size B={b} H={h} N={n} D={d} w1={w1} w2={w2}")
+    inputs = draw((b, n, h, d), seed=808, dtype=torch.bfloat16)
+    scale = d ** -0.5
+    o, lse = simplicial_attn_det_fwd(*(x.cuda() for x in inputs[:5]), w1, w2, scale)
+    torch.cuda.synchronize()
+    rows = P.sample_rows(n, w1, w2, extra=6, seed=9)
+    o64, l64 = P.to64(o), P.to64(lse)
+    got_o, got_l, ref_o, ref_l = [], [], [], []
+    for hh in range(h):
+        arrs = P.head_arrays(inputs, 0, hh)
+        ro, rl = dor.forward(*arrs[:5], w1, w2, scale, queries=rows)
+        got_o.append(o64[0, rows, hh])
+        got_l.append(l64[0, hh, rows])
+        ref_o.append(ro[rows])
+        ref_l.append(rl[rows])
+    P.check_forward(np.concatenate(got_o), np.concatenate(got_l), np.concatenate(ref_o),
+                    np.concatenate(ref_l), "bf16", "determinant full size")
 
 
 def test_gqa_forward_full_size_sampled():
@@ -392,6 +421,26 @@ def test_backward_is_deterministic():
     for r in runs[1:]:
         for a, c in zip(runs[0], r):
             assert torch.equal(a.view(torch.int16), c.view(torch.int16))
+
+
+@pytest.mark.parametrize("d,w1", [(128, 230), (64, 200)])
+def test_forward_is_deterministic(d, w1):
+    """The forward has no atomics and a fixed order of operations: repeated
+    calls on the same inputs (3 heads of 4096 queries, w2 = 32) must agree
+    bit for bit."""
+    b, h, n, w2 = 1, 3, 4096, 32
+    _announce(f"forward determinism N={n} H={h} D={d} w1={w1} w2={w2}")
+    inputs = [x.cuda() for x in draw((b, n, h, d), seed=11 + d + w1 + w2)[:5]]
+    o0, l0 = simplicial_attn_fwd(*inputs, w1, w2)
+    torch.cuda.synchronize()
+    o0, l0 = o0.clone(), l0.clone()
+    differing = 0
+    for _ in range(8):
+        o, lse = simplicial_attn_fwd(*inputs, w1, w2)
+        torch.cuda.synchronize()
+        if not (torch.equal(o.view(torch.int16), o0.view(torch.int16)) and torch.equal(lse, l0)):
+            differing += 1
+    assert differing == 0, f"{differing} of 8 repeated forwards differ from the first"
 
 
 @pytest.mark.parametrize("shape", [(1, 2, 700, 128, 256, 32), (1, 1, 300, 64, 40, 64),
