@@ -98,12 +98,12 @@ def test_running_max_raised_mid_window(d):
 
 @pytest.mark.parametrize("d,w1,w2", [(64, 200, 32), (128, 230, 32), (64, 300, 32), (128, 230, 17)])
 def test_forward_tile_runs(d, w1, w2):
-    """Many tiles per workgroup of the streaming forward (two workgroups per
-    CU, each walking a run of 4-query tiles with its K/V rings running on from
-    one tile into the next): 3 heads of 4096 queries, so one XCD's run of tiles
-    crosses a head boundary; w1 = 200, 230, 300 give 7, 8 and 10 key blocks
-    per tile (tile start stages cycling by 3, 0 and 2 mod 4). Sampled rows of
-    every head, the first rows of each head included."""
+    """The forward's XCD-aware tile order over 3 heads of 4096 queries (one
+    XCD's contiguous run of 4-query tiles crosses a head boundary), with
+    w1 = 200, 230, 300 giving 7, 8 and 10 key blocks per tile: the v' rows
+    issued in iteration 0 are covered by the ring waits (>= 7 blocks) and the
+    K/V ring stages wrap at different points. Sampled rows of every head, the
+    first rows of each head included."""
     b, h, n = 1, 3, 4096
     _announce(f"forward tile runs N={n} H={h} D={d} w1={w1} w2={w2} "
               f"fwd={simplicial_attn_path_name(0, b, n, h, d, w1, w2, 1)}")
