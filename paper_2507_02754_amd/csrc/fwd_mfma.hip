@@ -49,6 +49,7 @@
 // not computed otherwise. The row sum l adds the bf16-rounded p that the P V
 // product consumes, so O is a convex combination of V rows.
 // Rows with k < 0 or k <= i - w2 get q~ = 0 and weight 0 in the merge.
+#include "fwd_schedule.h"
 #include "mfma_common.h"
 
 namespace sa {
@@ -56,7 +57,7 @@ namespace {
 
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
-constexpr int kStages = 4;
+constexpr int kStages = fwd_schedule::kStages;
 constexpr float kPmax = 65536.0f;  // largest block row sum of p before the running max is raised
 
 template <int X>
@@ -384,13 +385,20 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
     constexpr int cur = S & 1, nxt = cur ^ 1;
     // K(blk + 2) (loaded in iteration blk - 2) and V(blk) (iteration
     // blk - 3) must be in LDS for every wavefront: wait until at most the
-    // 3 tiles' loads issued after K(blk + 2) are in flight, then synchronise.
-    wait_tiles(IC<3>{});
+    // loads this wavefront issued after them are in flight (3 tiles in
+    // steady state, fewer in the last three iterations, where the ring
+    // issues no more loads), then synchronise.
+    switch (fwd_schedule::inflight_tiles(blk, nb)) {
+      case 3: wait_tiles(IC<3>{}); break;
+      case 2: wait_tiles(IC<2>{}); break;
+      case 1: wait_tiles(IC<1>{}); break;
+      default: wait_tiles(IC<0>{}); break;
+    }
     lds_barrier_tracked();
     // K(blk + 4) replaces K(blk), read in iteration blk - 2; V(blk + 3)
     // replaces V(blk - 1), read in iteration blk - 1.
-    if (blk + 4 < nb) load_tile(rk, kst(IC<S>{}), blk + 4);
-    if (blk + 3 < nb) load_tile(rv, vst(IC<(S + 3) % kStages>{}), blk + 3);
+    if (fwd_schedule::loads_k(blk, nb)) load_tile(rk, kst(IC<S>{}), blk + 4);
+    if (fwd_schedule::loads_v(blk, nb)) load_tile(rv, vst(IC<(S + 3) % kStages>{}), blk + 3);
     if constexpr (G == 1 && S == 0) {
       // v' rows into the staging tile, whose q and k' rows every wavefront
       // has read before the barrier above.
@@ -477,9 +485,9 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
   u32x2_t vpr[4 * NDT];
   if constexpr (G == 1) {
     // The v' rows (issued in iteration 0) are in LDS for every wavefront
-    // once 3 tiles' later loads have been waited for and a barrier passed,
-    // which iterations 1-3 do when the window has at least 7 blocks.
-    if (nb < 7) {
+    // once the last iteration (n = nb - 1 >= 1) has waited for every load
+    // and passed its barrier; a one-block window waits here.
+    if (fwd_schedule::epilogue_waits(nb)) {
       wait_vmcnt<0>();
       lds_barrier_tracked();
     }
