@@ -15,14 +15,11 @@ Tolerances (the bar each parity test asserts), with the arithmetic behind them:
   LSE (fp32 output): |LSE - ref| <= 2e-2; the bf16 rounding of the modulated
   query perturbs each logit by ~2^-9 |logit|.
 * bf16 data, backward: per gradient max |g - ref| / max |ref| <= 5e-2 and
-  normwise <= 2e-2 (P, dS and the modulated operands are rounded to bf16
-  before each matrix product, and the result is rounded to bf16).
-  Delta_i = <dO_i, O_i> is formed from the stored bf16 output, so a gradient
-  that vanishes exactly (dQ, dK, dK' with unit windows or unit values) comes
-  out at ~2^-9 of the call's gradient scale instead of 0. A gradient whose
-  reference is that small (max |ref| below 10% of the largest gradient of the
-  call) is therefore measured against 10% of the largest gradient instead of
-  its own maximum, and its normwise error is not asserted.
+  normwise <= 2e-2, each gradient on its own scale (P, dS and the modulated
+  operands are rounded to bf16 before each matrix product, and the result is
+  rounded to bf16). Gradients that vanish in exact arithmetic (dQ, dK, dK' with
+  unit windows or unit values) have no scale of their own; the tests of those
+  identities bound them explicitly instead of calling check_grads on them.
 """
 
 import json
@@ -117,21 +114,33 @@ def check_grads(grads, refs, dtype, label="", rows=None):
                 continue
             g, r = g[sel], r[sel]
         pairs.append((name, np.asarray(g, np.float64), np.asarray(r, np.float64)))
-    gscale = max(float(np.max(np.abs(r))) if r.size else 0.0 for _, _, r in pairs)
     for name, g, r in pairs:
         e = err(g, r)
-        mref = float(np.max(np.abs(r))) if r.size else 0.0
-        degenerate = dtype == "bf16" and mref < 0.1 * gscale
-        if degenerate:
-            e["max_rel"] = e["max_abs"] / (0.1 * gscale)
-            e["degenerate"] = True
         out[name] = e
         assert e["finite"], f"{label}: {name} non-finite"
         assert e["max_rel"] <= t["g_maxrel"], f"{label}: {name} {e}"
-        if not degenerate:
-            assert e["norm_rel"] <= t["g_norm"], f"{label}: {name} {e}"
+        assert e["norm_rel"] <= t["g_norm"], f"{label}: {name} {e}"
     report("bwd", label, out)
     return out
+
+
+def check_single_pair_grads(dgrads, arrs, scale, label=""):
+    """dQ, dK, dK' when every query sees exactly one (j, k) pair (unit windows
+    or a one-token sequence): then P = 1 and dS = dP - Delta = 0 in exact
+    arithmetic, so the three gradients vanish. On the GPU dP is a product of
+    bf16-rounded operands and Delta comes from the bf16 output, so each is off
+    by at most 2^-9 * sum_d |dO_id v_id v'_id|; with scale * (x o y) on top this
+    bounds the gradients (a factor 2 of margin). dgrads: dq, dk, dkp as fp64
+    [.., N, H, D] arrays; arrs: q, k, kp, v, vp, do in the same layout."""
+    q, k, kp, v, vp, do = arrs
+    eps = 2.0 ** -8 * np.abs(do * v * vp).sum(axis=-1, keepdims=True)
+    out = {}
+    for name, g, (x, y) in zip(("dq", "dk", "dkp"), dgrads, [(k, kp), (q, kp), (q, k)]):
+        bound = 2 * scale * eps * np.abs(x * y) + 1e-6
+        excess = float(np.max(np.abs(g) - bound))
+        out[name] = {"max_abs": float(np.max(np.abs(g))), "excess_over_bound": excess}
+        assert np.all(np.abs(g) <= bound), f"{label}: {name} exceeds the rounding bound by {excess}"
+    report("bwd_single_pair", label, out)
 
 
 def full_oracle(inputs, w1, w2, scale, backward=True):
