@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define SIMPLICIAL_ATTN_ABI_VERSION 2
+#define SIMPLICIAL_ATTN_ABI_VERSION 3
 
 #define SA_DTYPE_F32 0
 #define SA_DTYPE_BF16 1
@@ -52,6 +52,10 @@ extern "C" {
 #define SA_ERR_UNSUPPORTED 2 /* head_dim or dtype this build does not implement */
 #define SA_ERR_WORKSPACE 3   /* workspace smaller than simplicial_attn_bwd_workspace_size() */
 #define SA_ERR_HIP 4         /* HIP runtime reported an error when launching */
+#define SA_ERR_SCRATCH 5     /* simplicial_attn_bwd_noalloc: sizes need more than its fixed scratch */
+
+/* Bytes of the fixed device scratch array of simplicial_attn_bwd_noalloc (64 MiB per GPU). */
+#define SA_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
 
 /*
  * Forward pass (Section 4 equations over Section 6's windows).
@@ -110,6 +114,36 @@ int simplicial_attn_bwd(const void* q, const void* k, const void* kp, const void
                         void* dkp, void* dv, void* dvp, void* workspace, size_t workspace_bytes,
                         int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1, int32_t w2,
                         float scale, int32_t dtype, void* stream);
+
+/*
+ * The backward without any allocation, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc). Same operation, arguments, results and errors as
+ * simplicial_attn_bwd, except that there is no workspace argument: the
+ * workspace is a file-scope device array of SA_NOALLOC_SCRATCH_BYTES that each
+ * GPU holds from the first call on that device (or the library's first use of
+ * it) until the process ends. The call makes no hipMalloc/hipFree and calls no
+ * allocating library routine; its first call on a device looks up that
+ * device's copy of the array (hipGetSymbolAddress, with the device current).
+ *   Limit  the per-query Delta (4 bytes per query and head) plus the partial
+ *          sums of the backward's deterministic reduction must fit the array.
+ *          When the workspace simplicial_attn_bwd_workspace_size() reports
+ *          fits, the kernels, their work split and the result are exactly
+ *          those of simplicial_attn_bwd (bitwise). Otherwise the query-side
+ *          kernel walks longer query chunks so that fewer partial sums are
+ *          kept (same gradients up to the order of fp32 additions at chunk
+ *          boundaries, still deterministic); sizes for which even that does
+ *          not fit return SA_ERR_SCRATCH, before any HIP call.
+ *   Races  every call on one GPU uses that GPU's one array, and every call
+ *          overwrites what it reads from it (contents on entry are ignored),
+ *          so calls that overlap in time on one GPU (other streams, other
+ *          host threads) race; calls ordered on one stream do not.
+ */
+int simplicial_attn_bwd_noalloc(const void* q, const void* k, const void* kp, const void* v,
+                                const void* vp, const void* out, const void* dout, const float* lse,
+                                void* dq, void* dk, void* dkp, void* dv, void* dvp, int64_t B,
+                                int64_t N, int64_t H, int64_t D, int32_t w1, int32_t w2, float scale,
+                                int32_t dtype, void* stream);
 
 /*
  * Forward and backward with the determinant logits of Section 5, Eq. (logits)

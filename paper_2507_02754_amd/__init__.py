@@ -17,6 +17,7 @@ from .binding import (  # noqa: F401
     simplicial_attn_bwd,
     simplicial_attn_bwd_gqa,
     simplicial_attn_bwd_gqa_workspace_size,
+    simplicial_attn_bwd_noalloc,
     simplicial_attn_det_bwd,
     simplicial_attn_det_fwd,
     simplicial_attn_bwd_key_side,

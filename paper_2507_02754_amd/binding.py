@@ -20,6 +20,7 @@ __all__ = [
     "simplicial_attn_fwd_gqa",
     "simplicial_attn_bwd",
     "simplicial_attn_bwd_gqa",
+    "simplicial_attn_bwd_noalloc",
     "simplicial_attn_det_fwd",
     "simplicial_attn_det_bwd",
     "simplicial_attn_bwd_gqa_workspace_size",
@@ -65,6 +66,8 @@ def load_library():
     lib.simplicial_attn_fwd_gqa.restype = ctypes.c_int
     lib.simplicial_attn_bwd.argtypes = [vp] * 14 + [ctypes.c_size_t] + [i64] * 4 + [i32, i32, f32, i32, vp]
     lib.simplicial_attn_bwd.restype = ctypes.c_int
+    lib.simplicial_attn_bwd_noalloc.argtypes = [vp] * 13 + [i64] * 4 + [i32, i32, f32, i32, vp]
+    lib.simplicial_attn_bwd_noalloc.restype = ctypes.c_int
     lib.simplicial_attn_det_fwd.argtypes = lib.simplicial_attn_fwd.argtypes
     lib.simplicial_attn_det_fwd.restype = ctypes.c_int
     lib.simplicial_attn_det_bwd.argtypes = lib.simplicial_attn_bwd.argtypes
@@ -274,6 +277,31 @@ def simplicial_attn_bwd(q, k, kp, v, vp, out, dout, lse, w1, w2, scale=None, gra
     """(dQ, dK, dK', dV, dV') = backward(...); `out`/`lse` come from the forward."""
     return _bwd("simplicial_attn_bwd", q, k, kp, v, vp, out, dout, lse, w1, w2, scale, grads,
                 workspace)
+
+
+def simplicial_attn_bwd_noalloc(q, k, kp, v, vp, out, dout, lse, w1, w2, scale=None, grads=None):
+    """(dQ, dK, dK', dV, dV') through the allocation-free entry point, whose
+    workspace is the library's fixed device scratch array. Pass preallocated
+    `grads` to keep the whole call free of allocations (otherwise torch
+    allocates them here, before the entry point is called)."""
+    (B, N, H, D), dt = _check_inputs((q, k, kp, v, vp, out, dout),
+                                     ("q", "k", "kp", "v", "vp", "out", "dout"))
+    if scale is None:
+        scale = D ** -0.5
+    if lse.shape != (B, H, N) or lse.dtype != torch.float32 or not lse.is_contiguous() \
+            or lse.device != q.device:
+        raise ValueError("lse must be a contiguous float32 [B, H, N] tensor on the inputs' device")
+    if grads is None:
+        grads = tuple(torch.empty_like(q) for _ in range(5))
+    else:
+        _check_inputs((q, *grads), ("q", "dq", "dk", "dkp", "dv", "dvp"))
+    rc = load_library().simplicial_attn_bwd_noalloc(
+        _ptr(q), _ptr(k), _ptr(kp), _ptr(v), _ptr(vp), _ptr(out), _ptr(dout), _ptr(lse),
+        *(_ptr(g) for g in grads), B, N, H, D, int(w1), int(w2), float(scale), dt,
+        _stream(q.device))
+    if rc != 0:
+        raise SimplicialAttnError(rc, "simplicial_attn_bwd_noalloc")
+    return grads
 
 
 def simplicial_attn_det_bwd(q, k, kp, v, vp, out, dout, lse, w1, w2, scale=None, grads=None,

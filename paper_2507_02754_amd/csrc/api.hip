@@ -7,6 +7,7 @@
 #include <math.h>
 
 #include <initializer_list>
+#include <mutex>
 
 #include "sa_internal.h"
 
@@ -55,6 +56,7 @@ Shape make_shape(int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1, int32_t
   s.dtype = dtype;
   s.Hkv = s.H;
   s.form = 0;
+  s.ws_cap = 0;
   return s;
 }
 
@@ -146,6 +148,41 @@ int run_stage(const Shape& s, Path path, BwdStage stage, const void* q, const vo
                                          static_cast<const float*>(workspace), g0, g1, g2, st));
 }
 
+// ---- device scratch of the allocation-free backward ----
+//
+// The workspace of simplicial_attn_bwd_noalloc is this file-scope device
+// array: each GPU the library runs on holds its own copy, at its own address,
+// until the process ends. In host code the name `scratch` is only a host-side
+// stand-in for the symbol, so it is never passed to a kernel or a copy: the
+// device address comes from hipGetSymbolAddress, taken once per device with
+// that device current and kept per device.
+constexpr size_t kScratchBytes = SA_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+
+// Device address of the current device's scratch array (SA_OK), or SA_ERR_HIP.
+int current_device_scratch(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return SA_ERR_HIP;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) {
+      (void)hipGetLastError();
+      return SA_ERR_HIP;
+    }
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return SA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -159,6 +196,9 @@ const char* simplicial_attn_error_string(int code) {
     case SA_ERR_UNSUPPORTED: return "unsupported head_dim or dtype";
     case SA_ERR_WORKSPACE: return "workspace smaller than simplicial_attn_bwd_workspace_size()";
     case SA_ERR_HIP: return "HIP runtime error while launching kernels";
+    case SA_ERR_SCRATCH:
+      return "problem needs more device scratch than the allocation-free backward's fixed "
+             "SA_NOALLOC_SCRATCH_BYTES";
     default: return "unknown status";
   }
 }
@@ -247,6 +287,33 @@ int simplicial_attn_bwd(const void* q, const void* k, const void* kp, const void
   if (r != SA_OK) return r;
   return run_stage(s, path, BwdStage::Key, q, k, kp, v, vp, dout, lse, dk, dv, nullptr, workspace,
                    st);
+}
+
+int simplicial_attn_bwd_noalloc(const void* q, const void* k, const void* kp, const void* v,
+                                const void* vp, const void* out, const void* dout, const float* lse,
+                                void* dq, void* dk, void* dkp, void* dv, void* dvp, int64_t B,
+                                int64_t N, int64_t H, int64_t D, int32_t w1, int32_t w2, float scale,
+                                int32_t dtype, void* stream) {
+  if (check_ptrs({q, k, kp, v, vp, out, dout, lse, dq, dk, dkp, dv, dvp}) != SA_OK)
+    return SA_ERR_INVALID;
+  if (!isfinite(scale)) return SA_ERR_INVALID;
+  const int rc = check_sizes(B, N, H, D, w1, w2, dtype);
+  if (rc != SA_OK) return rc;
+  Shape s = make_shape(B, N, H, D, w1, w2, scale, dtype);
+  s.ws_cap = kScratchBytes;
+  const Path path = choose_path(1, B, N, H, D, w1, w2, dtype);
+  const size_t need = path == Path::Mfma ? sa::mfma_bwd_plan(s).bytes
+                                         : workspace_bytes_for(B, N, H, D, w1, w2, dtype);
+  if (need > kScratchBytes) return SA_ERR_SCRATCH;
+  void* ws = nullptr;
+  int r = current_device_scratch(&ws);
+  if (r != SA_OK) return r;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  r = run_delta(s, path, out, dout, ws, st);
+  if (r != SA_OK) return r;
+  r = run_stage(s, path, BwdStage::Query, q, k, kp, v, vp, dout, lse, dq, dkp, dvp, ws, st);
+  if (r != SA_OK) return r;
+  return run_stage(s, path, BwdStage::Key, q, k, kp, v, vp, dout, lse, dk, dv, nullptr, ws, st);
 }
 
 int simplicial_attn_det_fwd(const void* q, const void* k, const void* kp, const void* v,

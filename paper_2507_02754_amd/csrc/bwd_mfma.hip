@@ -37,14 +37,22 @@ BwdPlan mfma_bwd_plan(const Shape& s) {
   long cq = 128;
   while (cq < 1024 && bh * ((s.N + cq - 1) / cq) > 4096) cq *= 2;
   if (cq < p.W2P) cq = p.W2P;
-  p.CQ = static_cast<int>(cq);
-  p.nchunks = static_cast<int>((s.N + cq - 1) / cq);
   const size_t halo_rows = static_cast<size_t>(p.W2P - 1);
-  p.halo_floats = bh * static_cast<size_t>(p.nchunks) * halo_rows * s.D;
   const size_t delta_bytes = ((bh * static_cast<size_t>(s.N) * 4) + 255) & ~size_t(255);
+  auto set_chunk = [&](long c) {
+    p.CQ = static_cast<int>(c);
+    p.nchunks = static_cast<int>((s.N + c - 1) / c);
+    p.halo_floats = bh * static_cast<size_t>(p.nchunks) * halo_rows * s.D;
+    p.bytes = delta_bytes + 4 * p.halo_floats * 4;
+  };
+  set_chunk(cq);
+  // A capped workspace takes longer chunks (one chunk per head at most).
+  while (s.ws_cap > 0 && p.bytes > s.ws_cap && cq < s.N) {
+    cq *= 2;
+    set_chunk(cq);
+  }
   p.delta_off = 0;
   p.halo_off = delta_bytes;  // 4 arrays: head/tail x dk'/dv'
-  p.bytes = delta_bytes + 4 * p.halo_floats * 4;
   return p;
 }
 

@@ -21,8 +21,12 @@ struct Shape {
   // read it; the backward kernels run per query head with Hkv == H.
   int Hkv;
   // Logit form: 0 trilinear (Section 4), 1 sum of 3 x 3 determinants over
-  // 3-component chunks (Section 5; generic path only).
+  // 3-component chunks (Section 5).
   int form;
+  // Largest backward workspace the caller can provide, in bytes (0: no
+  // limit). The MFMA backward plan lengthens its query chunks until its
+  // workspace fits (fewer chunk-boundary partial sums).
+  size_t ws_cap;
 };
 
 // bf16 is carried as raw 16-bit patterns (uint16_t) in every kernel.

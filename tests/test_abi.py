@@ -50,7 +50,7 @@ def test_header_declares_the_expected_entry_points():
         "simplicial_attn_bwd_gqa_workspace_size", "simplicial_attn_det_fwd", "simplicial_attn_det_bwd",
         "simplicial_attn_error_string", "simplicial_attn_abi_version", "simplicial_attn_path_name",
         "simplicial_attn_bwd_preprocess", "simplicial_attn_bwd_query_side",
-        "simplicial_attn_bwd_key_side",
+        "simplicial_attn_bwd_key_side", "simplicial_attn_bwd_noalloc",
     ])
 
 
@@ -69,7 +69,7 @@ def test_abi_version_matches_header(lib):
 
 
 def test_error_strings(lib):
-    for code in range(5):
+    for code in range(6):
         s = binding.simplicial_attn_error_string(code)
         assert s and s != "unknown status"
     assert binding.simplicial_attn_error_string(99) == "unknown status"
