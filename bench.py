@@ -89,7 +89,18 @@ def cpu_baseline(w, inputs, target_s):
         "value": flops / el / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
         "sample": f"fwd+bwd of {done} queries (head 0, queries {start}..{start + done - 1}) "
                   f"of {w.name}; {el:.1f} s; nominal 16*w1*w2*D FLOPs per query",
+        "host_cores": len(os.sched_getaffinity(0)), "cpu_model": cpu_model(),
     }
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def main():
@@ -199,19 +210,32 @@ def main():
     fwd_tf = fwd_flops / (ms["fwd"] * 1e-3) / 1e12
     bwd_tf = bwd_flops / (bwd_ms * 1e-3) / 1e12
 
-    # Roofline of the dominant kernel: algorithmic FLOPs per launch / its time.
-    algo = {
-        "fwd": ("fwd_mfma_kernel", 4 * unit),
-        "bwd_query_side": ("bwd_query_kernel", 8 * unit),   # S recompute, dP, dQ~, U~
-        "bwd_key_side": ("bwd_key_kernel", 4 * unit),    # dV, dK (its S/dP recompute is not counted)
+    # Roofline of the dominant kernel: algorithmic FLOPs per launch / its time
+    # (HIP events on the stream the library launches on). The query-side stage
+    # also runs the small chunk-boundary fix-up kernel inside its events.
+    qkernel = "bwd_query_kernel" if w.w2 <= 32 else "bwd_q_kernel"
+    algo = {  # phase: (kernel, algorithmic FLOPs, executed MFMA FLOPs)
+        "fwd": ("fwd_mfma_kernel", 4 * unit, 4 * unit),
+        "bwd_query_side": (qkernel, 8 * unit, 8 * unit),   # S recompute, dP, dQ~, U~
+        "bwd_key_side": ("bwd_key_kernel", 4 * unit, 8 * unit),  # dV, dK (+ S/dP recompute, not counted)
     }
     dom = max(algo, key=lambda p: ms[p])
-    kname, kflops = algo[dom]
+    kname, kflops, _ = algo[dom]
     achieved = kflops / (ms[dom] * 1e-3) / 1e12
+    kernels = {}
+    for p_, (kn, af, ef) in algo.items():
+        kernels[kn] = {"ms": round(ms[p_], 4),
+                       "algorithmic_tflops": round(af / (ms[p_] * 1e-3) / 1e12, 2),
+                       "frac": round(af / (ms[p_] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                       "executed_frac": round(ef / (ms[p_] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}
     roofline = {"bound": "mfma", "kernel": kname, "achieved": round(achieved, 2),
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                "traffic": read_traffic(kname, w.name)}
+                "traffic": read_traffic(kname, w.name),
+                "fwd_frac": round(fwd_flops / (ms["fwd"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                "bwd_frac": round(bwd_flops / (bwd_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                "step_frac": round(value / PEAK_BF16_TFLOPS, 4),
+                "kernels": kernels}
 
     result = {
         "metric": METRIC,

@@ -10,6 +10,9 @@ the package.
   form that is unchanged when one rotation in SO(3) is applied to all three.
 * Section 5, Eq. (logits): the vectors are cut into chunks of 3 components and
   A_ijk = scale * sum_l det([q_i^(l); k_j^(l); k'_k^(l)]).
+  Reading: Eq. (logits) has no scale factor; `scale` is kept as an argument so
+  that both logit forms share one interface, and scale = 1 is the paper's form
+  (pinned by test_scale_one_is_the_papers_unscaled_form).
   Reading: the paper takes the head dimension as a multiple of 3; for other D
   the chunks are components 3l .. 3l + 2 for l < floor(D / 3) and the D mod 3
   trailing components enter no logit (their Q, K, K' gradients are zero).

@@ -155,9 +155,10 @@ def simplicial_attn_fwd(q, k, kp, v, vp, w1, w2, scale=None, out=None, lse=None)
     return _fwd("simplicial_attn_fwd", q, k, kp, v, vp, w1, w2, scale, out, lse)
 
 
-def simplicial_attn_det_fwd(q, k, kp, v, vp, w1, w2, scale=None, out=None, lse=None):
+def simplicial_attn_det_fwd(q, k, kp, v, vp, w1, w2, scale=1.0, out=None, lse=None):
     """Forward with the determinant logits of Section 5 (arguments and results
-    as simplicial_attn_fwd)."""
+    as simplicial_attn_fwd). `scale` defaults to 1: Eq. (logits) has no scale
+    factor."""
     return _fwd("simplicial_attn_det_fwd", q, k, kp, v, vp, w1, w2, scale, out, lse)
 
 
@@ -304,10 +305,11 @@ def simplicial_attn_bwd_noalloc(q, k, kp, v, vp, out, dout, lse, w1, w2, scale=N
     return grads
 
 
-def simplicial_attn_det_bwd(q, k, kp, v, vp, out, dout, lse, w1, w2, scale=None, grads=None,
+def simplicial_attn_det_bwd(q, k, kp, v, vp, out, dout, lse, w1, w2, scale=1.0, grads=None,
                             workspace=None):
     """Backward with the determinant logits of Section 5 (arguments and results
-    as simplicial_attn_bwd; `out`/`lse` from simplicial_attn_det_fwd)."""
+    as simplicial_attn_bwd; `out`/`lse` from simplicial_attn_det_fwd; `scale`
+    defaults to 1 as in the forward)."""
     return _bwd("simplicial_attn_det_bwd", q, k, kp, v, vp, out, dout, lse, w1, w2, scale, grads,
                 workspace)
 

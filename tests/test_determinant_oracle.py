@@ -140,3 +140,25 @@ def test_backward_matches_central_finite_differences():
             fm = float(np.sum(dor.forward(*minus, w1, w2, scale)[0] * arrs[5]))
             num = (fp - fm) / (2 * eps)
             assert abs(num - g[t][r, c]) <= 1e-6 * max(1.0, abs(num)), (t, r, c, num, g[t][r, c])
+
+
+def test_scale_one_is_the_papers_unscaled_form():
+    """Eq. (logits) carries no scale factor: at scale = 1 the oracle's logits are
+    the plain sum of chunk determinants, and its forward is the joint softmax of
+    exactly those logits over the windows (dense brute force with numpy's det)."""
+    n, d, w1, w2 = 7, 9, 4, 3
+    q, k, kp, v, vp = (_rand((n, d), s) for s in range(50, 55))
+    o, lse = dor.forward(q, k, kp, v, vp, w1, w2, 1.0)
+    for i in range(n):
+        js = range(max(0, i - w1 + 1), i + 1)
+        ks = range(max(0, i - w2 + 1), i + 1)
+        a = np.array([[sum(np.linalg.det(np.stack([q[i, 3 * l:3 * l + 3], k[j, 3 * l:3 * l + 3],
+                                                    kp[kk, 3 * l:3 * l + 3]])) for l in range(d // 3))
+                       for kk in ks] for j in js])
+        assert np.allclose(dor.det_logits(q[i], k[js[0]:i + 1], kp[ks[0]:i + 1], 1.0), a,
+                           rtol=1e-12, atol=1e-12)
+        p = np.exp(a - a.max())
+        z = p.sum()
+        ref_o = np.einsum("jk,jd,kd->d", p / z, v[js[0]:i + 1], vp[ks[0]:i + 1])
+        np.testing.assert_allclose(o[i], ref_o, rtol=1e-11, atol=1e-12)
+        assert lse[i] == pytest.approx(a.max() + np.log(z), rel=1e-12, abs=1e-12)
