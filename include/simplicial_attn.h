@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define SIMPLICIAL_ATTN_ABI_VERSION 3
+#define SIMPLICIAL_ATTN_ABI_VERSION 4
 
 #define SA_DTYPE_F32 0
 #define SA_DTYPE_BF16 1
@@ -114,6 +114,29 @@ int simplicial_attn_bwd(const void* q, const void* k, const void* kp, const void
                         void* dkp, void* dv, void* dvp, void* workspace, size_t workspace_bytes,
                         int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1, int32_t w2,
                         float scale, int32_t dtype, void* stream);
+
+/*
+ * Forward and backward with the K' and V' bias constants of the paper's
+ * Appendix B kernels (the K2_BIAS / V2_BIAS constants, there a "KV2 norm"
+ * applied to every loaded K' / V' element): the operation of simplicial_attn_fwd
+ * / simplicial_attn_bwd with K' + kp_bias and V' + vp_bias (every element
+ * shifted by the constant) in place of K' and V'. Masked pairs stay excluded
+ * whatever the constants. dK' and dV' are the gradients with respect to the
+ * given K' and V' (a constant shift does not change them). Arguments, layouts,
+ * workspace (simplicial_attn_bwd_workspace_size) and errors as the plain pair;
+ * non-finite constants are SA_ERR_INVALID. Constants 0 give exactly the plain
+ * pair's results.
+ */
+int simplicial_attn_fwd_biased(const void* q, const void* k, const void* kp, const void* v,
+                               const void* vp, void* out, float* lse, int64_t B, int64_t N,
+                               int64_t H, int64_t D, int32_t w1, int32_t w2, float scale,
+                               float kp_bias, float vp_bias, int32_t dtype, void* stream);
+int simplicial_attn_bwd_biased(const void* q, const void* k, const void* kp, const void* v,
+                               const void* vp, const void* out, const void* dout, const float* lse,
+                               void* dq, void* dk, void* dkp, void* dv, void* dvp, void* workspace,
+                               size_t workspace_bytes, int64_t B, int64_t N, int64_t H, int64_t D,
+                               int32_t w1, int32_t w2, float scale, float kp_bias, float vp_bias,
+                               int32_t dtype, void* stream);
 
 /*
  * The backward without any allocation, for callers that cannot allocate

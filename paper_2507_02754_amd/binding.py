@@ -21,6 +21,8 @@ __all__ = [
     "simplicial_attn_bwd",
     "simplicial_attn_bwd_gqa",
     "simplicial_attn_bwd_noalloc",
+    "simplicial_attn_fwd_biased",
+    "simplicial_attn_bwd_biased",
     "simplicial_attn_det_fwd",
     "simplicial_attn_det_bwd",
     "simplicial_attn_bwd_gqa_workspace_size",
@@ -66,6 +68,11 @@ def load_library():
     lib.simplicial_attn_fwd_gqa.restype = ctypes.c_int
     lib.simplicial_attn_bwd.argtypes = [vp] * 14 + [ctypes.c_size_t] + [i64] * 4 + [i32, i32, f32, i32, vp]
     lib.simplicial_attn_bwd.restype = ctypes.c_int
+    lib.simplicial_attn_fwd_biased.argtypes = [vp] * 7 + [i64] * 4 + [i32, i32, f32, f32, f32, i32, vp]
+    lib.simplicial_attn_fwd_biased.restype = ctypes.c_int
+    lib.simplicial_attn_bwd_biased.argtypes = ([vp] * 14 + [ctypes.c_size_t] + [i64] * 4 +
+                                               [i32, i32, f32, f32, f32, i32, vp])
+    lib.simplicial_attn_bwd_biased.restype = ctypes.c_int
     lib.simplicial_attn_bwd_noalloc.argtypes = [vp] * 13 + [i64] * 4 + [i32, i32, f32, i32, vp]
     lib.simplicial_attn_bwd_noalloc.restype = ctypes.c_int
     lib.simplicial_attn_det_fwd.argtypes = lib.simplicial_attn_fwd.argtypes
@@ -162,7 +169,15 @@ def simplicial_attn_det_fwd(q, k, kp, v, vp, w1, w2, scale=1.0, out=None, lse=No
     return _fwd("simplicial_attn_det_fwd", q, k, kp, v, vp, w1, w2, scale, out, lse)
 
 
-def _fwd(entry, q, k, kp, v, vp, w1, w2, scale, out, lse):
+def simplicial_attn_fwd_biased(q, k, kp, v, vp, w1, w2, scale=None, kp_bias=0.0, vp_bias=0.0,
+                               out=None, lse=None):
+    """Forward with the K' / V' bias constants (K' + kp_bias, V' + vp_bias in
+    place of K', V'); otherwise as simplicial_attn_fwd."""
+    return _fwd("simplicial_attn_fwd_biased", q, k, kp, v, vp, w1, w2, scale, out, lse,
+                biases=(float(kp_bias), float(vp_bias)))
+
+
+def _fwd(entry, q, k, kp, v, vp, w1, w2, scale, out, lse, biases=()):
     (B, N, H, D), dt = _check_inputs((q, k, kp, v, vp), ("q", "k", "kp", "v", "vp"))
     if scale is None:
         scale = D ** -0.5
@@ -177,7 +192,7 @@ def _fwd(entry, q, k, kp, v, vp, w1, w2, scale, out, lse):
         raise ValueError("lse must be a contiguous float32 [B, H, N] tensor on the inputs' device")
     rc = getattr(load_library(), entry)(
         _ptr(q), _ptr(k), _ptr(kp), _ptr(v), _ptr(vp), _ptr(out), _ptr(lse),
-        B, N, H, D, int(w1), int(w2), float(scale), dt, _stream(q.device))
+        B, N, H, D, int(w1), int(w2), float(scale), *biases, dt, _stream(q.device))
     if rc != 0:
         raise SimplicialAttnError(rc, entry)
     return out, lse
@@ -314,7 +329,15 @@ def simplicial_attn_det_bwd(q, k, kp, v, vp, out, dout, lse, w1, w2, scale=1.0, 
                 workspace)
 
 
-def _bwd(entry, q, k, kp, v, vp, out, dout, lse, w1, w2, scale, grads, workspace):
+def simplicial_attn_bwd_biased(q, k, kp, v, vp, out, dout, lse, w1, w2, scale=None, kp_bias=0.0,
+                               vp_bias=0.0, grads=None, workspace=None):
+    """Backward of simplicial_attn_fwd_biased (same constants); gradients are
+    with respect to the given K' and V'."""
+    return _bwd("simplicial_attn_bwd_biased", q, k, kp, v, vp, out, dout, lse, w1, w2, scale, grads,
+                workspace, biases=(float(kp_bias), float(vp_bias)))
+
+
+def _bwd(entry, q, k, kp, v, vp, out, dout, lse, w1, w2, scale, grads, workspace, biases=()):
     (B, N, H, D), dt = _check_inputs((q, k, kp, v, vp, out, dout),
                                      ("q", "k", "kp", "v", "vp", "out", "dout"))
     if scale is None:
@@ -330,7 +353,7 @@ def _bwd(entry, q, k, kp, v, vp, out, dout, lse, w1, w2, scale, grads, workspace
     rc = getattr(load_library(), entry)(
         _ptr(q), _ptr(k), _ptr(kp), _ptr(v), _ptr(vp), _ptr(out), _ptr(dout), _ptr(lse),
         *(_ptr(g) for g in grads), _ptr(workspace), ctypes.c_size_t(workspace.numel()),
-        B, N, H, D, int(w1), int(w2), float(scale), dt, _stream(q.device))
+        B, N, H, D, int(w1), int(w2), float(scale), *biases, dt, _stream(q.device))
     if rc != 0:
         raise SimplicialAttnError(rc, entry)
     return grads

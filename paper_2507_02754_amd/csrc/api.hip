@@ -57,6 +57,8 @@ Shape make_shape(int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1, int32_t
   s.Hkv = s.H;
   s.form = 0;
   s.ws_cap = 0;
+  s.kp_bias = 0.f;
+  s.vp_bias = 0.f;
   return s;
 }
 
@@ -113,17 +115,21 @@ int check_bwd(int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1, int32_t w2
   return SA_OK;
 }
 
-// Forward with Hkv K/V heads (Hkv == H: the plain forward).
+// Forward with Hkv K/V heads (Hkv == H: the plain forward) and K'/V' bias
+// constants (0: none).
 int forward(const void* q, const void* k, const void* kp, const void* v, const void* vp, void* out,
             float* lse, int64_t B, int64_t N, int64_t H, int64_t Hkv, int64_t D, int32_t w1,
-            int32_t w2, float scale, int32_t dtype, void* stream) {
+            int32_t w2, float scale, int32_t dtype, void* stream, float kp_bias = 0.f,
+            float vp_bias = 0.f) {
   if (check_ptrs({q, k, kp, v, vp, out, lse}) != SA_OK) return SA_ERR_INVALID;
-  if (!isfinite(scale)) return SA_ERR_INVALID;
+  if (!isfinite(scale) || !isfinite(kp_bias) || !isfinite(vp_bias)) return SA_ERR_INVALID;
   if (Hkv <= 0 || Hkv > H || H % Hkv != 0) return SA_ERR_INVALID;
   const int rc = check_sizes(B, N, H, D, w1, w2, dtype);
   if (rc != SA_OK) return rc;
   Shape s = make_shape(B, N, H, D, w1, w2, scale, dtype);
   s.Hkv = static_cast<int>(Hkv);
+  s.kp_bias = kp_bias;
+  s.vp_bias = vp_bias;
   hipStream_t st = static_cast<hipStream_t>(stream);
   switch (choose_path(0, B, N, H, D, w1, w2, dtype)) {
     case Path::Generic: return to_status(sa::generic_fwd(s, q, k, kp, v, vp, out, lse, st));
@@ -274,11 +280,33 @@ int simplicial_attn_bwd(const void* q, const void* k, const void* kp, const void
                         void* dkp, void* dv, void* dvp, void* workspace, size_t workspace_bytes,
                         int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1, int32_t w2,
                         float scale, int32_t dtype, void* stream) {
+  return simplicial_attn_bwd_biased(q, k, kp, v, vp, out, dout, lse, dq, dk, dkp, dv, dvp,
+                                    workspace, workspace_bytes, B, N, H, D, w1, w2, scale, 0.f, 0.f,
+                                    dtype, stream);
+}
+
+int simplicial_attn_fwd_biased(const void* q, const void* k, const void* kp, const void* v,
+                               const void* vp, void* out, float* lse, int64_t B, int64_t N,
+                               int64_t H, int64_t D, int32_t w1, int32_t w2, float scale,
+                               float kp_bias, float vp_bias, int32_t dtype, void* stream) {
+  return forward(q, k, kp, v, vp, out, lse, B, N, H, H, D, w1, w2, scale, dtype, stream, kp_bias,
+                 vp_bias);
+}
+
+int simplicial_attn_bwd_biased(const void* q, const void* k, const void* kp, const void* v,
+                               const void* vp, const void* out, const void* dout, const float* lse,
+                               void* dq, void* dk, void* dkp, void* dv, void* dvp, void* workspace,
+                               size_t workspace_bytes, int64_t B, int64_t N, int64_t H, int64_t D,
+                               int32_t w1, int32_t w2, float scale, float kp_bias, float vp_bias,
+                               int32_t dtype, void* stream) {
   if (check_ptrs({q, k, kp, v, vp, out, dout, lse, dq, dk, dkp, dv, dvp, workspace}) != SA_OK)
     return SA_ERR_INVALID;
+  if (!isfinite(kp_bias) || !isfinite(vp_bias)) return SA_ERR_INVALID;
   const int rc = check_bwd(B, N, H, D, w1, w2, scale, dtype, workspace_bytes);
   if (rc != SA_OK) return rc;
-  const Shape s = make_shape(B, N, H, D, w1, w2, scale, dtype);
+  Shape s = make_shape(B, N, H, D, w1, w2, scale, dtype);
+  s.kp_bias = kp_bias;
+  s.vp_bias = vp_bias;
   const Path path = choose_path(1, B, N, H, D, w1, w2, dtype);
   hipStream_t st = static_cast<hipStream_t>(stream);
   int r = run_delta(s, path, out, dout, workspace, st);

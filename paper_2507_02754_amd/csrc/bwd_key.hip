@@ -55,7 +55,7 @@ struct KeyLds {
 template <int X>
 using ic = std::integral_constant<int, X>;
 
-template <int D, int G>
+template <int D, int G, bool BIAS>
 __global__ __launch_bounds__(kKeyThreads, 1) void bwd_key_kernel(
     Shape s, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ kp, const uint16_t* __restrict__ v, const uint16_t* __restrict__ vp,
@@ -158,8 +158,12 @@ __global__ __launch_bounds__(kKeyThreads, 1) void bwd_key_kernel(
 #pragma unroll
   for (int y = 0; y < IPT; ++y) formoff[y] = T::off(rho + RPI * y, dc) + (roleA ? 0 : T::bytes);
   // Two register sets for the formation loads (role A keeps loads in flight
-  // for two iterations, role B for one).
+  // for two iterations, role B for one). With bias constants, fb holds the
+  // constant for rows inside the window and 0 for the others, which must stay
+  // zero rows (their k' / v' load as zeros).
   u32x4_t fr[2], fm[2][IPT];
+  float fb[2][IPT];
+  const float mbias = roleA ? s.kp_bias : s.vp_bias;
   auto fetch = [&](int rb, auto set) __attribute__((always_inline)) {
     constexpr int X = decltype(set)::value;
     const int i = j0 + rb / G, g = rb % G;
@@ -167,7 +171,9 @@ __global__ __launch_bounds__(kKeyThreads, 1) void bwd_key_kernel(
 #pragma unroll
     for (int y = 0; y < IPT; ++y) {
       const int kk = i - W2P + 1 + 32 * g + rho + RPI * y;
-      fm[X][y] = ldbuf128(rmod, kk > i - w2 ? kk * rsb + 16 * dc : -1);
+      const bool inwin = kk > i - w2 && (!BIAS || kk >= 0);  // kk < 0 also loads zeros
+      fm[X][y] = ldbuf128(rmod, inwin ? kk * rsb + 16 * dc : -1);
+      if constexpr (BIAS) fb[X][y] = inwin ? mbias : 0.f;
     }
   };
   auto form_put = [&](int tile_off, auto set) __attribute__((always_inline)) {
@@ -182,7 +188,9 @@ __global__ __launch_bounds__(kKeyThreads, 1) void bwd_key_kernel(
     for (int y = 0; y < IPT; ++y) {
       u32x4_t a4;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) a4[e] = pack_bf16x2(lo[e] * bf16_lo(fm[X][y][e]), hi[e] * bf16_hi(fm[X][y][e]));
+      for (int e = 0; e < 4; ++e)
+        a4[e] = pack_bf16x2(lo[e] * plus_bias<BIAS>(bf16_lo(fm[X][y][e]), fb[X][y]),
+                            hi[e] * plus_bias<BIAS>(bf16_hi(fm[X][y][e]), fb[X][y]));
       lds_st(lds + formoff[y] + tile_off, a4);
     }
   };
@@ -483,12 +491,12 @@ __global__ __launch_bounds__(kKeyThreads, 1) void bwd_key_kernel(
   }
 }
 
-template <int D, int G>
+template <int D, int G, bool BIAS>
 hipError_t launch_key(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
                       const void* vp, const void* dout, const float* lse, const float* delta, void* dk,
                       void* dv, hipStream_t st) {
   const long tot = static_cast<long>((s.N + 127) / 128) * s.B * s.H;
-  hipLaunchKernelGGL((bwd_key_kernel<D, G>), dim3(static_cast<unsigned>(((tot + 7) / 8) * 8)),
+  hipLaunchKernelGGL((bwd_key_kernel<D, G, BIAS>), dim3(static_cast<unsigned>(((tot + 7) / 8) * 8)),
                      dim3(kKeyThreads), 0, st, s, static_cast<const uint16_t*>(q),
                      static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(kp),
                      static_cast<const uint16_t*>(v), static_cast<const uint16_t*>(vp),
@@ -499,17 +507,26 @@ hipError_t launch_key(const Shape& s, const void* q, const void* k, const void* 
 
 }  // namespace
 
+template <bool BIAS>
+hipError_t mfma_bwd_key_b(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
+                          const void* vp, const void* dout, const float* lse, const float* delta,
+                          void* dk, void* dv, hipStream_t st) {
+  const int G = s.w2 <= 32 ? 1 : 2;
+  if (s.D == 128)
+    return G == 1 ? launch_key<128, 1, BIAS>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, st)
+                  : launch_key<128, 2, BIAS>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, st);
+  if (s.D == 64)
+    return G == 1 ? launch_key<64, 1, BIAS>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, st)
+                  : launch_key<64, 2, BIAS>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, st);
+  return hipErrorInvalidValue;
+}
+
 hipError_t mfma_bwd_key(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
                         const void* vp, const void* dout, const float* lse, const float* delta,
                         void* dk, void* dv, hipStream_t st) {
-  const int G = s.w2 <= 32 ? 1 : 2;
-  if (s.D == 128)
-    return G == 1 ? launch_key<128, 1>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, st)
-                  : launch_key<128, 2>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, st);
-  if (s.D == 64)
-    return G == 1 ? launch_key<64, 1>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, st)
-                  : launch_key<64, 2>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, st);
-  return hipErrorInvalidValue;
+  return s.kp_bias != 0.f || s.vp_bias != 0.f
+             ? mfma_bwd_key_b<true>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, st)
+             : mfma_bwd_key_b<false>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, st);
 }
 
 }  // namespace sa

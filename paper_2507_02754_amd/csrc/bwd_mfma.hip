@@ -112,7 +112,7 @@ struct BwdQLds {
   static constexpr int bytes = qringOff + 2 * RQ * 2 * D;
 };
 
-template <int D, int G, int WAVES>
+template <int D, int G, int WAVES, bool BIAS>
 __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
     Shape s, BwdPlan plan, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ kp, const uint16_t* __restrict__ v, const uint16_t* __restrict__ vp,
@@ -295,8 +295,10 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
         if (rowvalid) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            a4[e] = pack_bf16x2(bf16_lo(qa[e]) * bf16_lo(ka[e]) * qscale, bf16_hi(qa[e]) * bf16_hi(ka[e]) * qscale);
-            b4[e] = pack_bf16x2(bf16_lo(oa[e]) * bf16_lo(va[e]), bf16_hi(oa[e]) * bf16_hi(va[e]));
+            a4[e] = pack_bf16x2(bf16_lo(qa[e]) * plus_bias<BIAS>(bf16_lo(ka[e]), s.kp_bias) * qscale,
+                                bf16_hi(qa[e]) * plus_bias<BIAS>(bf16_hi(ka[e]), s.kp_bias) * qscale);
+            b4[e] = pack_bf16x2(bf16_lo(oa[e]) * plus_bias<BIAS>(bf16_lo(va[e]), s.vp_bias),
+                                bf16_hi(oa[e]) * plus_bias<BIAS>(bf16_hi(va[e]), s.vp_bias));
           }
         }
         qt[t] = a4;
@@ -462,10 +464,10 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
         for (int qd = 0; qd < 4; ++qd) {
           const int d = 32 * dt + 8 * qd + 4 * h;
           const u32x2_t m = *reinterpret_cast<const u32x2_t*>(krow + 16 * ((d >> 3) ^ T::swz(kslot)) + 8 * h);
-          xv[16 * dt + 4 * qd + 0] = bf16_lo(m[0]) * adq[dt][4 * qd + 0];
-          xv[16 * dt + 4 * qd + 1] = bf16_hi(m[0]) * adq[dt][4 * qd + 1];
-          xv[16 * dt + 4 * qd + 2] = bf16_lo(m[1]) * adq[dt][4 * qd + 2];
-          xv[16 * dt + 4 * qd + 3] = bf16_hi(m[1]) * adq[dt][4 * qd + 3];
+          xv[16 * dt + 4 * qd + 0] = plus_bias<BIAS>(bf16_lo(m[0]), s.kp_bias) * adq[dt][4 * qd + 0];
+          xv[16 * dt + 4 * qd + 1] = plus_bias<BIAS>(bf16_hi(m[0]), s.kp_bias) * adq[dt][4 * qd + 1];
+          xv[16 * dt + 4 * qd + 2] = plus_bias<BIAS>(bf16_lo(m[1]), s.kp_bias) * adq[dt][4 * qd + 2];
+          xv[16 * dt + 4 * qd + 3] = plus_bias<BIAS>(bf16_hi(m[1]), s.kp_bias) * adq[dt][4 * qd + 3];
         }
       reduce_lanes32<NV>(xv, lane);
       constexpr int NO = NV / 32;  // sums per lane: columns j0 .. j0 + NO - 1
@@ -621,10 +623,15 @@ hipError_t launch_stage(const Shape& s, BwdStage stage, const void* q, const voi
   } else if (stage == BwdStage::Query) {
     constexpr int WAVES = 4;
     const long totq = static_cast<long>(plan.nchunks) * s.B * s.H;
-    hipLaunchKernelGGL((bwd_q_kernel<D, G, WAVES>), dim3(static_cast<unsigned>(((totq + 7) / 8) * 8)),
-                       dim3(64 * WAVES), 0, st, s, plan, Q, K, KP, V, VP, DO, lse, delta,
-                       static_cast<uint16_t*>(g0), static_cast<uint16_t*>(g1),
-                       static_cast<uint16_t*>(g2), halo);
+    auto go = [&](auto kern) {
+      hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(((totq + 7) / 8) * 8)), dim3(64 * WAVES), 0, st,
+                         s, plan, Q, K, KP, V, VP, DO, lse, delta, static_cast<uint16_t*>(g0),
+                         static_cast<uint16_t*>(g1), static_cast<uint16_t*>(g2), halo);
+    };
+    if (s.kp_bias != 0.f || s.vp_bias != 0.f)
+      go(bwd_q_kernel<D, G, WAVES, true>);
+    else
+      go(bwd_q_kernel<D, G, WAVES, false>);
     if (plan.nchunks > 1) {
       const long n = static_cast<long>(s.B) * s.H * (plan.nchunks - 1) * (plan.W2P - 1) * D;
       hipLaunchKernelGGL(halo_fixup_kernel<D>, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256),

@@ -60,7 +60,7 @@ struct QueryLds {
   static constexpr int bytes = qringOff + 2 * RQ * 2 * D;
 };
 
-template <int D>
+template <int D, bool BIAS>
 __global__ __launch_bounds__(kQThreads, 1) void bwd_query_kernel(
     Shape s, BwdPlan plan, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ kp, const uint16_t* __restrict__ v, const uint16_t* __restrict__ vp,
@@ -312,7 +312,8 @@ __global__ __launch_bounds__(kQThreads, 1) void bwd_query_kernel(
           if (rowvalid) {
 #pragma unroll
             for (int e = 0; e < 4; ++e)
-              a4[e] = pack_bf16x2(bf16_lo(qa[e]) * bf16_lo(ka[e]) * qscale, bf16_hi(qa[e]) * bf16_hi(ka[e]) * qscale);
+              a4[e] = pack_bf16x2(bf16_lo(qa[e]) * plus_bias<BIAS>(bf16_lo(ka[e]), s.kp_bias) * qscale,
+                                  bf16_hi(qa[e]) * plus_bias<BIAS>(bf16_hi(ka[e]), s.kp_bias) * qscale);
           }
           qt[t] = a4;
         }
@@ -428,7 +429,8 @@ __global__ __launch_bounds__(kQThreads, 1) void bwd_query_kernel(
           if (rowvalid) {
 #pragma unroll
             for (int e = 0; e < 4; ++e)
-              b4[e] = pack_bf16x2(bf16_lo(oa[e]) * bf16_lo(va[e]), bf16_hi(oa[e]) * bf16_hi(va[e]));
+              b4[e] = pack_bf16x2(bf16_lo(oa[e]) * plus_bias<BIAS>(bf16_lo(va[e]), s.vp_bias),
+                                  bf16_hi(oa[e]) * plus_bias<BIAS>(bf16_hi(va[e]), s.vp_bias));
           }
           ot[t] = b4;
         }
@@ -505,10 +507,10 @@ __global__ __launch_bounds__(kQThreads, 1) void bwd_query_kernel(
           for (int qd = 0; qd < 4; ++qd) {
             const int d = 32 * dt + 8 * qd + 4 * h;
             const u32x2_t m = *reinterpret_cast<const u32x2_t*>(krow + 16 * ((d >> 3) ^ T::swz(kslot)) + 8 * h);
-            xv[16 * dt + 4 * qd + 0] = bf16_lo(m[0]) * adq[dt][4 * qd + 0];
-            xv[16 * dt + 4 * qd + 1] = bf16_hi(m[0]) * adq[dt][4 * qd + 1];
-            xv[16 * dt + 4 * qd + 2] = bf16_lo(m[1]) * adq[dt][4 * qd + 2];
-            xv[16 * dt + 4 * qd + 3] = bf16_hi(m[1]) * adq[dt][4 * qd + 3];
+            xv[16 * dt + 4 * qd + 0] = plus_bias<BIAS>(bf16_lo(m[0]), s.kp_bias) * adq[dt][4 * qd + 0];
+            xv[16 * dt + 4 * qd + 1] = plus_bias<BIAS>(bf16_hi(m[0]), s.kp_bias) * adq[dt][4 * qd + 1];
+            xv[16 * dt + 4 * qd + 2] = plus_bias<BIAS>(bf16_lo(m[1]), s.kp_bias) * adq[dt][4 * qd + 2];
+            xv[16 * dt + 4 * qd + 3] = plus_bias<BIAS>(bf16_hi(m[1]), s.kp_bias) * adq[dt][4 * qd + 3];
           }
         reduce_lanes32_level<NV, 0>(xv, lane);
         const char* qrow = qring + ((i - cs) % RQ) * 2 * D;  // q_i
@@ -568,14 +570,16 @@ hipError_t mfma_bwd_query(const Shape& s, const BwdPlan& plan, const void* q, co
   const auto* V = static_cast<const uint16_t*>(v);
   const auto* VP = static_cast<const uint16_t*>(vp);
   const auto* DO = static_cast<const uint16_t*>(dout);
+  const bool bias = s.kp_bias != 0.f || s.vp_bias != 0.f;
+  auto go = [&](auto kern) {
+    hipLaunchKernelGGL(kern, grid, dim3(kQThreads), 0, st, s, plan, Q, K, KP, V, VP, DO, lse, delta,
+                       static_cast<uint16_t*>(dq), static_cast<uint16_t*>(dkp), static_cast<uint16_t*>(dvp),
+                       halo);
+  };
   if (s.D == 128)
-    hipLaunchKernelGGL(bwd_query_kernel<128>, grid, dim3(kQThreads), 0, st, s, plan, Q, K, KP, V, VP, DO,
-                       lse, delta, static_cast<uint16_t*>(dq), static_cast<uint16_t*>(dkp),
-                       static_cast<uint16_t*>(dvp), halo);
+    bias ? go(bwd_query_kernel<128, true>) : go(bwd_query_kernel<128, false>);
   else if (s.D == 64)
-    hipLaunchKernelGGL(bwd_query_kernel<64>, grid, dim3(kQThreads), 0, st, s, plan, Q, K, KP, V, VP, DO,
-                       lse, delta, static_cast<uint16_t*>(dq), static_cast<uint16_t*>(dkp),
-                       static_cast<uint16_t*>(dvp), halo);
+    bias ? go(bwd_query_kernel<64, true>) : go(bwd_query_kernel<64, false>);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

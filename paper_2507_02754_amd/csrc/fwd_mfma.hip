@@ -74,7 +74,8 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 // FORM 0: trilinear logits (Section 4); FORM 1: determinant logits (Section 5,
 // w2 <= 32 only), which differ only in the modulated query formed below.
-template <int D, int G, int FORM>
+// BIAS: K' and V' values get the constants s.kp_bias / s.vp_bias added on load.
+template <int D, int G, int FORM, bool BIAS>
 __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const uint16_t* __restrict__ q,
                                                                const uint16_t* __restrict__ k,
                                                                const uint16_t* __restrict__ kp,
@@ -270,8 +271,8 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
     for (int t = 0; t < NT; ++t)
 #pragma unroll
       for (int e = 0; e < 4; ++e)
-        qt[t][e] = pack_bf16x2(bf16_lo(qa[t][e]) * bf16_lo(ka[t][e]) * qscale,
-                               bf16_hi(qa[t][e]) * bf16_hi(ka[t][e]) * qscale);
+        qt[t][e] = pack_bf16x2(bf16_lo(qa[t][e]) * plus_bias<BIAS>(bf16_lo(ka[t][e]), s.kp_bias) * qscale,
+                               bf16_hi(qa[t][e]) * plus_bias<BIAS>(bf16_hi(ka[t][e]), s.kp_bias) * qscale);
   }
 
   f32x16_t acc[NDT];
@@ -314,8 +315,8 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
       for (int t = 0; t < NT; ++t)
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          qt[t][e] = keep & pack_bf16x2(bf16_lo(qa[t][e]) * bf16_lo(ka[t][e]) * qscale,
-                                        bf16_hi(qa[t][e]) * bf16_hi(ka[t][e]) * qscale);
+          qt[t][e] = keep & pack_bf16x2(bf16_lo(qa[t][e]) * plus_bias<BIAS>(bf16_lo(ka[t][e]), s.kp_bias) * qscale,
+                                        bf16_hi(qa[t][e]) * plus_bias<BIAS>(bf16_hi(ka[t][e]), s.kp_bias) * qscale);
     } else {
       // Determinant logits: per 3-component chunk, det([q; k; k']) =
       // k . (k' x q), so q~ = (scale log2 e) * (k'_k x q_i) chunk by chunk and
@@ -338,11 +339,14 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
                                 lds_ld<unsigned>(qrow + 16 * (chn ^ swq))};
         // window x = 0 .. 11 holds components 8 ch - 2 .. 8 ch + 9
         float fk[12], fq[12];
-        fk[0] = bf16_lo(kw[0]), fk[1] = bf16_hi(kw[0]), fk[10] = bf16_lo(kw[1]), fk[11] = bf16_hi(kw[1]);
+        const float kb = s.kp_bias;
+        fk[0] = plus_bias<BIAS>(bf16_lo(kw[0]), kb), fk[1] = plus_bias<BIAS>(bf16_hi(kw[0]), kb);
+        fk[10] = plus_bias<BIAS>(bf16_lo(kw[1]), kb), fk[11] = plus_bias<BIAS>(bf16_hi(kw[1]), kb);
         fq[0] = bf16_lo(qw[0]), fq[1] = bf16_hi(qw[0]), fq[10] = bf16_lo(qw[1]), fq[11] = bf16_hi(qw[1]);
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
-          fk[2 + 2 * w] = bf16_lo(kc[w]), fk[3 + 2 * w] = bf16_hi(kc[w]);
+          fk[2 + 2 * w] = plus_bias<BIAS>(bf16_lo(kc[w]), kb);
+          fk[3 + 2 * w] = plus_bias<BIAS>(bf16_hi(kc[w]), kb);
           fq[2 + 2 * w] = bf16_lo(qc[w]), fq[3 + 2 * w] = bf16_hi(qc[w]);
         }
         // component e of the fragment sits at position m of its chunk, which
@@ -540,10 +544,10 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
 #pragma unroll
     for (int qd = 0; qd < 4; ++qd) {
       const u32x2_t x = vpr[4 * dt + qd];
-      xv[16 * dt + 4 * qd + 0] = wgt * bf16_lo(x[0]) * acc[dt][4 * qd + 0];
-      xv[16 * dt + 4 * qd + 1] = wgt * bf16_hi(x[0]) * acc[dt][4 * qd + 1];
-      xv[16 * dt + 4 * qd + 2] = wgt * bf16_lo(x[1]) * acc[dt][4 * qd + 2];
-      xv[16 * dt + 4 * qd + 3] = wgt * bf16_hi(x[1]) * acc[dt][4 * qd + 3];
+      xv[16 * dt + 4 * qd + 0] = wgt * plus_bias<BIAS>(bf16_lo(x[0]), s.vp_bias) * acc[dt][4 * qd + 0];
+      xv[16 * dt + 4 * qd + 1] = wgt * plus_bias<BIAS>(bf16_hi(x[0]), s.vp_bias) * acc[dt][4 * qd + 1];
+      xv[16 * dt + 4 * qd + 2] = wgt * plus_bias<BIAS>(bf16_lo(x[1]), s.vp_bias) * acc[dt][4 * qd + 2];
+      xv[16 * dt + 4 * qd + 3] = wgt * plus_bias<BIAS>(bf16_hi(x[1]), s.vp_bias) * acc[dt][4 * qd + 3];
     }
   reduce_lanes32<NV>(xv, lane);
   const int j0 = NV / 2 * ((c >> 4) & 1) + NV / 4 * ((c >> 3) & 1) + NV / 8 * ((c >> 2) & 1) +
@@ -574,14 +578,14 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
   }
 }
 
-template <int D, int G, int FORM = 0>
+template <int D, int G, int FORM = 0, bool BIAS = false>
 hipError_t launch(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
                   const void* vp, void* out, float* lse, hipStream_t st) {
   constexpr int QW = kWaves / G;
   const long tiles = (s.N + QW - 1) / QW;
   const long total = tiles * s.B * s.H;
   const long grid = ((total + 7) / 8) * 8;
-  hipLaunchKernelGGL((fwd_mfma_kernel<D, G, FORM>), dim3(static_cast<unsigned>(grid)), dim3(kThreads), 0,
+  hipLaunchKernelGGL((fwd_mfma_kernel<D, G, FORM, BIAS>), dim3(static_cast<unsigned>(grid)), dim3(kThreads), 0,
                      st, s, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                      static_cast<const uint16_t*>(kp), static_cast<const uint16_t*>(v),
                      static_cast<const uint16_t*>(vp), static_cast<uint16_t*>(out), lse);
@@ -596,19 +600,26 @@ bool mfma_fwd_supported(const Shape& s) {
   return s.dtype == 1 && (s.D == 64 || s.D == 128) && s.w2 <= (s.form == 1 ? 32 : 64) && fits;
 }
 
-hipError_t mfma_fwd(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
-                    const void* vp, void* out, float* lse, hipStream_t st) {
+template <bool BIAS>
+hipError_t mfma_fwd_b(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
+                      const void* vp, void* out, float* lse, hipStream_t st) {
   const int G = s.w2 <= 32 ? 1 : 2;
   if (s.form == 1) {  // determinant logits: w2 <= 32 only (mfma_fwd_supported)
     if (G != 1) return hipErrorInvalidValue;
-    return s.D == 128 ? launch<128, 1, 1>(s, q, k, kp, v, vp, out, lse, st)
-                      : launch<64, 1, 1>(s, q, k, kp, v, vp, out, lse, st);
+    return s.D == 128 ? launch<128, 1, 1, BIAS>(s, q, k, kp, v, vp, out, lse, st)
+                      : launch<64, 1, 1, BIAS>(s, q, k, kp, v, vp, out, lse, st);
   }
-  if (s.D == 128) return G == 1 ? launch<128, 1>(s, q, k, kp, v, vp, out, lse, st)
-                                : launch<128, 2>(s, q, k, kp, v, vp, out, lse, st);
-  if (s.D == 64) return G == 1 ? launch<64, 1>(s, q, k, kp, v, vp, out, lse, st)
-                               : launch<64, 2>(s, q, k, kp, v, vp, out, lse, st);
+  if (s.D == 128) return G == 1 ? launch<128, 1, 0, BIAS>(s, q, k, kp, v, vp, out, lse, st)
+                                : launch<128, 2, 0, BIAS>(s, q, k, kp, v, vp, out, lse, st);
+  if (s.D == 64) return G == 1 ? launch<64, 1, 0, BIAS>(s, q, k, kp, v, vp, out, lse, st)
+                               : launch<64, 2, 0, BIAS>(s, q, k, kp, v, vp, out, lse, st);
   return hipErrorInvalidValue;
+}
+
+hipError_t mfma_fwd(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
+                    const void* vp, void* out, float* lse, hipStream_t st) {
+  return s.kp_bias != 0.f || s.vp_bias != 0.f ? mfma_fwd_b<true>(s, q, k, kp, v, vp, out, lse, st)
+                                              : mfma_fwd_b<false>(s, q, k, kp, v, vp, out, lse, st);
 }
 
 }  // namespace sa

@@ -111,11 +111,13 @@ struct Rows {
   __device__ size_t at(int n) const { return base + static_cast<size_t>(n) * stride; }
 };
 
+// Operands x and y are read with the constant bx / by added to every element
+// (the K' / V' bias constants; 0 for the other tensors).
 template <typename T, int D>
-__device__ __forceinline__ float tri(const float* a, const T* x, const T* y) {
+__device__ __forceinline__ float tri(const float* a, const T* x, float bx, const T* y, float by) {
   float s = 0.f;
 #pragma unroll 8
-  for (int d = 0; d < D; ++d) s += a[d] * ld(x + d) * ld(y + d);
+  for (int d = 0; d < D; ++d) s += a[d] * (ld(x + d) + bx) * (ld(y + d) + by);
   return s;
 }
 
@@ -123,11 +125,11 @@ __device__ __forceinline__ float tri(const float* a, const T* x, const T* y) {
 // chunks c of det([a_c; x_c; y_c]) = a_c . (x_c cross y_c); the D mod 3
 // trailing components take no part.
 template <typename T, int D>
-__device__ __forceinline__ float tri_det(const float* a, const T* x, const T* y) {
+__device__ __forceinline__ float tri_det(const float* a, const T* x, float bx, const T* y, float by) {
   float s = 0.f;
   for (int c = 0; c + 2 < D; c += 3) {
-    const float x0 = ld(x + c), x1 = ld(x + c + 1), x2 = ld(x + c + 2);
-    const float y0 = ld(y + c), y1 = ld(y + c + 1), y2 = ld(y + c + 2);
+    const float x0 = ld(x + c) + bx, x1 = ld(x + c + 1) + bx, x2 = ld(x + c + 2) + bx;
+    const float y0 = ld(y + c) + by, y1 = ld(y + c + 1) + by, y2 = ld(y + c + 2) + by;
     s += a[c] * (x1 * y2 - x2 * y1) + a[c + 1] * (x2 * y0 - x0 * y2) + a[c + 2] * (x0 * y1 - x1 * y0);
   }
   return s;
@@ -136,25 +138,26 @@ __device__ __forceinline__ float tri_det(const float* a, const T* x, const T* y)
 // Logit of form FORM (0: trilinear, Eq. (3d-attention); 1: determinant) with
 // operands in the order (a, x, y) of the form.
 template <typename T, int D, int FORM>
-__device__ __forceinline__ float logit3(const float* a, const T* x, const T* y) {
+__device__ __forceinline__ float logit3(const float* a, const T* x, float bx, const T* y, float by) {
   if constexpr (FORM == 0)
-    return tri<T, D>(a, x, y);
+    return tri<T, D>(a, x, bx, y, by);
   else
-    return tri_det<T, D>(a, x, y);
+    return tri_det<T, D>(a, x, bx, y, by);
 }
 
 // acc += w * dA/da for A = form(a, x, y): x o y (trilinear) or, per chunk,
 // x cross y (determinant; trailing components get nothing).
 template <typename T, int D, int FORM>
-__device__ __forceinline__ void add_partial(float (&acc)[D], float w, const T* x, const T* y) {
+__device__ __forceinline__ void add_partial(float (&acc)[D], float w, const T* x, float bx, const T* y,
+                                            float by) {
   if constexpr (FORM == 0) {
 #pragma unroll
-    for (int d = 0; d < D; ++d) acc[d] += w * ld(x + d) * ld(y + d);
+    for (int d = 0; d < D; ++d) acc[d] += w * (ld(x + d) + bx) * (ld(y + d) + by);
   } else {
 #pragma unroll
     for (int c = 0; c + 2 < D; c += 3) {
-      const float x0 = ld(x + c), x1 = ld(x + c + 1), x2 = ld(x + c + 2);
-      const float y0 = ld(y + c), y1 = ld(y + c + 1), y2 = ld(y + c + 2);
+      const float x0 = ld(x + c) + bx, x1 = ld(x + c + 1) + bx, x2 = ld(x + c + 2) + bx;
+      const float y0 = ld(y + c) + by, y1 = ld(y + c + 1) + by, y2 = ld(y + c + 2) + by;
       acc[c] += w * (x1 * y2 - x2 * y1);
       acc[c + 1] += w * (x2 * y0 - x0 * y2);
       acc[c + 2] += w * (x0 * y1 - x1 * y0);
@@ -188,7 +191,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(Shape s, const T* __restr
   float m = -INFINITY;
   for (int p = threadIdx.x; p < np; p += kThreads) {
     const int j = j0 + p / nk, kk = k0 + p % nk;
-    m = fmaxf(m, logit3<T, D, FORM>(qs, k + kvr.at(j), kp + kvr.at(kk)));
+    m = fmaxf(m, logit3<T, D, FORM>(qs, k + kvr.at(j), 0.f, kp + kvr.at(kk), s.kp_bias));
   }
   m = block_max(m, sred);
 
@@ -198,12 +201,12 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(Shape s, const T* __restr
   for (int d = 0; d < D; ++d) acc[d] = 0.f;
   for (int p = threadIdx.x; p < np; p += kThreads) {
     const int j = j0 + p / nk, kk = k0 + p % nk;
-    const float e = expf(logit3<T, D, FORM>(qs, k + kvr.at(j), kp + kvr.at(kk)) - m);
+    const float e = expf(logit3<T, D, FORM>(qs, k + kvr.at(j), 0.f, kp + kvr.at(kk), s.kp_bias) - m);
     l += e;
     const T* vj = v + kvr.at(j);
     const T* vk = vp + kvr.at(kk);
 #pragma unroll
-    for (int d = 0; d < D; ++d) acc[d] += e * ld(vj + d) * ld(vk + d);
+    for (int d = 0; d < D; ++d) acc[d] += e * ld(vj + d) * (ld(vk + d) + s.vp_bias);
   }
   l = block_sum(l, sred);
   const float o = block_sum_vec<D>(acc, red);
@@ -262,10 +265,10 @@ __global__ __launch_bounds__(kThreads) void dq_kernel(Shape s, const T* __restri
     const int j = j0 + p / nk, kk = k0 + p % nk;
     const T* kj = k + rows.at(j);
     const T* kk_ = kp + rows.at(kk);
-    const float pr = expf(logit3<T, D, FORM>(qs, kj, kk_) - lse_i);
-    const float dp = tri<T, D>(ds_, v + rows.at(j), vp + rows.at(kk));
+    const float pr = expf(logit3<T, D, FORM>(qs, kj, 0.f, kk_, s.kp_bias) - lse_i);
+    const float dp = tri<T, D>(ds_, v + rows.at(j), 0.f, vp + rows.at(kk), s.vp_bias);
     const float dsv = pr * (dp - delta_i);
-    add_partial<T, D, FORM>(acc, dsv, kj, kk_);
+    add_partial<T, D, FORM>(acc, dsv, kj, 0.f, kk_, s.kp_bias);
   }
   const float g = block_sum_vec<D>(acc, red);
   if (threadIdx.x < D) st(dq + rows.at(i) + threadIdx.x, g * s.scale);
@@ -292,9 +295,13 @@ __global__ __launch_bounds__(kThreads) void keyside_kernel(
   __shared__ float kr[D];
   __shared__ float vr[D];
   __shared__ float red[kWaves * D];
+  // Bias constants: K' / V' are the self operands of SIDE 1, the other
+  // operands of SIDE 0.
+  const float bks = SIDE == 1 ? s.kp_bias : 0.f, bvs = SIDE == 1 ? s.vp_bias : 0.f;
+  const float bko = SIDE == 0 ? s.kp_bias : 0.f, bvo = SIDE == 0 ? s.vp_bias : 0.f;
   if (threadIdx.x < D) {
-    kr[threadIdx.x] = ld(kself + rows.at(r) + threadIdx.x) * s.scale;
-    vr[threadIdx.x] = ld(vself + rows.at(r) + threadIdx.x);
+    kr[threadIdx.x] = (ld(kself + rows.at(r) + threadIdx.x) + bks) * s.scale;
+    vr[threadIdx.x] = ld(vself + rows.at(r) + threadIdx.x) + bvs;
   }
   __syncthreads();
   const int na = min(wself, s.N - r);
@@ -312,19 +319,19 @@ __global__ __launch_bounds__(kThreads) void keyside_kernel(
     const T* ko = kother + rows.at(o);
     const T* doi = dout + rows.at(i);
     const T* vo = vother + rows.at(o);
-    const float a = FORM == 0 || SIDE == 1 ? logit3<T, D, FORM>(kr, qi, ko)
-                                           : logit3<T, D, FORM>(kr, ko, qi);
+    const float a = FORM == 0 || SIDE == 1 ? logit3<T, D, FORM>(kr, qi, 0.f, ko, bko)
+                                           : logit3<T, D, FORM>(kr, ko, bko, qi, 0.f);
     const float pr = expf(a - lse[stat + i]);
     if (MODE == 0) {
-      const float dp = tri<T, D>(vr, doi, vo);
+      const float dp = tri<T, D>(vr, doi, 0.f, vo, bvo);
       const float dsv = pr * (dp - delta[stat + i]);
       if (FORM == 0 || SIDE == 1)
-        add_partial<T, D, FORM>(acc, dsv, qi, ko);
+        add_partial<T, D, FORM>(acc, dsv, qi, 0.f, ko, bko);
       else
-        add_partial<T, D, FORM>(acc, dsv, ko, qi);
+        add_partial<T, D, FORM>(acc, dsv, ko, bko, qi, 0.f);
     } else {
 #pragma unroll
-      for (int d = 0; d < D; ++d) acc[d] += pr * ld(doi + d) * ld(vo + d);
+      for (int d = 0; d < D; ++d) acc[d] += pr * ld(doi + d) * (ld(vo + d) + bvo);
     }
   }
   const float g = block_sum_vec<D>(acc, red);

@@ -41,6 +41,16 @@ __device__ __forceinline__ unsigned pack_bf16x2(float lo, float hi) {
 __device__ __forceinline__ float bf16_lo(unsigned x) { return __uint_as_float(x << 16); }
 __device__ __forceinline__ float bf16_hi(unsigned x) { return __uint_as_float(x & 0xffff0000u); }
 
+// x + b for kernels instantiated with operand bias constants, x otherwise (so
+// the plain instantiation carries no extra instruction).
+template <bool BIAS>
+__device__ __forceinline__ float plus_bias(float x, float b) {
+  if constexpr (BIAS)
+    return x + b;
+  else
+    return x;
+}
+
 // Value of `x` held by lane (lane ^ 32): v_permlane32_swap exchanges the upper
 // half of its first operand with the lower half of its second.
 __device__ __forceinline__ float swap_halves(float x) {

@@ -27,6 +27,10 @@ struct Shape {
   // limit). The MFMA backward plan lengthens its query chunks until its
   // workspace fits (fewer chunk-boundary partial sums).
   size_t ws_cap;
+  // Constants added to every element of K' and V' after loading (the
+  // K2_BIAS / V2_BIAS constants of the paper's Appendix B kernel); 0 for the
+  // plain operation. Masked pairs stay excluded whatever the bias.
+  float kp_bias, vp_bias;
 };
 
 // bf16 is carried as raw 16-bit patterns (uint16_t) in every kernel.

@@ -9,7 +9,10 @@ Tolerances (the bar each parity test asserts), with the arithmetic behind them:
   query, the relative rounding error stays near 1e-6.
 * bf16 data, forward: max |O - O_ref| <= 2e-2 (absolute) and, because |O| is
   itself only ~1e-2 at the benchmark shapes, also the normwise
-  ||O - O_ref|| / ||O_ref|| <= 1e-2. The kernels round the modulated query
+  ||O - O_ref|| / ||O_ref|| <= 1e-2. Where max |O_ref| exceeds 1 (a query
+  seeing a single pair has O_i = v_i o v'_i; constants added to V' scale all
+  of O) the absolute bar is 2e-2 * max |O_ref|: bf16 resolves |x| in [8, 16)
+  only to 0.0625, so no bf16 result can meet a fixed 2e-2 there. The kernels round the modulated query
   q_i o k'_k, the probabilities P and the output to bf16 (unit roundoff
   2^-9 = 2e-3 each), which gives a normwise error of a few 1e-3.
   LSE (fp32 output): |LSE - ref| <= 2e-2; the bf16 rounding of the modulated
@@ -96,7 +99,8 @@ def check_forward(o, lse, o_ref, lse_ref, dtype, label=""):
     if dtype == "fp32":
         assert eo["max_rel"] <= t["o_maxrel"], f"{label}: O {eo}"
     else:
-        assert eo["max_abs"] <= t["o_abs"], f"{label}: O {eo}"
+        o_scale = max(1.0, float(np.max(np.abs(o_ref)))) if np.size(o_ref) else 1.0
+        assert eo["max_abs"] <= t["o_abs"] * o_scale, f"{label}: O {eo} (bar scaled by {o_scale:.3g})"
         assert eo["norm_rel"] <= t["o_norm"], f"{label}: O {eo}"
     assert el["max_abs"] <= t["lse_abs"], f"{label}: LSE {el}"
     return eo, el
@@ -261,3 +265,25 @@ def sampled_backward_check(inputs, grads_gpu, w1, w2, scale, dtype, heads, q_row
             ref[t].append(g_ref[t][rows])
     return check_grads([np.concatenate(x) for x in got], [np.concatenate(x) for x in ref],
                        dtype, label)
+
+
+class OracleAttention(torch.autograd.Function):
+    """The oracle's attention as a CPU float64 autograd function, for references
+    of modules built around the kernels: forward = oracle.forward_batched,
+    backward = oracle.backward_batched (tensors [B, N, H, D] float64 on the CPU;
+    K' and V' enter with the bias constants added, as the kernels take them)."""
+
+    @staticmethod
+    def forward(ctx, q, k, kp, v, vp, w1, w2, scale, kp_bias, vp_bias):
+        arrs = [x.detach().numpy() for x in (q, k, kp, v, vp)]
+        arrs[2] = arrs[2] + kp_bias
+        arrs[4] = arrs[4] + vp_bias
+        o, _ = orc.forward_batched(*arrs, w1, w2, scale)
+        ctx.arrs, ctx.cfg = arrs, (w1, w2, scale)
+        return torch.from_numpy(o)
+
+    @staticmethod
+    def backward(ctx, do):
+        w1, w2, scale = ctx.cfg
+        g = orc.backward_batched(*ctx.arrs, do.detach().numpy(), w1, w2, scale)
+        return (*(torch.from_numpy(x) for x in g), None, None, None, None, None)

@@ -51,6 +51,7 @@ def test_header_declares_the_expected_entry_points():
         "simplicial_attn_error_string", "simplicial_attn_abi_version", "simplicial_attn_path_name",
         "simplicial_attn_bwd_preprocess", "simplicial_attn_bwd_query_side",
         "simplicial_attn_bwd_key_side", "simplicial_attn_bwd_noalloc",
+        "simplicial_attn_fwd_biased", "simplicial_attn_bwd_biased",
     ])
 
 
@@ -258,3 +259,27 @@ def test_path_names(lib):
     assert f(2, 1, 128, 1, 64, 16, 8, 0) == "invalid"
     for which in (0, 1):
         assert f(which, 1, 32768, 16, 128, 512, 32, 1) in ("generic", "mfma_bf16")
+
+
+@only_without_gpu
+def test_biased_entry_points_reject_invalid_arguments(lib):
+    f32 = ctypes.c_float
+
+    def fwd(kb=0.5, vb=0.5, ptrs=None, D=128):
+        ptrs = ptrs or [A] * 7
+        return lib.simplicial_attn_fwd_biased(*[ctypes.c_void_p(p) for p in ptrs], 1, 64, 2, D, 16, 8,
+                                              f32(0.1), f32(kb), f32(vb), 1, None)
+
+    def bwd(kb=0.5, vb=0.5, ws=1 << 30, ptrs=None):
+        ptrs = ptrs or [A] * 14
+        return lib.simplicial_attn_bwd_biased(*[ctypes.c_void_p(p) for p in ptrs], ctypes.c_size_t(ws),
+                                              1, 64, 2, 128, 16, 8, f32(0.1), f32(kb), f32(vb), 1, None)
+
+    for kb, vb in [(float("nan"), 0.0), (0.0, float("inf")), (float("-inf"), 1.0)]:
+        assert fwd(kb, vb) == 1
+        assert bwd(kb, vb) == 1
+    ptrs = [A] * 7
+    ptrs[3] = 0
+    assert fwd(ptrs=ptrs) == 1
+    assert fwd(D=48) == 2
+    assert bwd(ws=16) == 3
