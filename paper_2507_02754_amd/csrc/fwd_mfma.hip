@@ -30,6 +30,8 @@
 //     P(n), while the matrix cores compute S(n+1) from K fragments that were
 //     read one iteration earlier,
 //   - accumulates P(n) V(n) while the K fragments of block n+2 are read.
+// The last block's iteration is a separate copy without the products of a
+// block after it (which would be discarded).
 // With w2 <= 32 the prologue brings the workgroup's k' and q rows into a
 // staging tile with the same LDS-DMA loads and forms q~ from LDS (one 16-byte
 // load per row instead of per-wavefront register loads of overlapping rows),
@@ -384,8 +386,9 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
   for (int t = 0; t < NT; ++t) kf[t] = kfrag(IC<1>{}, t);
 
   const bf16x2_t ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
-  auto iteration = [&](auto SC, int blk) __attribute__((always_inline)) {
+  auto iteration = [&](auto SC, int blk, auto LASTC) __attribute__((always_inline)) {
     constexpr int S = decltype(SC)::value;  // ring stage of block blk
+    constexpr bool LAST = decltype(LASTC)::value;  // blk == nb - 1: no S(blk + 1)
     constexpr int cur = S & 1, nxt = cur ^ 1;
     // K(blk + 2) (loaded in iteration blk - 2) and V(blk) (iteration
     // blk - 3) must be in LDS for every wavefront: wait until at most the
@@ -433,7 +436,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
     // other one on its SIMD while that one is at the barrier or issuing its
     // loads (wavefront priority 1; back to 0 at the end of the block).
     __builtin_amdgcn_s_setprio(1);
-    logits(sc[nxt]);
+    if constexpr (!LAST) logits(sc[nxt]);
     u32x4_t pf[2];
     float lb = 0.f;
     auto form_p = [&]() __attribute__((always_inline)) {
@@ -473,14 +476,23 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
       for (int dt = 0; dt < NDT; ++dt) acc[dt] = mfma32(vf[u][dt], pf[u], acc[dt]);
     // K fragments of block blk + 2 (stage written in iteration blk - 1).
 #pragma unroll
-    for (int t = 0; t < NT; ++t) kf[t] = kfrag(IC<(S + 2) % kStages>{}, t);
+    for (int t = 0; t < NT; ++t)
+      if constexpr (!LAST) kf[t] = kfrag(IC<(S + 2) % kStages>{}, t);
     __builtin_amdgcn_s_setprio(0);
   };
-  for (int b0 = 0; b0 < nb; b0 += kStages) {
-    iteration(IC<0>{}, b0);
-    if (b0 + 1 < nb) iteration(IC<1>{}, b0 + 1);
-    if (b0 + 2 < nb) iteration(IC<2>{}, b0 + 2);
-    if (b0 + 3 < nb) iteration(IC<3>{}, b0 + 3);
+  // Blocks 0 .. nb-2, then the last block without the products of a next one.
+  const int nmain = nb - 1;
+  for (int b0 = 0; b0 < nmain; b0 += kStages) {
+    iteration(IC<0>{}, b0, std::false_type{});
+    if (b0 + 1 < nmain) iteration(IC<1>{}, b0 + 1, std::false_type{});
+    if (b0 + 2 < nmain) iteration(IC<2>{}, b0 + 2, std::false_type{});
+    if (b0 + 3 < nmain) iteration(IC<3>{}, b0 + 3, std::false_type{});
+  }
+  switch (nmain & 3) {
+    case 0: iteration(IC<0>{}, nmain, std::true_type{}); break;
+    case 1: iteration(IC<1>{}, nmain, std::true_type{}); break;
+    case 2: iteration(IC<2>{}, nmain, std::true_type{}); break;
+    default: iteration(IC<3>{}, nmain, std::true_type{}); break;
   }
   // ---- epilogue: merge the k-rows of each query (log-sum-exp), apply v'_k ----
   // v'_k of this lane's row in the accumulator layout (d = 32 dt + 8 (v/4) +
