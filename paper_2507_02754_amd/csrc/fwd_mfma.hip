@@ -77,7 +77,12 @@ __device__ __forceinline__ void wait_vmcnt() {
 // FORM 0: trilinear logits (Section 4); FORM 1: determinant logits (Section 5,
 // w2 <= 32 only), which differ only in the modulated query formed below.
 // BIAS: K' and V' values get the constants s.kp_bias / s.vp_bias added on load.
-template <int D, int G, int FORM, bool BIAS>
+// HF (grouped-query attention with a multiple of 4 query heads per K-side
+// head, w2 <= 32): the 4 wavefronts take 4 query heads of one K-side head at
+// the same position i instead of 4 consecutive positions of one head, so they
+// share one key window: ceil(w1 / 32) blocks with no masked columns away from
+// the start of the sequence (the query-head tiling of Section 6).
+template <int D, int G, int FORM, bool BIAS, bool HF>
 __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const uint16_t* __restrict__ q,
                                                                const uint16_t* __restrict__ k,
                                                                const uint16_t* __restrict__ kp,
@@ -114,28 +119,46 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
   // XCD-aware tile order: hardware deals workgroups round-robin over the 8
   // XCDs; remap so each XCD walks a contiguous run of tiles of one head and
   // the overlapping K/V windows of neighbouring tiles hit the same L2.
-  const int tiles = (s.N + QW - 1) / QW;
-  const int total = tiles * s.B * s.H;
-  const int per_xcd = (total + 7) / 8;
-  const int logical = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
-  if (logical >= total) return;
-  const int bh = logical / tiles;
-  const int tile = logical - bh * tiles;
-  const int b = bh / s.H, hh = bh - b * s.H;
-
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, c = lane & 31, h = lane >> 5;
   const int qs = wave / G, g = wave % G;
+  static_assert(!HF || G == 1, "head-folded tiles take one wavefront per query");
   // Q-side tensors (q, out) have H heads; K-side ones (k, k', v, v') Hkv,
-  // query head hh reading K-side head hh / (H / Hkv) (grouped-query attention;
-  // Hkv == H otherwise).
+  // query head hh reading K-side head hk = hh / (H / Hkv) (grouped-query
+  // attention; Hkv == H otherwise). A tile is QW consecutive queries of one
+  // head, or (HF) QW query heads hq0 .. hq0 + QW - 1 of one K-side head at one
+  // position; tiles sharing K / V rows are adjacent in the XCD order below.
+  int b, hk, hh, i0, hq0 = 0;
+  {
+    const int per_bh = HF ? s.N * (s.H / s.Hkv / QW) : (s.N + QW - 1) / QW;
+    const int total = per_bh * s.B * (HF ? s.Hkv : s.H);
+    const int per_xcd = (total + 7) / 8;
+    const int logical = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+    if (logical >= total) return;
+    const int bhx = logical / per_bh;
+    const int tile = logical - bhx * per_bh;
+    if constexpr (HF) {
+      const int quads = s.H / s.Hkv / QW;
+      b = bhx / s.Hkv;
+      hk = bhx - b * s.Hkv;
+      i0 = tile / quads;
+      hq0 = hk * (s.H / s.Hkv) + (tile - i0 * quads) * QW;
+      hh = hq0 + qs;
+    } else {
+      b = bhx / s.H;
+      hh = bhx - b * s.H;
+      hk = hh / (s.H / s.Hkv);
+      i0 = tile * QW;
+    }
+  }
+  const int bh = b * s.H + hh;  // query head row of lse
+  const int qoff = HF ? 0 : qs;  // position of this wavefront's query after i0
   const size_t rs = static_cast<size_t>(s.H) * D;
   const size_t base = (static_cast<size_t>(b) * s.N * s.H + hh) * D;
   const size_t rskv = static_cast<size_t>(s.Hkv) * D;
-  const size_t kvbase = (static_cast<size_t>(b) * s.N * s.Hkv + hh / (s.H / s.Hkv)) * D;
+  const size_t kvbase = (static_cast<size_t>(b) * s.N * s.Hkv + hk) * D;
   const int N = s.N, w1 = s.w1, w2 = s.w2;
-  const int i0 = tile * QW;
-  const int i = i0 + qs;
+  const int i = i0 + qoff;
   const bool qvalid = i < N;
 
   const int kk = i - W2P + 1 + 32 * g + c;
@@ -143,7 +166,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
   const float qscale = s.scale * kLog2e;
 
   const int jlo = i0 - w1 + 1;
-  const int nb = (w1 + QW - 1 + 31) / 32;
+  const int nb = (w1 + (HF ? 0 : QW - 1) + 31) / 32;
   const int rsbq = static_cast<int>(rs) * 2;     // bytes between rows of q, out
   const int rsb = static_cast<int>(rskv) * 2;    // bytes between rows of k, k', v, v'
   const __amdgpu_buffer_rsrc_t rk = make_rsrc(k + kvbase, head_bytes(N, rsb, D));
@@ -242,10 +265,19 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
     // first one on. Blocks past the window only cost the loads.
 #pragma unroll
     for (int x = wave; x < KI + 1; x += kWaves) {
-      if (x < KI)
+      if (x < KI) {
         stage(rkp, rsb, x, kk0);
-      else
+      } else if constexpr (HF) {
+        // q rows of the QW heads at position i0: contiguous, QW * 2D bytes
+        // (a resource of exactly that size zero-fills the rest of the load).
+        const __amdgpu_buffer_rsrc_t rqh = make_rsrc(q + (static_cast<size_t>(b) * N + i0) * rs +
+                                                     static_cast<size_t>(hq0) * D, QW * 2 * D);
+        const int rr = lane / T::CH;
+        const int ch = (lane % T::CH) ^ ((KR + rr) % T::CH);
+        load_lds16(rqh, to_lds(stg) + 1024 * x, rr * 2 * D + 16 * ch);
+      } else {
         stage(rq, rsbq, x, i0 - KR);
+      }
     }
     load_tile(rk, kst(IC<0>{}), 0);
     load_tile(rk, kst(IC<1>{}), 1);
@@ -301,7 +333,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
     // modulated queries q~ = (scale*log2 e) * q_i o k'_k as B operands, from
     // the staged rows (local k' row qs + c, q row KR + qs); rows outside the
     // window or the sequence are zero.
-    const int rr = qs + c, rq_ = KR + qs;
+    const int rr = qoff + c, rq_ = KR + qs;
     const lds_char* krow = to_lds(stg) + rr * 2 * D;
     const lds_char* qrow = to_lds(stg) + rq_ * 2 * D;
     const unsigned keep = rowvalid ? 0xFFFFFFFFu : 0u;
@@ -422,8 +454,8 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
       for (int dt = 0; dt < NDT; ++dt) vf[u][dt] = vfrag(SC, dt, u);
 
     // Valid block-local columns of this wavefront's query.
-    const int lo = max(qs, -jlo) - 32 * blk;
-    const int hi = min(qs + w1 - 1, N - 1 - jlo) - 32 * blk;
+    const int lo = max(qoff, -jlo) - 32 * blk;
+    const int hi = min(qoff + w1 - 1, N - 1 - jlo) - 32 * blk;
     if (lo > 0 || hi < 31) {
 #pragma unroll
       for (int vv = 0; vv < 16; ++vv) {
@@ -507,7 +539,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
       wait_vmcnt<0>();
       lds_barrier_tracked();
     }
-    const int r = qs + c;
+    const int r = qoff + c;
     const lds_char* vrow = to_lds(stg) + r * 2 * D + 8 * h;
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
@@ -590,19 +622,23 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_mfma_kernel(Shape s, const ui
   }
 }
 
-template <int D, int G, int FORM = 0, bool BIAS = false>
+template <int D, int G, int FORM = 0, bool BIAS = false, bool HF = false>
 hipError_t launch(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
                   const void* vp, void* out, float* lse, hipStream_t st) {
   constexpr int QW = kWaves / G;
-  const long tiles = (s.N + QW - 1) / QW;
-  const long total = tiles * s.B * s.H;
+  const long total = HF ? static_cast<long>(s.N) * (s.H / QW) * s.B
+                        : static_cast<long>((s.N + QW - 1) / QW) * s.B * s.H;
   const long grid = ((total + 7) / 8) * 8;
-  hipLaunchKernelGGL((fwd_mfma_kernel<D, G, FORM, BIAS>), dim3(static_cast<unsigned>(grid)), dim3(kThreads), 0,
+  hipLaunchKernelGGL((fwd_mfma_kernel<D, G, FORM, BIAS, HF>), dim3(static_cast<unsigned>(grid)), dim3(kThreads), 0,
                      st, s, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                      static_cast<const uint16_t*>(kp), static_cast<const uint16_t*>(v),
                      static_cast<const uint16_t*>(vp), static_cast<uint16_t*>(out), lse);
   return hipGetLastError();
 }
+
+// Grouped-query attention with a multiple of 4 query heads per K-side head
+// takes the head-folded tiles (trilinear logits).
+bool head_folded(const Shape& s) { return s.form == 0 && s.Hkv < s.H && (s.H / s.Hkv) % kWaves == 0; }
 
 }  // namespace
 
@@ -620,6 +656,11 @@ hipError_t mfma_fwd_b(const Shape& s, const void* q, const void* k, const void* 
     if (G != 1) return hipErrorInvalidValue;
     return s.D == 128 ? launch<128, 1, 1, BIAS>(s, q, k, kp, v, vp, out, lse, st)
                       : launch<64, 1, 1, BIAS>(s, q, k, kp, v, vp, out, lse, st);
+  }
+  if constexpr (!BIAS) {
+    if (G == 1 && head_folded(s))
+      return s.D == 128 ? launch<128, 1, 0, false, true>(s, q, k, kp, v, vp, out, lse, st)
+                        : launch<64, 1, 0, false, true>(s, q, k, kp, v, vp, out, lse, st);
   }
   if (s.D == 128) return G == 1 ? launch<128, 1, 0, BIAS>(s, q, k, kp, v, vp, out, lse, st)
                                 : launch<128, 2, 0, BIAS>(s, q, k, kp, v, vp, out, lse, st);

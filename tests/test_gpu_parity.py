@@ -125,12 +125,20 @@ def test_forward_tile_runs(d, w1, w2):
 GQA = [
     # (B, H, Hkv, N, D, w1, w2, dtype)
     (1, 4, 2, 300, 128, 64, 32, "bf16"),   # MFMA path, two query heads per K-side head
-    (2, 8, 1, 200, 64, 40, 32, "bf16"),    # head_dim 64, all query heads on one K-side head
+    (2, 8, 1, 200, 64, 40, 32, "bf16"),    # head_dim 64, all query heads on one K-side head (head-folded)
     (1, 4, 2, 333, 128, 96, 64, "bf16"),   # w2 = 64 (two wavefronts per query)
     (1, 6, 3, 100, 64, 7, 5, "fp32"),      # generic path
     (1, 3, 3, 129, 128, 33, 7, "bf16"),    # Hkv == H
     (1, 64, 1, 96, 64, 40, 32, "bf16"),    # 64 query heads per K-side head (Section 6's ratio)
+    (1, 8, 2, 257, 128, 100, 17, "bf16"),  # head-folded, w1 and w2 not multiples of 32
+    (2, 16, 1, 70, 128, 512, 32, "bf16"),  # head-folded, windows longer than the sequence
+    (1, 4, 1, 1, 128, 512, 32, "bf16"),    # head-folded, a single query
 ]
+
+
+def _head_folded(h, hkv, d, w2, dt):
+    """Shapes the forward runs with query heads folded into one tile."""
+    return dt == "bf16" and d in (64, 128) and w2 <= 32 and hkv < h and (h // hkv) % 4 == 0
 
 
 def _gqa_inputs(b, h, hkv, n, d, dt, seed):
@@ -145,8 +153,10 @@ def _gqa_inputs(b, h, hkv, n, d, dt, seed):
 @pytest.mark.parametrize("shape", GQA, ids=[str(s) for s in GQA])
 def test_gqa_forward(shape):
     """Grouped-query forward against the oracle (query head h reads K-side head
-    h // (H // Hkv)), and bit for bit against the plain forward on K, K', V, V'
-    repeated per query head."""
+    h // (H // Hkv)), and, where query heads are not folded into one tile, bit
+    for bit against the plain forward on K, K', V, V' repeated per query head
+    (folded tiles walk each query's own key window, a different block
+    alignment, so only the oracle comparison applies)."""
     from paper_2507_02754_amd import simplicial_attn_fwd_gqa
 
     b, h, hkv, n, d, w1, w2, dt = shape
@@ -161,7 +171,8 @@ def test_gqa_forward(shape):
     rep = [x.repeat_interleave(h // hkv, dim=2).contiguous() for x in kv]
     o_m, lse_m = simplicial_attn_fwd(q.cuda(), *(x.cuda() for x in rep), w1, w2, scale)
     torch.cuda.synchronize()
-    assert torch.equal(o, o_m) and torch.equal(lse, lse_m), "GQA forward differs from repeated K/V"
+    if not _head_folded(h, hkv, d, w2, dt):
+        assert torch.equal(o, o_m) and torch.equal(lse, lse_m), "GQA forward differs from repeated K/V"
     ref = P.gqa_oracle_forward(q, kv, w1, w2, scale)
     o_ref = np.stack([np.stack([ref[(bb, hh)][0] for hh in range(h)], axis=1) for bb in range(b)])
     lse_ref = np.stack([np.stack([ref[(bb, hh)][1] for hh in range(h)]) for bb in range(b)])
@@ -188,7 +199,22 @@ def test_gqa_backward(shape):
     for name, g1, g2 in zip(P.GRAD_NAMES, grads, comp):
         assert torch.equal(g1, g2), f"{name}: GQA backward differs from the per-head composite"
     dq_ref, dkv_ref = P.gqa_oracle_backward(q, kv, do, w1, w2, scale)
-    P.check_grads([P.to64(g_) for g_ in grads], [dq_ref, *dkv_ref], dt, f"gqa backward {shape}")
+    got = [P.to64(g_) for g_ in grads]
+    if n == 1:
+        # one pair per query: dQ, dK, dK' vanish exactly; on the GPU each query
+        # head's term is off by at most the operand-rounding error of
+        # check_single_pair_grads, and the K-side gradients sum H / Hkv of them
+        P.check_grads(got[3:], dkv_ref[2:], dt, f"gqa backward {shape} dv")
+        g = h // hkv
+        q64, do64 = q.double().numpy(), do.double().numpy()
+        k64, kp64, v64, vp64 = (x.double().numpy().repeat(g, axis=2) for x in kv)
+        eps = 2.0 ** -8 * np.abs(do64 * v64 * vp64).sum(axis=-1, keepdims=True)
+        terms = [2 * scale * eps * np.abs(x * y) for x, y in [(k64, kp64), (q64, kp64), (q64, k64)]]
+        bounds = [terms[0]] + [t.reshape(b, n, hkv, g, d).sum(axis=3) for t in terms[1:]]
+        for name, g_, bd in zip(("dq", "dk", "dkp"), got[:3], bounds):
+            assert np.all(np.abs(g_) <= bd + 1e-6), (name, float(np.max(np.abs(g_) - bd)))
+    else:
+        P.check_grads(got, [dq_ref, *dkv_ref], dt, f"gqa backward {shape}")
 
 
 def test_gqa_backward_full_size_sampled():
