@@ -134,6 +134,7 @@ def main():
                                       simplicial_attn_fwd_gqa, simplicial_attn_bwd_gqa,
                                       simplicial_attn_bwd_gqa_workspace_size,
                                       simplicial_attn_det_bwd, simplicial_attn_det_fwd,
+                                      simplicial_attn_det_bwd_workspace_size,
                                       simplicial_attn_path_name)
     from paper_2507_02754_amd.workloads import WORKLOADS, make_inputs
 
@@ -301,14 +302,15 @@ def main():
                          "step_tflops": round((fwd_flops + bwd_flops) / ((gf + gb) * 1e-3) / 1e12, 2)}
         del kv, gkv, gws
     if args.det:
-        # Determinant logits (forward on the MFMA kernel, backward on the plain
-        # fp32 kernels): timed on a 4096-token sequence with the windows and
-        # head shape of the main workload.
+        # Determinant logits (forward and backward on the MFMA kernels): timed
+        # on a 4096-token sequence with the windows and head shape of the main
+        # workload.
         db, dh, dn = 1, 16, 4096
         g = torch.Generator(device="cpu").manual_seed(11)
         dq_, dk_, dkp_, dv_, dvp_, ddo = (torch.randn((db, dn, dh, w.D), generator=g)
                                           .to(w.torch_dtype).to(dev) for _ in range(6))
-        dws = torch.empty(simplicial_attn_bwd_workspace_size(db, dn, dh, w.D, w.w1, w.w2, w.torch_dtype),
+        dws = torch.empty(simplicial_attn_det_bwd_workspace_size(db, dn, dh, w.D, w.w1, w.w2,
+                                                                 w.torch_dtype),
                           dtype=torch.uint8, device=dev)
         de = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
         dsteps = 3
@@ -337,7 +339,7 @@ def main():
                          "step_ms": round(whole, 3), "fwd_ms": round(t_f.elapsed_time(t_b), 3),
                          "bwd_ms": round(t_b.elapsed_time(t_e), 3),
                          "nominal_tflops": round(16 * dunit / (whole * 1e-3) / 1e12, 2),
-                         "kernels": "forward: MFMA kernel (w2 <= 32); backward: plain fp32 kernels"}
+                         "kernels": "forward and backward: MFMA kernels (w2 <= 32)"}
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(w, inputs_cpu, args.cpu_seconds)

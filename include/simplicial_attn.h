@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define SIMPLICIAL_ATTN_ABI_VERSION 4
+#define SIMPLICIAL_ATTN_ABI_VERSION 5
 
 #define SA_DTYPE_F32 0
 #define SA_DTYPE_BF16 1
@@ -174,16 +174,23 @@ int simplicial_attn_bwd_noalloc(const void* q, const void* k, const void* kp, co
  *   A_ijk = scale * sum_l det([q_i^(l); k_j^(l); k'_k^(l)])
  * over the 3-component chunks l = 0 .. floor(D/3) - 1 (components 3l .. 3l+2);
  * for D not a multiple of 3 the D mod 3 trailing components enter no logit and
- * get zero dQ, dK, dK'. Softmax, output, windows, arguments, layouts, workspace
- * (simplicial_attn_bwd_workspace_size) and errors are those of
- * simplicial_attn_fwd / simplicial_attn_bwd. Both run on the plain fp32
- * kernels (bf16 data is converted on load and rounded on store) for every
- * supported shape.
+ * get zero dQ, dK, dK'. Softmax, output, windows, arguments, layouts and
+ * errors are those of simplicial_attn_fwd / simplicial_attn_bwd; the backward
+ * workspace is at least simplicial_attn_det_bwd_workspace_size() bytes. Eq.
+ * (logits) carries no scale factor: scale = 1 is the paper's form.
+ * Kernels: for bf16 data with D in {64, 128} and w2 <= 32 both run on the MFMA
+ * kernels (the modulated query of the trilinear kernels is formed as the
+ * chunkwise cross product k'_k x q_i; the backward's workspace then also
+ * holds the query side's fp32 dQ~ rows, 4 * 32 * D bytes per query and head,
+ * from which a separate kernel forms dQ and dK'); every other shape runs on
+ * the plain fp32 kernels.
  */
 int simplicial_attn_det_fwd(const void* q, const void* k, const void* kp, const void* v,
                             const void* vp, void* out, float* lse, int64_t B, int64_t N, int64_t H,
                             int64_t D, int32_t w1, int32_t w2, float scale, int32_t dtype,
                             void* stream);
+size_t simplicial_attn_det_bwd_workspace_size(int64_t B, int64_t N, int64_t H, int64_t D,
+                                              int32_t w1, int32_t w2, int32_t dtype);
 int simplicial_attn_det_bwd(const void* q, const void* k, const void* kp, const void* v,
                             const void* vp, const void* out, const void* dout, const float* lse,
                             void* dq, void* dk, void* dkp, void* dv, void* dvp, void* workspace,

@@ -23,6 +23,7 @@ from .binding import (  # noqa: F401
     simplicial_attn_bwd_biased,
     simplicial_attn_bwd_noalloc,
     simplicial_attn_det_bwd,
+    simplicial_attn_det_bwd_workspace_size,
     simplicial_attn_det_fwd,
     simplicial_attn_bwd_key_side,
     simplicial_attn_bwd_preprocess,

@@ -26,6 +26,7 @@ __all__ = [
     "simplicial_attn_det_fwd",
     "simplicial_attn_det_bwd",
     "simplicial_attn_bwd_gqa_workspace_size",
+    "simplicial_attn_det_bwd_workspace_size",
     "simplicial_attn_bwd_preprocess",
     "simplicial_attn_bwd_query_side",
     "simplicial_attn_bwd_key_side",
@@ -81,6 +82,8 @@ def load_library():
     lib.simplicial_attn_det_bwd.restype = ctypes.c_int
     lib.simplicial_attn_bwd_gqa.argtypes = [vp] * 14 + [ctypes.c_size_t] + [i64] * 5 + [i32, i32, f32, i32, vp]
     lib.simplicial_attn_bwd_gqa.restype = ctypes.c_int
+    lib.simplicial_attn_det_bwd_workspace_size.argtypes = [i64] * 4 + [i32, i32, i32]
+    lib.simplicial_attn_det_bwd_workspace_size.restype = ctypes.c_size_t
     lib.simplicial_attn_bwd_gqa_workspace_size.argtypes = [i64] * 5 + [i32, i32, i32]
     lib.simplicial_attn_bwd_gqa_workspace_size.restype = ctypes.c_size_t
     lib.simplicial_attn_bwd_preprocess.argtypes = [vp] * 3 + [ctypes.c_size_t] + [i64] * 4 + [i32, i32, i32, vp]
@@ -118,6 +121,11 @@ def simplicial_attn_path_name(which, B, N, H, D, w1, w2, dtype):
 def simplicial_attn_bwd_workspace_size(B, N, H, D, w1, w2, dtype):
     dt = _DTYPES.get(dtype, dtype)
     return int(load_library().simplicial_attn_bwd_workspace_size(B, N, H, D, int(w1), int(w2), int(dt)))
+
+
+def simplicial_attn_det_bwd_workspace_size(B, N, H, D, w1, w2, dtype):
+    dt = _DTYPES.get(dtype, dtype)
+    return int(load_library().simplicial_attn_det_bwd_workspace_size(B, N, H, D, int(w1), int(w2), int(dt)))
 
 
 def simplicial_attn_bwd_gqa_workspace_size(B, N, H, Hkv, D, w1, w2, dtype):
@@ -325,6 +333,10 @@ def simplicial_attn_det_bwd(q, k, kp, v, vp, out, dout, lse, w1, w2, scale=1.0, 
     """Backward with the determinant logits of Section 5 (arguments and results
     as simplicial_attn_bwd; `out`/`lse` from simplicial_attn_det_fwd; `scale`
     defaults to 1 as in the forward)."""
+    if workspace is None:
+        B, N, H, D = q.shape
+        need = simplicial_attn_det_bwd_workspace_size(B, N, H, D, w1, w2, q.dtype)
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
     return _bwd("simplicial_attn_det_bwd", q, k, kp, v, vp, out, dout, lse, w1, w2, scale, grads,
                 workspace)
 

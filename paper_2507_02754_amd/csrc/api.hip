@@ -80,6 +80,17 @@ size_t workspace_bytes_for(int64_t B, int64_t N, int64_t H, int64_t D, int32_t w
   return ((static_cast<size_t>(B * H * N) * sizeof(float)) + 255) & ~size_t(255);
 }
 
+// Backward workspace of the determinant logits: the MFMA plan (with the dQ~
+// rows) where the MFMA kernels take the shape, else Delta only.
+size_t det_workspace_bytes_for(int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1, int32_t w2,
+                               int32_t dtype) {
+  if (check_sizes(B, N, H, D, w1, w2, dtype) != SA_OK) return 0;
+  Shape s = make_shape(B, N, H, D, w1, w2, 1.0f, dtype);
+  s.form = 1;
+  if (sa::mfma_bwd_supported(s)) return sa::mfma_bwd_plan(s).bytes;
+  return ((static_cast<size_t>(B * H * N) * sizeof(float)) + 255) & ~size_t(255);
+}
+
 // Backward workspace with Hkv K-side heads: the per-head backward's workspace,
 // then (Hkv < H only) K, K', V, V' expanded to H heads and the per-query-head
 // dK, dK', dV', dV before the group sum, each [B, N, H, D] of the data type.
@@ -359,6 +370,11 @@ int simplicial_attn_det_fwd(const void* q, const void* k, const void* kp, const 
   return to_status(sa::generic_fwd(s, q, k, kp, v, vp, out, lse, st));
 }
 
+size_t simplicial_attn_det_bwd_workspace_size(int64_t B, int64_t N, int64_t H, int64_t D,
+                                              int32_t w1, int32_t w2, int32_t dtype) {
+  return det_workspace_bytes_for(B, N, H, D, w1, w2, dtype);
+}
+
 int simplicial_attn_det_bwd(const void* q, const void* k, const void* kp, const void* v,
                             const void* vp, const void* out, const void* dout, const float* lse,
                             void* dq, void* dk, void* dkp, void* dv, void* dvp, void* workspace,
@@ -366,18 +382,20 @@ int simplicial_attn_det_bwd(const void* q, const void* k, const void* kp, const 
                             int32_t w1, int32_t w2, float scale, int32_t dtype, void* stream) {
   if (check_ptrs({q, k, kp, v, vp, out, dout, lse, dq, dk, dkp, dv, dvp, workspace}) != SA_OK)
     return SA_ERR_INVALID;
-  const int rc = check_bwd(B, N, H, D, w1, w2, scale, dtype, workspace_bytes);
+  if (!isfinite(scale)) return SA_ERR_INVALID;
+  const int rc = check_sizes(B, N, H, D, w1, w2, dtype);
   if (rc != SA_OK) return rc;
+  if (workspace_bytes < det_workspace_bytes_for(B, N, H, D, w1, w2, dtype)) return SA_ERR_WORKSPACE;
   Shape s = make_shape(B, N, H, D, w1, w2, scale, dtype);
   s.form = 1;
+  const Path path = sa::mfma_bwd_supported(s) ? Path::Mfma : Path::Generic;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  int r = run_delta(s, Path::Generic, out, dout, workspace, st);
+  int r = run_delta(s, path, out, dout, workspace, st);
   if (r != SA_OK) return r;
-  r = run_stage(s, Path::Generic, BwdStage::Query, q, k, kp, v, vp, dout, lse, dq, dkp, dvp,
-                workspace, st);
+  r = run_stage(s, path, BwdStage::Query, q, k, kp, v, vp, dout, lse, dq, dkp, dvp, workspace, st);
   if (r != SA_OK) return r;
-  return run_stage(s, Path::Generic, BwdStage::Key, q, k, kp, v, vp, dout, lse, dk, dv, nullptr,
-                   workspace, st);
+  return run_stage(s, path, BwdStage::Key, q, k, kp, v, vp, dout, lse, dk, dv, nullptr, workspace,
+                   st);
 }
 
 size_t simplicial_attn_bwd_gqa_workspace_size(int64_t B, int64_t N, int64_t H, int64_t Hkv,

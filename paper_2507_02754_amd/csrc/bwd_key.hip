@@ -55,7 +55,10 @@ struct KeyLds {
 template <int X>
 using ic = std::integral_constant<int, X>;
 
-template <int D, int G, bool BIAS>
+// FORM 1: determinant logits (Section 5): role A forms q~ = k'_k x q_i per
+// 3-component chunk (unscaled), so S = q~ K^T is the determinant logit and
+// dK = scale sum_r dS_rj q~_r as for the trilinear form.
+template <int D, int G, bool BIAS, int FORM>
 __global__ __launch_bounds__(kKeyThreads, 1) void bwd_key_kernel(
     Shape s, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ kp, const uint16_t* __restrict__ v, const uint16_t* __restrict__ vp,
@@ -163,21 +166,62 @@ __global__ __launch_bounds__(kKeyThreads, 1) void bwd_key_kernel(
   // zero rows (their k' / v' load as zeros).
   u32x4_t fr[2], fm[2][IPT];
   float fb[2][IPT];
+  // FORM 1, role A: the 4-byte words on either side of each 16-byte slot of
+  // q and k' (a 3-chunk reaches 2 components into the neighbouring slots;
+  // out-of-range offsets load zeros and are not used).
+  unsigned frw[2][2], fmw[2][IPT][2];
   const float mbias = roleA ? s.kp_bias : s.vp_bias;
   auto fetch = [&](int rb, auto set) __attribute__((always_inline)) {
     constexpr int X = decltype(set)::value;
     const int i = j0 + rb / G, g = rb % G;
     fr[X] = ldbuf128(rrow, i * rsb + 16 * dc);
+    if constexpr (FORM == 1) {
+      if (roleA) {
+        frw[X][0] = ldbuf32(rrow, i * rsb + 16 * dc - 4);
+        frw[X][1] = ldbuf32(rrow, i * rsb + 16 * dc + 16);
+      }
+    }
 #pragma unroll
     for (int y = 0; y < IPT; ++y) {
       const int kk = i - W2P + 1 + 32 * g + rho + RPI * y;
       const bool inwin = kk > i - w2 && (!BIAS || kk >= 0);  // kk < 0 also loads zeros
       fm[X][y] = ldbuf128(rmod, inwin ? kk * rsb + 16 * dc : -1);
+      if constexpr (FORM == 1) {
+        if (roleA) {
+          fmw[X][y][0] = ldbuf32(rmod, inwin ? kk * rsb + 16 * dc - 4 : -1);
+          fmw[X][y][1] = ldbuf32(rmod, inwin ? kk * rsb + 16 * dc + 16 : -1);
+        }
+      }
       if constexpr (BIAS) fb[X][y] = inwin ? mbias : 0.f;
     }
   };
   auto form_put = [&](int tile_off, auto set) __attribute__((always_inline)) {
     constexpr int X = decltype(set)::value;
+    if constexpr (FORM == 1) {
+      if (roleA) {
+        // q~ = k'_k x q_i per chunk from the windows of components
+        // 8 dc - 2 .. 8 dc + 9 (rows outside the window load as zeros).
+        float fq[12];
+        fq[0] = bf16_lo(frw[X][0]), fq[1] = bf16_hi(frw[X][0]);
+        fq[10] = bf16_lo(frw[X][1]), fq[11] = bf16_hi(frw[X][1]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) fq[2 + 2 * e] = bf16_lo(fr[X][e]), fq[3 + 2 * e] = bf16_hi(fr[X][e]);
+#pragma unroll
+        for (int y = 0; y < IPT; ++y) {
+          float fk[12], cr[8];
+          fk[0] = bf16_lo(fmw[X][y][0]), fk[1] = bf16_hi(fmw[X][y][0]);
+          fk[10] = bf16_lo(fmw[X][y][1]), fk[11] = bf16_hi(fmw[X][y][1]);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) fk[2 + 2 * e] = bf16_lo(fm[X][y][e]), fk[3 + 2 * e] = bf16_hi(fm[X][y][e]);
+          cross8_rt<3 * (D / 3)>(fk, fq, dc, cr);
+          u32x4_t a4;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) a4[e] = pack_bf16x2(cr[2 * e], cr[2 * e + 1]);
+          lds_st(lds + formoff[y] + tile_off, a4);
+        }
+        return;
+      }
+    }
     float lo[4], hi[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -491,12 +535,12 @@ __global__ __launch_bounds__(kKeyThreads, 1) void bwd_key_kernel(
   }
 }
 
-template <int D, int G, bool BIAS>
+template <int D, int G, bool BIAS, int FORM = 0>
 hipError_t launch_key(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
                       const void* vp, const void* dout, const float* lse, const float* delta, void* dk,
                       void* dv, hipStream_t st) {
   const long tot = static_cast<long>((s.N + 127) / 128) * s.B * s.H;
-  hipLaunchKernelGGL((bwd_key_kernel<D, G, BIAS>), dim3(static_cast<unsigned>(((tot + 7) / 8) * 8)),
+  hipLaunchKernelGGL((bwd_key_kernel<D, G, BIAS, FORM>), dim3(static_cast<unsigned>(((tot + 7) / 8) * 8)),
                      dim3(kKeyThreads), 0, st, s, static_cast<const uint16_t*>(q),
                      static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(kp),
                      static_cast<const uint16_t*>(v), static_cast<const uint16_t*>(vp),
@@ -524,6 +568,11 @@ hipError_t mfma_bwd_key_b(const Shape& s, const void* q, const void* k, const vo
 hipError_t mfma_bwd_key(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
                         const void* vp, const void* dout, const float* lse, const float* delta,
                         void* dk, void* dv, hipStream_t st) {
+  if (s.form == 1) {  // determinant logits: w2 <= 32, no bias constants
+    if (s.w2 > 32) return hipErrorInvalidValue;
+    return s.D == 128 ? launch_key<128, 1, false, 1>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, st)
+                      : launch_key<64, 1, false, 1>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, st);
+  }
   return s.kp_bias != 0.f || s.vp_bias != 0.f
              ? mfma_bwd_key_b<true>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, st)
              : mfma_bwd_key_b<false>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, st);

@@ -53,6 +53,11 @@ BwdPlan mfma_bwd_plan(const Shape& s) {
   }
   p.delta_off = 0;
   p.halo_off = delta_bytes;  // 4 arrays: head/tail x dk'/dv'
+  p.dqt_off = 0;
+  if (s.form == 1) {  // determinant logits: the dQ~ rows of every query
+    p.dqt_off = (p.bytes + 255) & ~size_t(255);
+    p.bytes = p.dqt_off + bh * static_cast<size_t>(s.N) * 32 * s.D * 4;
+  }
   return p;
 }
 
@@ -598,6 +603,61 @@ __global__ __launch_bounds__(256) void halo_fixup_kernel(Shape s, BwdPlan plan, 
   dvp[dst] = f32_to_bf16(tail_vp[o] + head_vp[o]);
 }
 
+// Determinant logits (Section 5), from the dQ~ rows the query side stored:
+//   dq_i  = scale sum_k  dQ~_(i,k) x k'_k   (k in the w2 window of i)
+//   dk'_k = scale sum_i  q_i x dQ~_(i,k)    (i in [k, k + w2))
+// per 3-component chunk (the gradients of <dQ~, k' x q> in q and in k'); the
+// D mod 3 trailing components get 0. One thread per (query or key row,
+// chunk), fixed summation order: deterministic.
+template <int D, int WHICH>  // WHICH 0: dq, 1: dk'
+__global__ __launch_bounds__(256) void det_grad_kernel(Shape s, const float* __restrict__ dqt,
+                                                       const uint16_t* __restrict__ other,
+                                                       uint16_t* __restrict__ out) {
+  constexpr int NCH = (D + 2) / 3;  // chunks, the last one partial when D % 3 != 0
+  const long idx = static_cast<long>(blockIdx.x) * 256 + threadIdx.x;
+  const long total = static_cast<long>(s.B) * s.H * s.N * NCH;
+  if (idx >= total) return;
+  const int l = static_cast<int>(idx % NCH);
+  const long row = idx / NCH;  // bh * N + n
+  const int n = static_cast<int>(row % s.N);
+  const int bh = static_cast<int>(row / s.N);
+  const int b = bh / s.H, hh = bh - b * s.H;
+  const size_t rs = static_cast<size_t>(s.H) * D;
+  const size_t base = (static_cast<size_t>(b) * s.N * s.H + hh) * D;
+  float acc[3] = {0.f, 0.f, 0.f};
+  if (3 * l + 2 < D) {
+    auto cross = [](const float* x, const float* y, float* a) {
+      a[0] += x[1] * y[2] - x[2] * y[1];
+      a[1] += x[2] * y[0] - x[0] * y[2];
+      a[2] += x[0] * y[1] - x[1] * y[0];
+    };
+    if constexpr (WHICH == 0) {  // n = query i; rows r <-> k = i - 31 + r
+      for (int r = 0; r < 32; ++r) {
+        const int kk = n - 31 + r;
+        if (kk < 0 || kk <= n - s.w2) continue;
+        const float* a = dqt + ((static_cast<size_t>(row) * 32 + r) * D + 3 * l);
+        const uint16_t* y = other + base + static_cast<size_t>(kk) * rs + 3 * l;  // k'
+        const float xa[3] = {a[0], a[1], a[2]};
+        const float ya[3] = {bf16_to_f32(y[0]), bf16_to_f32(y[1]), bf16_to_f32(y[2])};
+        cross(xa, ya, acc);
+      }
+    } else {  // n = key row k; queries i = k .. k + w2 - 1, row r = k - i + 31
+      const int iend = min(s.N, n + s.w2);
+      for (int i = n; i < iend; ++i) {
+        const float* a = dqt + (((static_cast<size_t>(bh) * s.N + i) * 32 + (n - i + 31)) * D + 3 * l);
+        const uint16_t* x = other + base + static_cast<size_t>(i) * rs + 3 * l;  // q
+        const float xq[3] = {bf16_to_f32(x[0]), bf16_to_f32(x[1]), bf16_to_f32(x[2])};
+        const float ya[3] = {a[0], a[1], a[2]};
+        cross(xq, ya, acc);
+      }
+    }
+  }
+  uint16_t* dst = out + base + static_cast<size_t>(n) * rs + 3 * l;
+#pragma unroll
+  for (int e = 0; e < 3; ++e)
+    if (3 * l + e < D) dst[e] = f32_to_bf16(acc[e] * s.scale);
+}
+
 template <int D, int G>
 hipError_t launch_stage(const Shape& s, BwdStage stage, const void* q, const void* k, const void* kp,
                         const void* v, const void* vp, const void* dout, const float* lse, void* g0,
@@ -613,14 +673,22 @@ hipError_t launch_stage(const Shape& s, BwdStage stage, const void* q, const voi
   const auto* VP = static_cast<const uint16_t*>(vp);
   const auto* DO = static_cast<const uint16_t*>(dout);
   if (stage == BwdStage::Query && mfma_bwd_query_supported(s)) {
-    const hipError_t e = mfma_bwd_query(s, plan, Q, K, KP, V, VP, DO, lse, delta, g0, g1, g2, halo, st);
+    float* dqt = s.form == 1 ? reinterpret_cast<float*>(wsb + plan.dqt_off) : nullptr;
+    const hipError_t e = mfma_bwd_query(s, plan, Q, K, KP, V, VP, DO, lse, delta, g0, g1, g2, halo, dqt, st);
     if (e != hipSuccess) return e;
     if (plan.nchunks > 1) {
       const long n = static_cast<long>(s.B) * s.H * (plan.nchunks - 1) * (plan.W2P - 1) * D;
       hipLaunchKernelGGL(halo_fixup_kernel<D>, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256),
                          0, st, s, plan, halo, static_cast<uint16_t*>(g1), static_cast<uint16_t*>(g2));
     }
+    if (s.form == 1) {  // dq and dk' of the determinant logits (overwrite dk' entirely)
+      const long n = static_cast<long>(s.B) * s.H * s.N * ((D + 2) / 3);
+      const dim3 grid(static_cast<unsigned>((n + 255) / 256));
+      hipLaunchKernelGGL((det_grad_kernel<D, 0>), grid, dim3(256), 0, st, s, dqt, KP, static_cast<uint16_t*>(g0));
+      hipLaunchKernelGGL((det_grad_kernel<D, 1>), grid, dim3(256), 0, st, s, dqt, Q, static_cast<uint16_t*>(g1));
+    }
   } else if (stage == BwdStage::Query) {
+    if (s.form == 1) return hipErrorInvalidValue;  // determinant logits: w2 <= 32 only
     constexpr int WAVES = 4;
     const long totq = static_cast<long>(plan.nchunks) * s.B * s.H;
     auto go = [&](auto kern) {

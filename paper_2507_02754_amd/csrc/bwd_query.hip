@@ -60,13 +60,18 @@ struct QueryLds {
   static constexpr int bytes = qringOff + 2 * RQ * 2 * D;
 };
 
-template <int D, bool BIAS>
+// FORM 1: determinant logits (Section 5): role A forms q~ = (scale log2 e)
+// k'_k x q_i per 3-component chunk; role B stores its dQ~ rows (fp32, [B*H,
+// N, 32, D]) in dqt instead of reducing them, because dq_i = scale sum_k
+// dQ~_r x k'_k and dk'_k = scale sum_i q_i x dQ~_r mix components of a chunk
+// that lie in different lane halves; a separate kernel forms them.
+template <int D, bool BIAS, int FORM>
 __global__ __launch_bounds__(kQThreads, 1) void bwd_query_kernel(
     Shape s, BwdPlan plan, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ kp, const uint16_t* __restrict__ v, const uint16_t* __restrict__ vp,
     const uint16_t* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ delta,
     uint16_t* __restrict__ dq, uint16_t* __restrict__ dkp, uint16_t* __restrict__ dvp,
-    float* __restrict__ ws) {
+    float* __restrict__ ws, float* __restrict__ dqt) {
   constexpr int NT = D / 16, NDT = D / 32;
   using L = QueryLds<D>;
   using T = typename L::T;  // layout of the k'/v' row ring
@@ -309,7 +314,30 @@ __global__ __launch_bounds__(kQThreads, 1) void bwd_query_kernel(
           const u32x4_t qa = *reinterpret_cast<const u32x4_t*>(qrow + 16 * ch);
           const u32x4_t ka = *reinterpret_cast<const u32x4_t*>(krow + 16 * (ch ^ T::swz(kslot)));
           u32x4_t a4 = {0u, 0u, 0u, 0u};
-          if (rowvalid) {
+          if constexpr (FORM == 1) {
+            // windows of components 8 ch - 2 .. 8 ch + 9 of k' and q: the
+            // slot and the 4-byte words on either side (clamped at the row
+            // ends, where they are not used)
+            const int chp = ch > 0 ? ch - 1 : 0, chn = ch < T::CH - 1 ? ch + 1 : ch;
+            const int sw = T::swz(kslot);
+            const unsigned kw0 = *reinterpret_cast<const unsigned*>(krow + 16 * (chp ^ sw) + 12);
+            const unsigned kw1 = *reinterpret_cast<const unsigned*>(krow + 16 * (chn ^ sw));
+            const unsigned qw0 = *reinterpret_cast<const unsigned*>(qrow + 16 * chp + 12);
+            const unsigned qw1 = *reinterpret_cast<const unsigned*>(qrow + 16 * chn);
+            float fk[12], fq[12], cr[8];
+            fk[0] = bf16_lo(kw0), fk[1] = bf16_hi(kw0), fk[10] = bf16_lo(kw1), fk[11] = bf16_hi(kw1);
+            fq[0] = bf16_lo(qw0), fq[1] = bf16_hi(qw0), fq[10] = bf16_lo(qw1), fq[11] = bf16_hi(qw1);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              fk[2 + 2 * e] = bf16_lo(ka[e]), fk[3 + 2 * e] = bf16_hi(ka[e]);
+              fq[2 + 2 * e] = bf16_lo(qa[e]), fq[3 + 2 * e] = bf16_hi(qa[e]);
+            }
+            cross8_rt<3 * (D / 3)>(fk, fq, ch, cr);
+            if (rowvalid) {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) a4[e] = pack_bf16x2(cr[2 * e] * qscale, cr[2 * e + 1] * qscale);
+            }
+          } else if (rowvalid) {
 #pragma unroll
             for (int e = 0; e < 4; ++e)
               a4[e] = pack_bf16x2(bf16_lo(qa[e]) * plus_bias<BIAS>(bf16_lo(ka[e]), s.kp_bias) * qscale,
@@ -494,6 +522,24 @@ __global__ __launch_bounds__(kQThreads, 1) void bwd_query_kernel(
       }
       // ---- tile epilogue (B): dq_i, then scale q_i o dQ~_r into the dk' ring ----
       if (rowloader && tile + 1 < ntiles) row_put(i0 + QW, nrow);
+      if constexpr (FORM == 1) {
+        // dQ~ rows to dqt (row c of query i, d = 32 dt + 8 qd + 4 h + e);
+        // the ring phases keep their barriers (matching role A) without adds.
+        if (qvalid) {
+          float* dst = dqt + ((static_cast<size_t>(bh) * N + i) * 32 + c) * D;
+#pragma unroll
+          for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+            for (int qd = 0; qd < 4; ++qd)
+              *reinterpret_cast<float4*>(dst + 32 * dt + 8 * qd + 4 * h) =
+                  float4{adq[dt][4 * qd], adq[dt][4 * qd + 1], adq[dt][4 * qd + 2], adq[dt][4 * qd + 3]};
+        }
+        lds_barrier();  // matches the barrier before role A's ring phases
+        ring_add(ring_kp, adq, false, kk, [](auto) {});
+        flush_tile(i0);
+        lds_barrier();
+        continue;
+      }
       // dq_i = scale * sum_k k'_k o dQ~_(i,k): every lane multiplies its
       // accumulators (row c, d = 32 dt + 8 (v/4) + 4 h + v%4) by k'_k, then
       // the sums over the 32 rows run across lanes in registers: the first
@@ -561,7 +607,7 @@ bool mfma_bwd_query_supported(const Shape& s) { return s.w2 <= 32 && (s.D == 64 
 hipError_t mfma_bwd_query(const Shape& s, const BwdPlan& plan, const void* q, const void* k,
                           const void* kp, const void* v, const void* vp, const void* dout,
                           const float* lse, const float* delta, void* dq, void* dkp, void* dvp,
-                          float* halo, hipStream_t st) {
+                          float* halo, float* dqt, hipStream_t st) {
   const long tot = static_cast<long>(plan.nchunks) * s.B * s.H;
   const dim3 grid(static_cast<unsigned>(((tot + 7) / 8) * 8));
   const auto* Q = static_cast<const uint16_t*>(q);
@@ -574,14 +620,22 @@ hipError_t mfma_bwd_query(const Shape& s, const BwdPlan& plan, const void* q, co
   auto go = [&](auto kern) {
     hipLaunchKernelGGL(kern, grid, dim3(kQThreads), 0, st, s, plan, Q, K, KP, V, VP, DO, lse, delta,
                        static_cast<uint16_t*>(dq), static_cast<uint16_t*>(dkp), static_cast<uint16_t*>(dvp),
-                       halo);
+                       halo, dqt);
   };
-  if (s.D == 128)
-    bias ? go(bwd_query_kernel<128, true>) : go(bwd_query_kernel<128, false>);
-  else if (s.D == 64)
-    bias ? go(bwd_query_kernel<64, true>) : go(bwd_query_kernel<64, false>);
-  else
+  if (s.form == 1) {
+    if (s.D == 128)
+      go(bwd_query_kernel<128, false, 1>);
+    else if (s.D == 64)
+      go(bwd_query_kernel<64, false, 1>);
+    else
+      return hipErrorInvalidValue;
+  } else if (s.D == 128) {
+    bias ? go(bwd_query_kernel<128, true, 0>) : go(bwd_query_kernel<128, false, 0>);
+  } else if (s.D == 64) {
+    bias ? go(bwd_query_kernel<64, true, 0>) : go(bwd_query_kernel<64, false, 0>);
+  } else {
     return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 

@@ -92,6 +92,31 @@ __device__ __forceinline__ u32x4_t ldbuf128(__amdgpu_buffer_rsrc_t r, int off) {
 __device__ __forceinline__ u32x2_t ldbuf64(__amdgpu_buffer_rsrc_t r, int off) {
   return __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
 }
+__device__ __forceinline__ unsigned ldbuf32(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_bit_cast(unsigned, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
+
+// Chunkwise cross product for the determinant logits of Section 5: per
+// 3-component chunk, det[a; b; c] = a . (b x c). x[0 .. 11] and y[0 .. 11]
+// hold components 8 ch - 2 .. 8 ch + 9 of two vectors (a 3-chunk reaches at
+// most 2 components past a 16-byte slot of 8); out[e] = (x cross y) at
+// component 8 ch + e, and 0 for the D mod 3 trailing components (>= DC). The
+// chunk position m = (8 ch + e) mod 3 is taken at run time (ch may differ
+// between lanes): all three forms are evaluated and the right one selected.
+template <int DC>
+__device__ __forceinline__ void cross8_rt(const float* x, const float* y, int ch, float* out) {
+  const int m0 = (2 * ch) % 3;  // position of component 8 ch in its chunk
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int m = (m0 + e) % 3;
+    // chunk starting at window index e + 2 - m
+    const float c0 = x[e + 3] * y[e + 4] - x[e + 4] * y[e + 3];  // m = 0: b = e + 2
+    const float c1 = x[e + 3] * y[e + 1] - x[e + 1] * y[e + 3];  // m = 1: b = e + 1
+    const float c2 = x[e] * y[e + 1] - x[e + 1] * y[e];          // m = 2: b = e
+    const float v = m == 0 ? c0 : m == 1 ? c1 : c2;
+    out[e] = 8 * ch + e < DC ? v : 0.f;
+  }
+}
 // Byte-range of one head's rows of a [.., N, H, D] bf16 tensor, from row 0 to
 // the end of row N-1 (rows are rs_bytes apart).
 __device__ __forceinline__ unsigned head_bytes(int N, int rs_bytes, int D) {

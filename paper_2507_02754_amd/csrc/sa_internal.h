@@ -64,10 +64,12 @@ hipError_t mfma_fwd(const Shape& s, const void* q, const void* k, const void* kp
 
 // Backward work split and workspace layout of the MFMA path. The workspace
 // holds Delta ([B, H, N] floats) followed by four arrays of chunk-boundary
-// partial sums (head/tail x dk'/dv', each [B*H, nchunks, W2P - 1, D] floats).
+// partial sums (head/tail x dk'/dv', each [B*H, nchunks, W2P - 1, D] floats);
+// with determinant logits then the query side's dQ~ rows ([B*H, N, 32, D]
+// floats at dqt_off).
 struct BwdPlan {
   int G, W2P, CQ, nchunks;
-  size_t halo_floats, delta_off, halo_off, bytes;
+  size_t halo_floats, delta_off, halo_off, dqt_off, bytes;
 };
 BwdPlan mfma_bwd_plan(const Shape& s);
 bool mfma_bwd_supported(const Shape& s);
@@ -90,7 +92,7 @@ bool mfma_bwd_query_supported(const Shape& s);
 hipError_t mfma_bwd_query(const Shape& s, const BwdPlan& plan, const void* q, const void* k,
                           const void* kp, const void* v, const void* vp, const void* dout,
                           const float* lse, const float* delta, void* dq, void* dkp, void* dvp,
-                          float* halo, hipStream_t st);
+                          float* halo, float* dqt, hipStream_t st);
 
 // Grouped-query backward helpers (s.H query heads, s.Hkv K-side heads; the
 // four src/dst pointers are K, K', V, V' or their gradients).

@@ -78,16 +78,22 @@ def _load(paths):
     return [np.load(p, mmap_mode="r") for p in paths]
 
 
-def _fwd_task(paths, w1, w2, scale, queries):
-    import oracle as orc
+def _oracle(module):
+    import importlib
+
+    return importlib.import_module(module)
+
+
+def _fwd_task(paths, w1, w2, scale, queries, module="oracle"):
+    orc = _oracle(module)
 
     arrs = _load(paths)
     o, lse = orc.forward(*arrs, w1, w2, scale, queries=queries)
     return queries, o[queries], lse[queries]
 
 
-def _bwd_task(paths, w1, w2, scale, queries, rows):
-    import oracle as orc
+def _bwd_task(paths, w1, w2, scale, queries, rows, module="oracle"):
+    orc = _oracle(module)
 
     arrs = _load(paths)
     grads = orc.backward(*arrs, w1, w2, scale, queries=queries)
@@ -100,15 +106,16 @@ def _chunks(queries, n):
     return [queries[i:i + size] for i in range(0, len(queries), size)]
 
 
-def forward(q, k, kp, v, vp, w1, w2, scale, queries):
+def forward(q, k, kp, v, vp, w1, w2, scale, queries, module="oracle"):
     """Oracle O and LSE of one head ([N, D] arrays) at the listed queries:
-    returns (o [len(queries), D], lse [len(queries)]) in the order given."""
+    returns (o [len(queries), D], lse [len(queries)]) in the order given.
+    `module`: "oracle" (trilinear logits) or "oracle.determinant_oracle"."""
     paths = _save([q, k, kp, v, vp])
     try:
         pos = {x: i for i, x in enumerate(queries)}
         o = np.zeros((len(queries), q.shape[1]))
         lse = np.zeros(len(queries))
-        futs = [_pool().submit(_fwd_task, paths, w1, w2, scale, c)
+        futs = [_pool().submit(_fwd_task, paths, w1, w2, scale, c, module)
                 for c in _chunks(queries, 4 * workers())]
         for f in futs:
             qs, oc, lc = f.result()
@@ -120,7 +127,7 @@ def forward(q, k, kp, v, vp, w1, w2, scale, queries):
         _drop(paths)
 
 
-def backward(q, k, kp, v, vp, do, w1, w2, scale, queries, rows):
+def backward(q, k, kp, v, vp, do, w1, w2, scale, queries, rows, module="oracle"):
     """The oracle's backward of one head restricted to the listed queries,
     evaluated at rows = (dQ rows, dK rows, dK' rows, dV rows, dV' rows); returns
     five arrays [len(rows[t]), D]. A dK / dV row r is complete when `queries`
@@ -129,7 +136,7 @@ def backward(q, k, kp, v, vp, do, w1, w2, scale, queries, rows):
     try:
         rows = [list(r) for r in rows]
         acc = [np.zeros((len(r), q.shape[1])) for r in rows]
-        futs = [_pool().submit(_bwd_task, paths, w1, w2, scale, c, rows)
+        futs = [_pool().submit(_bwd_task, paths, w1, w2, scale, c, rows, module)
                 for c in _chunks(sorted(set(queries)), 4 * workers())]
         for f in futs:
             for a, part in zip(acc, f.result()):

@@ -52,6 +52,7 @@ def test_header_declares_the_expected_entry_points():
         "simplicial_attn_bwd_preprocess", "simplicial_attn_bwd_query_side",
         "simplicial_attn_bwd_key_side", "simplicial_attn_bwd_noalloc",
         "simplicial_attn_fwd_biased", "simplicial_attn_bwd_biased",
+        "simplicial_attn_det_bwd_workspace_size",
     ])
 
 

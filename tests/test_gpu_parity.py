@@ -341,6 +341,46 @@ def test_determinant_forward_full_size_sampled():
                     np.concatenate(ref_l), "bf16", "determinant full size")
 
 
+def test_determinant_backward_full_size_sampled():
+    """Determinant backward on the MFMA kernels at B=1, H=2, N=8192, D=128,
+    w1=512, w2=32 (with the dQ~ rows through the workspace): dQ every 64
+    queries, dK / dV and dK' / dV' on rows spread over the sequence, both heads,
+    against the determinant oracle (every query touching a checked row)."""
+    from oracle import determinant_oracle as dor
+    from paper_2507_02754_amd import simplicial_attn_det_bwd, simplicial_attn_det_fwd
+
+    b, h, n, d, w1, w2 = 1, 2, 8192, 128, 512, 32
+    _announce(f"determinant backward full size B={b} H={h} N={n} D={d} w1={w1} w2={w2} "
+              f"bwd={simplicial_attn_path_name(1, b, n, h, d, w1, w2, 1)}")
+    inputs = draw((b, n, h, d), seed=809, dtype=torch.bfloat16)
+    scale = d ** -0.5
+    x = [t.cuda() for t in inputs]
+    o, lse = simplicial_attn_det_fwd(*x[:5], w1, w2, scale)
+    grads = simplicial_attn_det_bwd(*x[:5], o, x[5], lse, w1, w2, scale)
+    torch.cuda.synchronize()
+    q_rows = sorted(set(range(0, n, 64)) | {1, 2, 31, 32, n - 2, n - 1})
+    k_rows = sorted({0, 1, 300, 511, n // 2, n - 700, n - 1})
+    kp_rows = sorted(set(range(5, n, 509)) | {0, 30, n - 1})
+    queries = set(q_rows)
+    for r in k_rows:
+        queries.update(range(r, min(n, r + w1)))
+    for r in kp_rows:
+        queries.update(range(r, min(n, r + w2)))
+    rows = [q_rows, k_rows, kp_rows, k_rows, kp_rows]
+    got = [[] for _ in range(5)]
+    ref = [[] for _ in range(5)]
+    import oracle_pool
+    for hh in range(h):
+        arrs = P.head_arrays(inputs, 0, hh)
+        g_ref = oracle_pool.backward(*arrs, w1, w2, scale, sorted(queries), rows,
+                                     module="oracle.determinant_oracle")
+        for t in range(5):
+            got[t].append(P.to64(grads[t][0, :, hh][torch.tensor(rows[t], device="cuda")]))
+            ref[t].append(g_ref[t])
+    P.check_grads([np.concatenate(g_) for g_ in got], [np.concatenate(r_) for r_ in ref], "bf16",
+                  "determinant backward full size")
+
+
 def test_gqa_forward_full_size_sampled():
     """16 query heads on 2 K-side heads, N = 8192, w1 = 512, w2 = 32: sampled rows
     of every query head against the oracle."""

@@ -21,4 +21,9 @@ def test_pooled_oracle_equals_direct_calls():
     ref = orc.backward(*arrs, w1, w2, scale)
     for g, r, sel in zip(got, ref, rows):
         np.testing.assert_allclose(g, r[sel], rtol=1e-12, atol=1e-14)
+    from oracle import determinant_oracle as dor
+    got = oracle_pool.backward(*arrs, w1, w2, scale, range(n), rows, module="oracle.determinant_oracle")
+    ref = dor.backward(*arrs, w1, w2, scale)
+    for g, r, sel in zip(got, ref, rows):
+        np.testing.assert_allclose(g, r[sel], rtol=1e-12, atol=1e-14)
     oracle_pool.shutdown()
