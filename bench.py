@@ -116,6 +116,10 @@ def main():
     ap.add_argument("--gqa-kv-heads", type=int, default=0,
                     help="also time the grouped-query forward and backward with this many "
                          "K-side heads (reported under \"gqa\"; not part of the step)")
+    ap.add_argument("--fused-main", action="store_true",
+                    help="time the fused backward (one S/dP computation, partial sums reduced in order) "
+                         "as the step's backward instead of the two-kernel backward")
+    ap.add_argument("--no-fused", action="store_true", help="skip the fused-backward section")
     ap.add_argument("--det", action="store_true",
                     help="also time the determinant-logit forward and backward (Section 5) at "
                          "B=1, H=16, N=4096, D=128, w1=512, w2=32 (reported under \"det\")")
@@ -129,6 +133,8 @@ def main():
     import torch
 
     from paper_2507_02754_amd import (load_library, simplicial_attn_bwd_key_side,
+                                      simplicial_attn_bwd_fused, simplicial_attn_bwd_fused_reduce,
+                                      simplicial_attn_bwd_fused_workspace_size,
                                       simplicial_attn_bwd_preprocess, simplicial_attn_bwd_query_side,
                                       simplicial_attn_bwd_workspace_size, simplicial_attn_fwd,
                                       simplicial_attn_fwd_gqa, simplicial_attn_bwd_gqa,
@@ -159,7 +165,16 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    phases = ["fwd", "bwd_preprocess", "bwd_query_side", "bwd_key_side"]
+    # The backward exactly as simplicial_attn_bwd runs it, stage by stage (its
+    # stage entry points), so that each kernel is timed by HIP events. With
+    # --fused-main the step's backward is the fused backward instead.
+    fws = simplicial_attn_bwd_fused_workspace_size(w.B, w.N, w.H, w.D, w.w1, w.w2, w.torch_dtype)
+    fused = bool(args.fused_main and fws)
+    if fused:
+        ws = torch.empty(fws, dtype=torch.uint8, device=dev)
+        phases = ["fwd", "bwd_preprocess", "bwd_fused", "bwd_reduce"]
+    else:
+        phases = ["fwd", "bwd_preprocess", "bwd_query_side", "bwd_key_side"]
 
     def step(ev=None):
         if ev:
@@ -170,12 +185,18 @@ def main():
         simplicial_attn_bwd_preprocess(out, do, w.w1, w.w2, ws)
         if ev:
             ev[2].record()
-        simplicial_attn_bwd_query_side(q, k, kp, v, vp, do, lse, w.w1, w.w2, ws, w.scale,
-                                       grads=(dq, dkp, dvp))
+        if fused:
+            simplicial_attn_bwd_fused(q, k, kp, v, vp, do, lse, w.w1, w.w2, ws, w.scale, grads=(dk, dv))
+        else:
+            simplicial_attn_bwd_query_side(q, k, kp, v, vp, do, lse, w.w1, w.w2, ws, w.scale,
+                                           grads=(dq, dkp, dvp))
         if ev:
             ev[3].record()
-        simplicial_attn_bwd_key_side(q, k, kp, v, vp, do, lse, w.w1, w.w2, ws, w.scale,
-                                     grads=(dk, dv))
+        if fused:
+            simplicial_attn_bwd_fused_reduce(q, w.w1, w.w2, ws, w.scale, grads=(dq, dkp, dvp))
+        else:
+            simplicial_attn_bwd_key_side(q, k, kp, v, vp, do, lse, w.w1, w.w2, ws, w.scale,
+                                         grads=(dk, dv))
         if ev:
             ev[4].record()
 
@@ -206,7 +227,7 @@ def main():
 
     unit = float(w.B) * w.H * w.N * w.w1 * w.w2 * w.D
     fwd_flops, bwd_flops = 4 * unit, 12 * unit
-    bwd_ms = ms["bwd_preprocess"] + ms["bwd_query_side"] + ms["bwd_key_side"]
+    bwd_ms = ms[phases[1]] + ms[phases[2]] + ms[phases[3]]
     value = (fwd_flops + bwd_flops) / (ms_step * 1e-3) / 1e12
     fwd_tf = fwd_flops / (ms["fwd"] * 1e-3) / 1e12
     bwd_tf = bwd_flops / (bwd_ms * 1e-3) / 1e12
@@ -215,11 +236,17 @@ def main():
     # (HIP events on the stream the library launches on). The query-side stage
     # also runs the small chunk-boundary fix-up kernel inside its events.
     qkernel = "bwd_query_kernel" if w.w2 <= 32 else "bwd_q_kernel"
-    algo = {  # phase: (kernel, algorithmic FLOPs, executed MFMA FLOPs)
-        "fwd": ("fwd_mfma_kernel", 4 * unit, 4 * unit),
-        "bwd_query_side": (qkernel, 8 * unit, 8 * unit),   # S recompute, dP, dQ~, U~
-        "bwd_key_side": ("bwd_key_kernel", 4 * unit, 8 * unit),  # dV, dK (+ S/dP recompute, not counted)
-    }
+    if fused:
+        algo = {  # phase: (kernel, algorithmic FLOPs, executed MFMA FLOPs)
+            "fwd": ("fwd_mfma_kernel", 4 * unit, 4 * unit),
+            "bwd_fused": ("bwd_fused_kernel", 12 * unit, 12 * unit),  # S, dP, dV, dK, dQ~, U~ once each
+        }
+    else:
+        algo = {
+            "fwd": ("fwd_mfma_kernel", 4 * unit, 4 * unit),
+            "bwd_query_side": (qkernel, 8 * unit, 8 * unit),   # S recompute, dP, dQ~, U~
+            "bwd_key_side": ("bwd_key_kernel", 4 * unit, 8 * unit),  # dV, dK (+ S/dP recompute, not counted)
+        }
     dom = max(algo, key=lambda p: ms[p])
     kname, kflops, _ = algo[dom]
     achieved = kflops / (ms[dom] * 1e-3) / 1e12
@@ -266,6 +293,44 @@ def main():
         "roofline": roofline,
         "cpu_baseline": None,
     }
+    if fws and not fused and not args.no_fused:
+        # The fused backward (same inputs, its own workspace): Delta, the fused
+        # kernel, the reduction of its partial sums; HIP events per stage.
+        fwsb = torch.empty(fws, dtype=torch.uint8, device=dev)
+
+        def fused_step(ev=None):
+            if ev:
+                ev[0].record()
+            simplicial_attn_bwd_preprocess(out, do, w.w1, w.w2, fwsb)
+            if ev:
+                ev[1].record()
+            simplicial_attn_bwd_fused(q, k, kp, v, vp, do, lse, w.w1, w.w2, fwsb, w.scale, grads=(dk, dv))
+            if ev:
+                ev[2].record()
+            simplicial_attn_bwd_fused_reduce(q, w.w1, w.w2, fwsb, w.scale, grads=(dq, dkp, dvp))
+            if ev:
+                ev[3].record()
+
+        for _ in range(args.warmup):
+            fused_step()
+        fev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+        torch.cuda.synchronize()
+        for i in range(args.steps):
+            fused_step(fev[i])
+        torch.cuda.synchronize()
+        fst = [sum(e[j].elapsed_time(e[j + 1]) for e in fev) / args.steps for j in range(3)]
+        fb = sum(fst)
+        result["fused_backward"] = {
+            "bwd_ms": round(fb, 4), "preprocess_ms": round(fst[0], 4), "fused_kernel_ms": round(fst[1], 4),
+            "reduce_ms": round(fst[2], 4),
+            "bwd_tflops": round(bwd_flops / (fb * 1e-3) / 1e12, 2),
+            "bwd_frac": round(bwd_flops / (fb * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "fused_kernel_frac": round(12 * unit / (fst[1] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "workspace_bytes": fws,
+            "note": "bwd_fused_kernel: S, dP, dV, dK, dQ~, U~ once each (12 units); fused_reduce_kernel adds "
+                    "the per-64-key partial sums of dq, dk', dv' in order",
+        }
+        del fwsb
     if args.gqa_kv_heads:
         # Grouped-query forward + backward at the same query shape, K, K', V, V'
         # taken from the first Hkv heads of the inputs.

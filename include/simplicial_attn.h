@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define SIMPLICIAL_ATTN_ABI_VERSION 5
+#define SIMPLICIAL_ATTN_ABI_VERSION 6
 
 #define SA_DTYPE_F32 0
 #define SA_DTYPE_BF16 1
@@ -108,6 +108,9 @@ size_t simplicial_attn_bwd_workspace_size(int64_t B, int64_t N, int64_t H, int64
  *                      bytes, 16-byte aligned; contents on entry are ignored
  *   other arguments    as simplicial_attn_fwd
  * The result is bitwise deterministic: no floating-point atomics are used.
+ * It runs Section 7's two kernels (query side and key side; see the stage
+ * entry points below). The fused backward below is the alternative with one
+ * computation of S and dP.
  */
 int simplicial_attn_bwd(const void* q, const void* k, const void* kp, const void* v, const void* vp,
                         const void* out, const void* dout, const float* lse, void* dq, void* dk,
@@ -252,6 +255,34 @@ int simplicial_attn_bwd_key_side(const void* q, const void* k, const void* kp, c
                                  void* dv, void* workspace, size_t workspace_bytes, int64_t B,
                                  int64_t N, int64_t H, int64_t D, int32_t w1, int32_t w2,
                                  float scale, int32_t dtype, void* stream);
+/*
+ * Fused backward: Section 7's five gradients from one computation of S and dP
+ * per (row block, key block), instead of the two kernels that each recompute
+ * them (12 units of matrix work per query instead of 16). A kernel owns 64
+ * keys: it writes dK, dV and its partial sums of dQ, dK', dV' (fp32) to
+ * `workspace`; the reduction adds the partial sums of the kernels in a fixed
+ * order, so the result is bitwise deterministic (no atomics). Same gradients
+ * as simplicial_attn_bwd up to the order of fp32 additions. Sequence on one
+ * stream: simplicial_attn_bwd_preprocess (Delta), simplicial_attn_bwd_fused,
+ * simplicial_attn_bwd_fused_reduce, all three with the same workspace of at
+ * least simplicial_attn_bwd_fused_workspace_size() bytes: Delta plus
+ * 4 * B * H * ceil(N / 64) * ((63 + w1) + 2 * (94 + w1)) * D bytes of
+ * partial sums (7.5 GB at B=1, H=16, N=32768, D=128, w1=512).
+ * Shapes: bf16, head_dim 128, w2 <= 32; the size function returns 0 and the
+ * two calls SA_ERR_UNSUPPORTED for others. kp_bias, vp_bias: the K' / V'
+ * constants of simplicial_attn_bwd_biased (0 for the plain operation; the
+ * reduction takes none). Arguments otherwise as for the stages above.
+ */
+size_t simplicial_attn_bwd_fused_workspace_size(int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1,
+                                                int32_t w2, int32_t dtype);
+int simplicial_attn_bwd_fused(const void* q, const void* k, const void* kp, const void* v,
+                              const void* vp, const void* dout, const float* lse, void* dk, void* dv,
+                              void* workspace, size_t workspace_bytes, int64_t B, int64_t N, int64_t H,
+                              int64_t D, int32_t w1, int32_t w2, float scale, float kp_bias,
+                              float vp_bias, int32_t dtype, void* stream);
+int simplicial_attn_bwd_fused_reduce(void* dq, void* dkp, void* dvp, const void* workspace,
+                                     size_t workspace_bytes, int64_t B, int64_t N, int64_t H, int64_t D,
+                                     int32_t w1, int32_t w2, float scale, int32_t dtype, void* stream);
 
 /* Static, NUL-terminated description of a status code ("unknown status" otherwise). */
 const char* simplicial_attn_error_string(int code);

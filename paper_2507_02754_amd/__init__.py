@@ -25,6 +25,9 @@ from .binding import (  # noqa: F401
     simplicial_attn_det_bwd,
     simplicial_attn_det_bwd_workspace_size,
     simplicial_attn_det_fwd,
+    simplicial_attn_bwd_fused,
+    simplicial_attn_bwd_fused_reduce,
+    simplicial_attn_bwd_fused_workspace_size,
     simplicial_attn_bwd_key_side,
     simplicial_attn_bwd_preprocess,
     simplicial_attn_bwd_query_side,

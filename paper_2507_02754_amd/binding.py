@@ -30,6 +30,9 @@ __all__ = [
     "simplicial_attn_bwd_preprocess",
     "simplicial_attn_bwd_query_side",
     "simplicial_attn_bwd_key_side",
+    "simplicial_attn_bwd_fused",
+    "simplicial_attn_bwd_fused_reduce",
+    "simplicial_attn_bwd_fused_workspace_size",
     "simplicial_attn_bwd_workspace_size",
     "simplicial_attn_error_string",
     "simplicial_attn_abi_version",
@@ -92,6 +95,12 @@ def load_library():
     lib.simplicial_attn_bwd_query_side.restype = ctypes.c_int
     lib.simplicial_attn_bwd_key_side.argtypes = [vp] * 10 + [ctypes.c_size_t] + [i64] * 4 + [i32, i32, f32, i32, vp]
     lib.simplicial_attn_bwd_key_side.restype = ctypes.c_int
+    lib.simplicial_attn_bwd_fused.argtypes = [vp] * 10 + [ctypes.c_size_t] + [i64] * 4 + [i32, i32, f32, f32, f32, i32, vp]
+    lib.simplicial_attn_bwd_fused.restype = ctypes.c_int
+    lib.simplicial_attn_bwd_fused_reduce.argtypes = [vp] * 4 + [ctypes.c_size_t] + [i64] * 4 + [i32, i32, f32, i32, vp]
+    lib.simplicial_attn_bwd_fused_reduce.restype = ctypes.c_int
+    lib.simplicial_attn_bwd_fused_workspace_size.argtypes = [i64] * 4 + [i32, i32, i32]
+    lib.simplicial_attn_bwd_fused_workspace_size.restype = ctypes.c_size_t
     lib.simplicial_attn_bwd_workspace_size.argtypes = [i64] * 4 + [i32, i32, i32]
     lib.simplicial_attn_bwd_workspace_size.restype = ctypes.c_size_t
     lib.simplicial_attn_error_string.argtypes = [ctypes.c_int]
@@ -293,6 +302,45 @@ def simplicial_attn_bwd_key_side(q, k, kp, v, vp, dout, lse, w1, w2, workspace, 
         B, N, H, D, int(w1), int(w2), float(scale), dt, _stream(q.device))
     if rc != 0:
         raise SimplicialAttnError(rc, "simplicial_attn_bwd_key_side")
+    return grads
+
+
+def simplicial_attn_bwd_fused_workspace_size(B, N, H, D, w1, w2, dtype):
+    """Bytes of the fused backward's workspace (0: shape not supported by it)."""
+    dt = _DTYPES.get(dtype, dtype)
+    return int(load_library().simplicial_attn_bwd_fused_workspace_size(B, N, H, D, int(w1), int(w2), int(dt)))
+
+
+def simplicial_attn_bwd_fused(q, k, kp, v, vp, dout, lse, w1, w2, workspace, scale=None, grads=None,
+                              kp_bias=0.0, vp_bias=0.0):
+    """(dK, dV) of the fused kernel after simplicial_attn_bwd_preprocess filled
+    `workspace` (of simplicial_attn_bwd_fused_workspace_size bytes); the
+    kernel also leaves the partial sums of dQ, dK', dV' there."""
+    (B, N, H, D), dt = _bwd_common(q, k, kp, v, vp, dout, lse, w1, w2)
+    scale = D ** -0.5 if scale is None else scale
+    grads = grads if grads is not None else tuple(torch.empty_like(q) for _ in range(2))
+    _check_inputs((q, *grads), ("q", "dk", "dv"))
+    rc = load_library().simplicial_attn_bwd_fused(
+        _ptr(q), _ptr(k), _ptr(kp), _ptr(v), _ptr(vp), _ptr(dout), _ptr(lse),
+        *(_ptr(g) for g in grads), _ptr(workspace), ctypes.c_size_t(workspace.numel()),
+        B, N, H, D, int(w1), int(w2), float(scale), float(kp_bias), float(vp_bias), dt, _stream(q.device))
+    if rc != 0:
+        raise SimplicialAttnError(rc, "simplicial_attn_bwd_fused")
+    return grads
+
+
+def simplicial_attn_bwd_fused_reduce(q, w1, w2, workspace, scale=None, grads=None):
+    """(dQ, dK', dV') from the partial sums simplicial_attn_bwd_fused left in
+    `workspace` (q gives sizes, dtype and device)."""
+    (B, N, H, D), dt = _check_inputs((q,), ("q",))
+    scale = D ** -0.5 if scale is None else scale
+    grads = grads if grads is not None else tuple(torch.empty_like(q) for _ in range(3))
+    _check_inputs((q, *grads), ("q", "dq", "dkp", "dvp"))
+    rc = load_library().simplicial_attn_bwd_fused_reduce(
+        *(_ptr(g) for g in grads), _ptr(workspace), ctypes.c_size_t(workspace.numel()),
+        B, N, H, D, int(w1), int(w2), float(scale), dt, _stream(q.device))
+    if rc != 0:
+        raise SimplicialAttnError(rc, "simplicial_attn_bwd_fused_reduce")
     return grads
 
 

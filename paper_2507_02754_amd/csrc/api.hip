@@ -71,6 +71,9 @@ Path choose_path(int which, int64_t B, int64_t N, int64_t H, int64_t D, int32_t 
   return Path::Generic;
 }
 
+// Shapes the fused backward kernel takes.
+bool fused_path(const Shape& s) { return sa::mfma_fused_supported(s); }
+
 size_t workspace_bytes_for(int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1, int32_t w2,
                            int32_t dtype) {
   if (check_sizes(B, N, H, D, w1, w2, dtype) != SA_OK) return 0;
@@ -326,6 +329,50 @@ int simplicial_attn_bwd_biased(const void* q, const void* k, const void* kp, con
   if (r != SA_OK) return r;
   return run_stage(s, path, BwdStage::Key, q, k, kp, v, vp, dout, lse, dk, dv, nullptr, workspace,
                    st);
+}
+
+size_t simplicial_attn_bwd_fused_workspace_size(int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1,
+                                                int32_t w2, int32_t dtype) {
+  if (check_sizes(B, N, H, D, w1, w2, dtype) != SA_OK) return 0;
+  const Shape s = make_shape(B, N, H, D, w1, w2, 1.0f, dtype);
+  return fused_path(s) ? sa::mfma_fused_plan(s).bytes : 0;
+}
+
+// Validation shared by the fused entry points.
+static int check_fused(int64_t B, int64_t N, int64_t H, int64_t D, int32_t w1, int32_t w2, float scale,
+                int32_t dtype, size_t workspace_bytes) {
+  if (!isfinite(scale)) return SA_ERR_INVALID;
+  const int rc = check_sizes(B, N, H, D, w1, w2, dtype);
+  if (rc != SA_OK) return rc;
+  const size_t need = simplicial_attn_bwd_fused_workspace_size(B, N, H, D, w1, w2, dtype);
+  if (need == 0) return SA_ERR_UNSUPPORTED;
+  return workspace_bytes < need ? SA_ERR_WORKSPACE : SA_OK;
+}
+
+int simplicial_attn_bwd_fused(const void* q, const void* k, const void* kp, const void* v,
+                              const void* vp, const void* dout, const float* lse, void* dk, void* dv,
+                              void* workspace, size_t workspace_bytes, int64_t B, int64_t N, int64_t H,
+                              int64_t D, int32_t w1, int32_t w2, float scale, float kp_bias,
+                              float vp_bias, int32_t dtype, void* stream) {
+  if (check_ptrs({q, k, kp, v, vp, dout, lse, dk, dv, workspace}) != SA_OK) return SA_ERR_INVALID;
+  if (!isfinite(kp_bias) || !isfinite(vp_bias)) return SA_ERR_INVALID;
+  const int rc = check_fused(B, N, H, D, w1, w2, scale, dtype, workspace_bytes);
+  if (rc != SA_OK) return rc;
+  Shape s = make_shape(B, N, H, D, w1, w2, scale, dtype);
+  s.kp_bias = kp_bias;
+  s.vp_bias = vp_bias;
+  return to_status(sa::mfma_bwd_fused(s, q, k, kp, v, vp, dout, lse, dk, dv, workspace,
+                                      static_cast<hipStream_t>(stream)));
+}
+
+int simplicial_attn_bwd_fused_reduce(void* dq, void* dkp, void* dvp, const void* workspace,
+                                     size_t workspace_bytes, int64_t B, int64_t N, int64_t H, int64_t D,
+                                     int32_t w1, int32_t w2, float scale, int32_t dtype, void* stream) {
+  if (check_ptrs({dq, dkp, dvp, workspace}) != SA_OK) return SA_ERR_INVALID;
+  const int rc = check_fused(B, N, H, D, w1, w2, scale, dtype, workspace_bytes);
+  if (rc != SA_OK) return rc;
+  const Shape s = make_shape(B, N, H, D, w1, w2, scale, dtype);
+  return to_status(sa::mfma_bwd_fused_reduce(s, dq, dkp, dvp, workspace, static_cast<hipStream_t>(stream)));
 }
 
 int simplicial_attn_bwd_noalloc(const void* q, const void* k, const void* kp, const void* v,

@@ -86,6 +86,26 @@ hipError_t mfma_bwd_key(const Shape& s, const void* q, const void* k, const void
                         const void* vp, const void* dout, const float* lse, const float* delta,
                         void* dk, void* dv, hipStream_t st);
 
+// Fused backward (w2 <= 32, trilinear logits, bf16, head_dim 128, one K-side
+// head per query head): one kernel computes S and dP once per (row block, key
+// group) and produces dK, dV directly and per-workgroup partial sums of dq,
+// dk', dv'; a second kernel adds the partials. A workgroup owns kw keys.
+// Workspace: Delta ([B, H, N] floats, as in BwdPlan) then the partials,
+// offsets in floats: dq at pq_off ([B*H, njb, RQ, D]; row i - kw jb), dk' at
+// pk_off and dv' at pv_off ([B*H, njb, RK, D]; row k - kw jb + 31),
+// njb = ceil(N / kw), RQ = kw - 1 + w1, RK = kw + 30 + w1.
+struct FusedPlan {
+  int kw, njb, RQ, RK;
+  size_t delta_floats, pq_off, pk_off, pv_off, bytes;
+};
+FusedPlan mfma_fused_plan(const Shape& s);
+bool mfma_fused_supported(const Shape& s);
+hipError_t mfma_bwd_fused(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
+                          const void* vp, const void* dout, const float* lse, void* dk, void* dv,
+                          void* workspace, hipStream_t st);
+hipError_t mfma_bwd_fused_reduce(const Shape& s, void* dq, void* dkp, void* dvp, const void* workspace,
+                                 hipStream_t st);
+
 // Query-side backward stage for w2 <= 32 (dq, dk', dv' and the chunk-boundary
 // partial sums in `halo`; the fix-up kernel runs afterwards).
 bool mfma_bwd_query_supported(const Shape& s);

@@ -32,7 +32,9 @@ import numpy as np
 import torch
 
 import oracle as orc
-from paper_2507_02754_amd import simplicial_attn_bwd, simplicial_attn_fwd
+from paper_2507_02754_amd import (simplicial_attn_bwd, simplicial_attn_bwd_fused, simplicial_attn_bwd_fused_reduce,
+                                  simplicial_attn_bwd_fused_workspace_size, simplicial_attn_bwd_preprocess,
+                                  simplicial_attn_fwd)
 
 TOL = {
     "fp32": dict(o_maxrel=1e-5, lse_abs=1e-5, g_maxrel=1e-5, o_norm=1e-5, g_norm=1e-5),
@@ -62,6 +64,21 @@ def gpu_backward(inputs, out, lse, w1, w2, scale, device="cuda"):
     grads = simplicial_attn_bwd(q, k, kp, v, vp, out, do, lse, w1, w2, scale)
     torch.cuda.synchronize()
     return grads
+
+
+def gpu_backward_fused(inputs, out, lse, w1, w2, scale, kp_bias=0.0, vp_bias=0.0, device="cuda"):
+    """The fused backward through its three C-ABI calls (Delta, fused kernel,
+    reduction); gradients in the order dq, dk, dk', dv, dv'."""
+    q, k, kp, v, vp, do = (x.to(device) for x in inputs)
+    b, n, h, d = q.shape
+    ws = torch.empty(simplicial_attn_bwd_fused_workspace_size(b, n, h, d, w1, w2, q.dtype), dtype=torch.uint8,
+                     device=device)
+    simplicial_attn_bwd_preprocess(out, do, w1, w2, ws)
+    dk, dv = simplicial_attn_bwd_fused(q, k, kp, v, vp, do, lse, w1, w2, ws, scale, kp_bias=kp_bias,
+                                       vp_bias=vp_bias)
+    dq, dkp, dvp = simplicial_attn_bwd_fused_reduce(q, w1, w2, ws, scale)
+    torch.cuda.synchronize()
+    return dq, dk, dkp, dv, dvp
 
 
 def head_arrays(inputs, b, h):

@@ -52,7 +52,8 @@ def test_header_declares_the_expected_entry_points():
         "simplicial_attn_bwd_preprocess", "simplicial_attn_bwd_query_side",
         "simplicial_attn_bwd_key_side", "simplicial_attn_bwd_noalloc",
         "simplicial_attn_fwd_biased", "simplicial_attn_bwd_biased",
-        "simplicial_attn_det_bwd_workspace_size",
+        "simplicial_attn_det_bwd_workspace_size", "simplicial_attn_bwd_fused",
+        "simplicial_attn_bwd_fused_reduce", "simplicial_attn_bwd_fused_workspace_size",
     ])
 
 
@@ -259,7 +260,49 @@ def test_path_names(lib):
     assert f(0, 1, 128, 1, 48, 16, 8, 0) == "invalid"
     assert f(2, 1, 128, 1, 64, 16, 8, 0) == "invalid"
     for which in (0, 1):
-        assert f(which, 1, 32768, 16, 128, 512, 32, 1) in ("generic", "mfma_bf16")
+        assert f(which, 1, 32768, 16, 128, 512, 32, 1) == "mfma_bf16"
+    assert f(1, 1, 4096, 8, 128, 512, 32, 0) == "generic"
+
+
+def test_fused_workspace_holds_the_partial_sums(lib):
+    """The fused backward's workspace: Delta, then per workgroup of 64 keys the
+    dq partials of 63 + w1 queries and the dk', dv' partials of 94 + w1
+    k-rows (fp32, D each); at least the split backward's workspace (the
+    preprocess stage checks that size). 0 for shapes it does not take."""
+    f = binding.simplicial_attn_bwd_fused_workspace_size
+    for B, N, H, w1, w2 in [(1, 32768, 16, 512, 32), (2, 8192, 8, 512, 32), (1, 100, 2, 7, 5), (1, 1, 1, 1, 1)]:
+        njb = -(-N // 64)
+        need = 4 * (B * H * N + B * H * njb * ((63 + w1) + 2 * (94 + w1)) * 128)
+        ws = f(B, N, H, 128, w1, w2, 1)
+        assert ws >= need and ws >= binding.simplicial_attn_bwd_workspace_size(B, N, H, 128, w1, w2, 1)
+    assert f(1, 4096, 8, 128, 512, 64, 1) == 0  # w2 > 32
+    assert f(1, 4096, 8, 64, 512, 32, 1) == 0   # head_dim 64
+    assert f(1, 4096, 8, 128, 512, 32, 0) == 0  # fp32
+    assert f(0, 4096, 8, 128, 512, 32, 1) == 0  # invalid
+
+
+@only_without_gpu
+def test_fused_stages_reject_invalid_arguments(lib):
+    size = ctypes.c_size_t
+    args = [1, 64, 2, 128, 16, 8]
+    fused = lambda ptrs, ws=1 << 30, scale=0.1, a=args, dtype=1, kb=0.0: lib.simplicial_attn_bwd_fused(
+        *[ctypes.c_void_p(p) for p in ptrs], size(ws), *a, ctypes.c_float(scale), ctypes.c_float(kb),
+        ctypes.c_float(0.0), dtype, None)
+    red = lambda ptrs, ws=1 << 30, scale=0.1, a=args, dtype=1: lib.simplicial_attn_bwd_fused_reduce(
+        *[ctypes.c_void_p(p) for p in ptrs], size(ws), *a, ctypes.c_float(scale), dtype, None)
+    for call, n in ((fused, 10), (red, 4)):
+        for i in range(n):
+            ptrs = [A] * n
+            ptrs[i] = 0
+            assert call(ptrs) == 1
+            ptrs[i] = MISALIGNED
+            assert call(ptrs) == 1
+        assert call([A] * n, ws=16) == 3
+        assert call([A] * n, scale=float("nan")) == 1
+        assert call([A] * n, a=[1, 64, 2, 64, 16, 8]) == 2   # head_dim 64: split path only
+        assert call([A] * n, a=[1, 64, 2, 128, 16, 40]) == 2  # w2 > 32
+        assert call([A] * n, dtype=0) == 2                     # fp32
+    assert fused([A] * 10, kb=float("inf")) == 1
 
 
 @only_without_gpu

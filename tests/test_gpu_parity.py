@@ -7,7 +7,8 @@ import pytest
 import torch
 
 import oracle as orc
-from paper_2507_02754_amd import (load_library, simplicial_attn_bwd, simplicial_attn_bwd_key_side,
+from paper_2507_02754_amd import (load_library, simplicial_attn_bwd, simplicial_attn_bwd_fused_workspace_size,
+                                  simplicial_attn_bwd_key_side, simplicial_attn_fwd_biased,
                                   simplicial_attn_bwd_preprocess, simplicial_attn_bwd_query_side,
                                   simplicial_attn_bwd_workspace_size, simplicial_attn_fwd,
                                   simplicial_attn_path_name)
@@ -581,7 +582,9 @@ def test_forward_is_deterministic(d, w1):
                                    (1, 1, 90, 64, 7, 5)])
 def test_staged_backward_matches_composite(shape):
     """preprocess + query side + key side (the three stage entry points) give
-    bitwise the same gradients as simplicial_attn_bwd."""
+    bitwise the same gradients as simplicial_attn_bwd; where the fused
+    backward takes the shape, its gradients agree with them at the parity
+    bar (both are checked against the oracle by other tests)."""
     b, h, n, d, w1, w2 = shape
     _announce(f"staged backward {shape}")
     dt = torch.bfloat16 if (w1, w2) != (7, 5) else torch.float32
@@ -596,6 +599,108 @@ def test_staged_backward_matches_composite(shape):
     torch.cuda.synchronize()
     for a, c in zip(ref, (dq, dk, dkp, dv, dvp)):
         assert torch.equal(a, c)
+    if simplicial_attn_bwd_fused_workspace_size(b, n, h, d, w1, w2, dt):
+        fused = P.gpu_backward_fused(x, o, lse, w1, w2, d ** -0.5)
+        P.check_grads([P.to64(g) for g in fused], [P.to64(g) for g in ref], "bf16", f"fused vs split {shape}")
+
+
+# ---- fused backward (one computation of S and dP; Section 7's gradients) ----
+
+FUSED = [
+    # (B, H, N, D, w1, w2)
+    (1, 2, 300, 128, 64, 32),    # several 64-key blocks and a ragged tail
+    (1, 1, 150, 128, 16, 32),    # w1 < w2
+    (1, 1, 20, 128, 512, 32),    # both windows longer than the sequence
+    (1, 2, 65, 128, 64, 17),     # a second key block with one key
+    (2, 1, 190, 128, 100, 31),   # w2 = 31
+    (1, 1, 129, 128, 33, 7),     # w2 not a multiple of 32, k-rows outside the window inside the tile
+    (2, 2, 640, 128, 300, 32),   # key blocks past the edge of every window
+]
+
+
+@pytest.mark.parametrize("shape", FUSED, ids=[str(s) for s in FUSED])
+def test_fused_backward_small_full(shape):
+    b, h, n, d, w1, w2 = shape
+    _announce(f"fused backward {shape}")
+    inputs = draw((b, n, h, d), seed=200 + n)
+    scale = d ** -0.5
+    o, lse = P.gpu_forward(inputs, w1, w2, scale)
+    grads = P.gpu_backward_fused(inputs, o, lse, w1, w2, scale)
+    _, _, g_ref = P.full_oracle(inputs, w1, w2, scale)
+    P.check_grads([P.to64(g) for g in grads], g_ref, "bf16", f"fused {shape}")
+
+
+def test_fused_backward_single_pair_edges():
+    """N = 1 and unit windows: one pair per query, so dQ, dK, dK' vanish
+    exactly (bounded by the operand rounding) and dV, dV' are exact products."""
+    for (b, h, n, d, w1, w2) in [(1, 3, 1, 128, 512, 32), (1, 2, 130, 128, 1, 1)]:
+        _announce(f"fused backward single pair {(b, h, n, d, w1, w2)}")
+        inputs = draw((b, n, h, d), seed=300 + n)
+        o, lse = P.gpu_forward(inputs, w1, w2, d ** -0.5)
+        grads = P.gpu_backward_fused(inputs, o, lse, w1, w2, d ** -0.5)
+        _, _, g_ref = P.full_oracle(inputs, w1, w2, d ** -0.5)
+        P.check_grads([P.to64(g) for g in grads[3:]], g_ref[3:], "bf16", f"fused single pair {n}")
+        P.check_single_pair_grads([P.to64(g) for g in grads[:3]], [t.double().numpy() for t in inputs],
+                                  d ** -0.5, f"fused single pair {n}")
+
+
+def test_fused_backward_with_bias_constants():
+    b, h, n, d, w1, w2 = 1, 2, 300, 128, 64, 32
+    kb, vb = 0.75, -0.5
+    _announce("fused backward with K'/V' constants")
+    inputs = draw((b, n, h, d), seed=71)
+    scale = d ** -0.5
+    q, k, kp, v, vp = (t.cuda() for t in inputs[:5])
+    o, lse = simplicial_attn_fwd_biased(q, k, kp, v, vp, w1, w2, scale, kb, vb)
+    grads = P.gpu_backward_fused(inputs, o, lse, w1, w2, scale, kp_bias=kb, vp_bias=vb)
+    shifted = [t.double() for t in inputs]
+    shifted[2] = shifted[2] + kb
+    shifted[4] = shifted[4] + vb
+    _, _, g_ref = P.full_oracle(shifted, w1, w2, scale)
+    P.check_grads([P.to64(g) for g in grads], g_ref, "bf16", "fused biased")
+
+
+def test_fused_backward_is_deterministic():
+    b, h, n, d, w1, w2 = 1, 4, 2000, 128, 512, 32
+    _announce("fused backward determinism")
+    inputs = draw((b, n, h, d), seed=81)
+    o, lse = P.gpu_forward(inputs, w1, w2, d ** -0.5)
+    g0 = P.gpu_backward_fused(inputs, o, lse, w1, w2, d ** -0.5)
+    for _ in range(3):
+        g1 = P.gpu_backward_fused(inputs, o, lse, w1, w2, d ** -0.5)
+        for a, c in zip(g0, g1):
+            assert torch.equal(a.view(torch.int16), c.view(torch.int16))
+
+
+@pytest.mark.parametrize("name", ["fb_bf16_n8k", "long_bf16_n32k"])
+def test_fused_backward_full_size(name):
+    """At full size: two heads, dQ every 16 queries, dK / dV and dK' / dV' rows
+    spread over the sequence (and the edges), each against the oracle run on
+    every query that touches them."""
+    import oracle_pool
+
+    w = WORKLOADS[name]
+    _announce(f"fused backward {w.name} {w.shape()} w1={w.w1} w2={w.w2}")
+    inputs = make_inputs(w)
+    o, lse = P.gpu_forward(inputs, w.w1, w.w2, w.scale)
+    grads = P.gpu_backward_fused(inputs, o, lse, w.w1, w.w2, w.scale)
+    n = w.N
+    edges = [0, 1, w.w2 - 1, w.w1 - 1, 63, 64, n // 2, n - 2, n - 1]
+    for (b, h), kstride, kpstride in FULL_BWD[name]:
+        q_rows = _spread_rows(n, 16, 7, w.w1, w.w2, w.seed)
+        k_rows = sorted(set(edges) | set(_spread_rows(n, kstride, 41, 1, 1, w.seed)))
+        kp_rows = sorted(set(edges) | set(_spread_rows(n, kpstride, 11, 1, 1, w.seed)))
+        queries = set(q_rows)
+        for r in k_rows:
+            queries.update(range(r, min(n, r + w.w1)))
+        for r in kp_rows:
+            queries.update(range(r, min(n, r + w.w2)))
+        rows = [q_rows, k_rows, kp_rows, k_rows, kp_rows]
+        arrs = P.head_arrays(inputs, b, h)
+        ref = oracle_pool.backward(*arrs, w.w1, w.w2, w.scale, sorted(queries), rows)
+        got = [P.to64(g[b, :, h][torch.tensor(r, device=g.device)]) for g, r in zip(grads, rows)]
+        P.check_grads(got, ref, w.dtype, f"fused {w.name} head {(b, h)}: dq {len(q_rows)} rows, "
+                      f"dk/dv {len(k_rows)}, dk'/dv' {len(kp_rows)} ({len(queries)} oracle queries)")
 
 
 def test_unit_values_through_gpu():
