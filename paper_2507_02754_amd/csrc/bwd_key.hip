@@ -108,8 +108,9 @@ __device__ __forceinline__ void key_body(
   static_assert(!FUSED || (G == 1 && FORM == 0), "fused backward: w2 <= 32, trilinear logits");
   using L = KeyLds<D, FUSED>;
   using T = typename L::T;
-  constexpr int IPT = T::CH / 8;  // tile items (row, 16-byte chunk) per thread and role
-  constexpr int RPI = 32 / IPT;   // rows covered by one pass of a role's 256 threads
+  // tile items (row, 16-byte chunk) per thread of a forming role (64 NKG threads)
+  constexpr int IPT = T::CH / (2 * key_groups<FUSED>());
+  constexpr int RPI = 32 / IPT;   // rows covered by one pass of a role's threads
   constexpr int NKG = L::NKG, KW = L::KW;
   __shared__ __attribute__((aligned(16))) char smem[L::bytes];
 
@@ -341,7 +342,9 @@ __device__ __forceinline__ void key_body(
                                            16 * (chunk ^ ((d >> 1) & 7)) + 2 * pos) = val;
       }
     }
-  } else {
+  }
+  // tiles 0 and 1 (fused: role B forms the do~ halves, role C the q~ halves)
+  if (FUSED ? role == 1 : true) {
     fetch(0, ic<0>{});
     form_put(0, ic<0>{});
     fetch(1, ic<0>{});
@@ -584,7 +587,7 @@ __device__ __forceinline__ void key_body(
         for (int uu = 0; uu < 2; ++uu)
 #pragma unroll
           for (int dt = 0; dt < NDT; ++dt) acc[dt] = mfma32(df[uu], qtr[uu][dt], acc[dt]);
-        if constexpr (!FUSED) form_put(S2 * L::tileBytes, ic<0>{});
+        form_put(S2 * L::tileBytes, ic<0>{});
         __builtin_amdgcn_sched_group_barrier(0x100, 2 + NT, 0);  // P, do~ row fragments
 #pragma unroll
         for (int x = 0; x < NT; ++x) {
@@ -618,9 +621,9 @@ __device__ __forceinline__ void key_body(
             for (int dt = 0; dt < NDT; ++dt) acc[dt] = mfma32(df, qtr[uu][dt], acc[dt]);
           }
         }
-        if constexpr (!FUSED) form_put(S2 * L::tileBytes, ic<0>{});
+        form_put(S2 * L::tileBytes, ic<0>{});
       }
-      if constexpr (!FUSED) fetch(rb + 3, ic<0>{});
+      fetch(rb + 3, ic<0>{});
       dpcur = dpnext;
       __builtin_amdgcn_s_setprio(0);
       lds_barrier();
@@ -654,26 +657,26 @@ __device__ __forceinline__ void key_body(
     auto ktfrag = [&](int tens, int g, int uu) __attribute__((always_inline)) {
       return lds_ld<u32x4_t>(lds + ktb + tens * D * L::ktRow + 16 * ((4 * g + 2 * uu) ^ ktm));
     };
-    // Tile formation for roles A and B (rows in k mod 32 order): thread u of
-    // this role forms rows rho + RPI y, chunk dc, of both halves of tile rb + 2
-    // in iteration rb: q~ = q_i o k'_k from loads issued two iterations
-    // earlier (two register sets), do~ = dO_i o v'_k from loads issued one
-    // iteration earlier.
+    // q~ half of the tiles for role A (rows in k mod 32 order; role B forms
+    // the do~ half): thread fu forms rows frho + RPIC y, chunk fdc, of tile
+    // rb + 2 in iteration rb from loads issued two iterations earlier (two
+    // register sets).
+    constexpr int IPTC = T::CH / 8, RPIC = 32 / IPTC;  // items per thread of role C's 256
     const int fu = xs * 64 + lane;
-    const int frho = fu % RPI, fdc = fu / RPI;
-    const __amdgpu_buffer_rsrc_t rkp_f = make_rsrc(kp + base, hb), rvp_f = make_rsrc(vp + base, hb);
-    int foff[IPT];
+    const int frho = fu % RPIC, fdc = fu / RPIC;
+    const __amdgpu_buffer_rsrc_t rkp_f = make_rsrc(kp + base, hb);
+    int foff[IPTC];
 #pragma unroll
-    for (int y = 0; y < IPT; ++y) foff[y] = T::off(frho + RPI * y, fdc);
-    u32x4_t cq[2], cm[2][IPT], co, cn[IPT];
-    float cbq[2][IPT], cbo[IPT];
+    for (int y = 0; y < IPTC; ++y) foff[y] = T::off(frho + RPIC * y, fdc);
+    u32x4_t cq[2], cm[2][IPTC];
+    float cbq[2][IPTC];
     auto fetch_rows = [&](int rb, __amdgpu_buffer_rsrc_t rr, __amdgpu_buffer_rsrc_t rm, float bias, u32x4_t& xr,
                           u32x4_t* xm, float* xb) __attribute__((always_inline)) {
       const int i = j0 + rb;
       xr = ldbuf128(rr, i * rsb + 16 * fdc);
 #pragma unroll
-      for (int y = 0; y < IPT; ++y) {
-        const int kk = i - ((i - frho - RPI * y) & 31);
+      for (int y = 0; y < IPTC; ++y) {
+        const int kk = i - ((i - frho - RPIC * y) & 31);
         const bool inwin = kk > i - w2 && (!BIAS || kk >= 0);
         xm[y] = ldbuf128(rm, inwin ? kk * rsb + 16 * fdc : -1);
         xb[y] = inwin ? bias : 0.f;
@@ -687,7 +690,7 @@ __device__ __forceinline__ void key_body(
         hi[e] = bf16_hi(xr[e]);
       }
 #pragma unroll
-      for (int y = 0; y < IPT; ++y) {
+      for (int y = 0; y < IPTC; ++y) {
         u32x4_t a4;
 #pragma unroll
         for (int e = 0; e < 4; ++e)
@@ -700,7 +703,6 @@ __device__ __forceinline__ void key_body(
       constexpr int X = decltype(set)::value;
       fetch_rows(rb, rq, rkp_f, s.kp_bias, cq[X], cm[X], cbq[X]);
     };
-    auto fetcho = [&](int rb) __attribute__((always_inline)) { fetch_rows(rb, rdo, rvp_f, s.vp_bias, co, cn, cbo); };
     // Key group g reaches row block rb (the test of is_active for group g).
     auto gact = [&](int rb, int g) {
       const int i = j0 + rb, jg = j0 + 32 * g;
@@ -752,22 +754,19 @@ __device__ __forceinline__ void key_body(
     // dO_i of row block rb (its U~), q_i and k'_i of row block rb - 1 (its dQ~),
     // each loaded one iteration ahead.
     float do_c = ld1(rdo, j0), q_c = 0.f, kp_c = 0.f;
-    // tiles 0 and 1, loads for tiles 2 (both halves) and 3 (q~ half)
+    // q~ halves of tiles 0 and 1, loads for tiles 2 and 3
     fetchq(0, ic<0>{});
-    fetcho(0);
     put_rows(0, cq[0], cm[0], cbq[0]);
-    put_rows(T::bytes, co, cn, cbo);
     fetchq(1, ic<0>{});
-    fetcho(1);
     put_rows(L::tileBytes, cq[0], cm[0], cbq[0]);
-    put_rows(L::tileBytes + T::bytes, co, cn, cbo);
     fetchq(2, ic<0>{});
     fetchq(3, ic<1>{});
-    fetcho(2);
     __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
     lds_barrier();  // tiles 0, 1 and K^T, V^T written (the barrier after the roles' first loads)
     lds_barrier();  // the prologue barrier of roles A and B
     auto step = [&](int rb, auto slot, auto guard) __attribute__((always_inline)) {
+      // priority above roles A and B: role C's work bounds the iteration
+      __builtin_amdgcn_s_setprio(2);
       constexpr int S = decltype(slot)::value;
       constexpr bool kGuard = decltype(guard)::value != 0;
       const int i = j0 + rb;
@@ -817,7 +816,6 @@ __device__ __forceinline__ void key_body(
         dv_update(ut);
         dq_update(qt);
         put_rows(S2 * L::tileBytes, cq[S & 1], cm[S & 1], cbq[S & 1]);
-        put_rows(S2 * L::tileBytes + T::bytes, co, cn, cbo);
       } else {
         if (rb < nrb) {
           f32x16_t ut = {};
@@ -843,11 +841,9 @@ __device__ __forceinline__ void key_body(
           dq_update(qt);
         }
         put_rows(S2 * L::tileBytes, cq[S & 1], cm[S & 1], cbq[S & 1]);
-        put_rows(S2 * L::tileBytes + T::bytes, co, cn, cbo);
       }
-      // the loads for tiles rb + 4 (q~) and rb + 3 (do~)
+      // the loads for tile rb + 4
       fetchq(rb + 4, ic<S & 1>{});
-      fetcho(rb + 3);
       do_c = do_n;
       q_c = q_n;
       kp_c = kp_n;
@@ -856,6 +852,7 @@ __device__ __forceinline__ void key_body(
       pin16(dvr);
       pin16(dkr);
       pin16(kpr);
+      __builtin_amdgcn_s_setprio(0);
       lds_barrier();
     };
     run_loops(step);
