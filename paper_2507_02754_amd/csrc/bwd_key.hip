@@ -807,15 +807,16 @@ __device__ __forceinline__ void key_body(
             qt = mfma32(xfrag((L::dsOff - L::xOff) + ((S + 1) & 1) * L::xBuf + 2048 * g + 256 * uu),
                         ktfrag(0, g, uu), qt);
           }
+        put_rows(S2 * L::tileBytes, cq[S & 1], cm[S & 1], cbq[S & 1]);
 #pragma unroll
         for (int x = 0; x < 4 * NKG; ++x) {
           __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);  // operand reads
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // product
+          __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);  // formation
         }
         __builtin_amdgcn_sched_barrier(0);
         dv_update(ut);
         dq_update(qt);
-        put_rows(S2 * L::tileBytes, cq[S & 1], cm[S & 1], cbq[S & 1]);
       } else {
         if (rb < nrb) {
           f32x16_t ut = {};
