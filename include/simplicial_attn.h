@@ -204,18 +204,23 @@ int simplicial_attn_det_bwd(const void* q, const void* k, const void* kp, const 
  * Backward with grouped-query attention, for the outputs of
  * simplicial_attn_fwd_gqa. Every K-side element enters the logits of all the
  * query heads of its group, so dK, dK', dV, dV' are the per-query-head
- * gradients summed over the group (in fp32, query heads in ascending order,
- * rounded once to dtype: bitwise deterministic).
+ * gradients summed over the group (bitwise deterministic). dK', dV': each
+ * query head's gradient in dtype, summed in fp32 in ascending head order and
+ * rounded once. dK, dV: on the MFMA kernels (bf16, D 64 or 128, w2 <= 64) the
+ * key-stationary kernel reads K, K', V, V' in place and accumulates the whole
+ * group in fp32 before rounding once; otherwise as dK', dV'.
  *   q, out, dout, dq        [B, N, H, D], dtype
  *   k, kp, v, vp            [B, N, Hkv, D], dtype
  *   dk, dkp, dv, dvp        [B, N, Hkv, D], dtype, fully overwritten
  *   lse                     [B, H, N] float32 from the forward
  *   workspace               at least simplicial_attn_bwd_gqa_workspace_size()
  *                           bytes, 16-byte aligned; contents on entry ignored.
- *                           For Hkv < H it holds K, K', V, V' expanded to H
- *                           heads and the per-query-head K-side gradients
- *                           (8 tensors of B*N*H*D elements) besides what
- *                           simplicial_attn_bwd needs.
+ *                           For Hkv < H it holds, besides what
+ *                           simplicial_attn_bwd needs, the per-query-head
+ *                           dK', dV' (MFMA kernels: 2 tensors of B*N*H*D
+ *                           elements), or K, K', V, V' expanded to H heads
+ *                           and all four per-query-head K-side gradients
+ *                           (other shapes: 8 such tensors).
  *   Hkv                     as simplicial_attn_fwd_gqa (else SA_ERR_INVALID)
  * Other arguments and errors as simplicial_attn_bwd; Hkv == H is exactly
  * simplicial_attn_bwd. The workspace size function returns 0 for arguments

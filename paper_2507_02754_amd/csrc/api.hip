@@ -95,11 +95,17 @@ size_t det_workspace_bytes_for(int64_t B, int64_t N, int64_t H, int64_t D, int32
 }
 
 // Backward workspace with Hkv K-side heads: the per-head backward's workspace,
-// then (Hkv < H only) K, K', V, V' expanded to H heads and the per-query-head
-// dK, dK', dV', dV before the group sum, each [B, N, H, D] of the data type.
+// then (Hkv < H only) per-query-head gradients of the data type, each
+// [B, N, H, D]: on the MFMA path dK' and dV' (the key side sums the group
+// itself), on the generic path K, K', V, V' expanded to H heads and dK, dK',
+// dV, dV' before the group sum.
 struct GqaLayout {
   size_t base, per_tensor, bytes;
 };
+
+// Whether the grouped-query backward takes the MFMA kernels with the K side
+// read in place (no expansion).
+bool gqa_native(const Shape& s) { return s.form == 0 && sa::mfma_bwd_supported(s); }
 
 GqaLayout gqa_layout(int64_t B, int64_t N, int64_t H, int64_t Hkv, int64_t D, int32_t w1,
                      int32_t w2, int32_t dtype) {
@@ -113,7 +119,8 @@ GqaLayout gqa_layout(int64_t B, int64_t N, int64_t H, int64_t Hkv, int64_t D, in
   }
   const size_t esize = dtype == SA_DTYPE_BF16 ? 2 : 4;
   l.per_tensor = (static_cast<size_t>(B * N * H * D) * esize + 255) & ~size_t(255);
-  l.bytes = l.base + 8 * l.per_tensor;
+  const bool native = gqa_native(make_shape(B, N, H, D, w1, w2, 1.0f, dtype));
+  l.bytes = l.base + (native ? 2 : 8) * l.per_tensor;
   return l;
 }
 
@@ -470,6 +477,22 @@ int simplicial_attn_bwd_gqa(const void* q, const void* k, const void* kp, const 
   s.Hkv = static_cast<int>(Hkv);
   hipStream_t st = static_cast<hipStream_t>(stream);
   char* ws = static_cast<char*>(workspace);
+  if (gqa_native(s)) {
+    // K side read in place: the query side writes each query head's dK', dV'
+    // (summed over the group afterwards), the key side accumulates dK, dV
+    // over the group's query heads itself.
+    void* gkp = ws + l.base;
+    void* gvp = ws + l.base + l.per_tensor;
+    int r = run_delta(s, Path::Mfma, out, dout, workspace, st);
+    if (r != SA_OK) return r;
+    r = run_stage(s, Path::Mfma, BwdStage::Query, q, k, kp, v, vp, dout, lse, dq, gkp, gvp, workspace, st);
+    if (r != SA_OK) return r;
+    r = run_stage(s, Path::Mfma, BwdStage::Key, q, k, kp, v, vp, dout, lse, dk, dv, nullptr, workspace, st);
+    if (r != SA_OK) return r;
+    const void* gsrc[4] = {gkp, gvp, nullptr, nullptr};
+    void* gdst[4] = {dkp, dvp, nullptr, nullptr};
+    return to_status(sa::gqa_group_sum(s, gsrc, gdst, st, 2));
+  }
   void* ex[4];  // K, K', V, V' expanded to H heads
   void* gx[4];  // per-query-head dK, dK', dV, dV'
   for (int t = 0; t < 4; ++t) {

@@ -114,14 +114,20 @@ __device__ __forceinline__ void key_body(
   constexpr int NKG = L::NKG, KW = L::KW;
   __shared__ __attribute__((aligned(16))) char smem[L::bytes];
 
+  // Grouped-query attention: a workgroup owns keys of one K-side head hk and
+  // walks the row blocks of its QG query heads hk QG .. hk QG + QG - 1 in turn
+  // (dK, dV accumulate over all of them).
+  // The fused kernel runs with one query head per K-side head only.
+  const int Hkv = FUSED ? s.H : s.Hkv, QG = FUSED ? 1 : s.H / s.Hkv;
   const int jblocks = (s.N + KW - 1) / KW;
-  const int total = jblocks * s.B * s.H;
+  const int total = jblocks * s.B * Hkv;
   const int per_xcd = (total + 7) / 8;
   const int logical = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
   if (logical >= total) return;
-  const int bh = logical / jblocks;
-  const int jblk = logical - bh * jblocks;
-  const int b = bh / s.H, hh = bh - b * s.H;
+  const int bk = logical / jblocks;
+  const int jblk = logical - bk * jblocks;
+  const int b = bk / Hkv, hk = bk - b * Hkv;
+  const int bh = b * s.H + hk * QG;  // (batch, first query head)
 
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -138,23 +144,26 @@ __device__ __forceinline__ void key_body(
   const bool roleA = role == 0;
   const int kg = roleA ? wave : NKG == 4 ? (wave + 2) & 3 : wave - NKG;  // key group (A, B)
   const int lane = tid & 63, c = lane & 31, h = lane >> 5;
-  const int rsb = s.H * D * 2;  // bytes between rows
-  const size_t base = (static_cast<size_t>(b) * s.N * s.H + hh) * D;
+  const int rsb = s.H * D * 2;   // bytes between rows of q, dO
+  const int rsbk = Hkv * D * 2;  // bytes between rows of K, K', V, V', dK, dV
+  const size_t basek = (static_cast<size_t>(b) * s.N * Hkv + hk) * D;
+  // q, dO of the group's first query head; head hg of the group is hg * 2 D bytes further
+  const size_t base = (static_cast<size_t>(b) * s.N * s.H + hk * QG) * D;
   const int N = s.N, w1 = s.w1, w2 = s.w2;
   const float qscale = s.scale * kLog2e;
-  const size_t stat = static_cast<size_t>(bh) * N;
+  const size_t stat = static_cast<size_t>(bh) * N;  // LSE / Delta of the group's first query head
   const int j0 = jblk * KW;
   const int jw = j0 + 32 * kg;  // keys jw .. jw + 31 of this wavefront
   const int jme = jw + c;       // key of this lane's accumulator column
-  const unsigned hb = head_bytes(N, rsb, D);
+  const unsigned hb = head_bytes(N, rsb, D) + (QG - 1) * 2 * D, hbk = head_bytes(N, rsbk, D);
 
   // K (role A) or V (role B) rows of the group as B operands: lane (h, c) holds
   // key jw + c, d = 16 t + 8 h .. + 7. Keys past the end load as zeros.
   u32x4_t kv[NT];
   if (role < 2) {
-    const __amdgpu_buffer_rsrc_t r = make_rsrc((roleA ? k : v) + base, hb);
+    const __amdgpu_buffer_rsrc_t r = make_rsrc((roleA ? k : v) + basek, hbk);
 #pragma unroll
-    for (int t = 0; t < NT; ++t) kv[t] = ldbuf128(r, jme * rsb + 32 * t + 16 * h);
+    for (int t = 0; t < NT; ++t) kv[t] = ldbuf128(r, jme * rsbk + 32 * t + 16 * h);
   }
   f32x16_t acc[NDT];
 #pragma unroll
@@ -209,7 +218,7 @@ __device__ __forceinline__ void key_body(
   const int u = kg * 64 + lane;  // index of this thread within its role
   const int rho = u % RPI, dc = u / RPI;
   const __amdgpu_buffer_rsrc_t rrow = make_rsrc((roleA ? q : dout) + base, hb);
-  const __amdgpu_buffer_rsrc_t rmod = make_rsrc((roleA ? kp : vp) + base, hb);
+  const __amdgpu_buffer_rsrc_t rmod = make_rsrc((roleA ? kp : vp) + basek, hbk);
   int formoff[IPT];
 #pragma unroll
   for (int y = 0; y < IPT; ++y) formoff[y] = T::off(rho + RPI * y, dc) + (roleA ? 0 : T::bytes);
@@ -224,14 +233,33 @@ __device__ __forceinline__ void key_body(
   // out-of-range offsets load zeros and are not used).
   unsigned frw[2][2], fmw[2][IPT][2];
   const float mbias = roleA ? s.kp_bias : s.vp_bias;
+  // Row blocks of a workgroup: those of query head 0 of the group, padded to
+  // nrb4, then those of head 1, ... (R = hg nrb4 + rb). The steps take the
+  // local rb of head hg; loc / hof map rb + k (k <= 4, possibly past the end
+  // of head hg) to its local index and head.
+  int hg = 0;
+  auto loc = [&](int r) {
+    if constexpr (FUSED)
+      return r;
+    else
+      return r < nrb4 ? r : r - nrb4;
+  };
+  auto hof = [&](int r) {
+    if constexpr (FUSED)
+      return 0;
+    else
+      return r < nrb4 ? hg : hg + 1;
+  };
   auto fetch = [&](int rb, auto set) __attribute__((always_inline)) {
     constexpr int X = decltype(set)::value;
-    const int i = j0 + rb / G, g = rb % G;
-    fr[X] = ldbuf128(rrow, i * rsb + 16 * dc);
+    const int r = loc(rb), hq = hof(rb);  // row block r of query head hq of the group
+    const int i = j0 + r / G, g = r % G;
+    const int qoff = hq < QG ? i * rsb + hq * 2 * D + 16 * dc : -1;
+    fr[X] = ldbuf128(rrow, qoff);
     if constexpr (FORM == 1) {
       if (roleA) {
-        frw[X][0] = ldbuf32(rrow, i * rsb + 16 * dc - 4);
-        frw[X][1] = ldbuf32(rrow, i * rsb + 16 * dc + 16);
+        frw[X][0] = ldbuf32(rrow, qoff - 4);
+        frw[X][1] = ldbuf32(rrow, qoff + 16);
       }
     }
 #pragma unroll
@@ -239,11 +267,11 @@ __device__ __forceinline__ void key_body(
       // fused: row rho + RPI y of the tile holds the k-row congruent to it mod 32
       const int kk = FUSED ? i - ((i - rho - RPI * y) & 31) : i - W2P + 1 + 32 * g + rho + RPI * y;
       const bool inwin = kk > i - w2 && (!BIAS || kk >= 0);  // kk < 0 also loads zeros
-      fm[X][y] = ldbuf128(rmod, inwin ? kk * rsb + 16 * dc : -1);
+      fm[X][y] = ldbuf128(rmod, inwin ? kk * rsbk + 16 * dc : -1);
       if constexpr (FORM == 1) {
         if (roleA) {
-          fmw[X][y][0] = ldbuf32(rmod, inwin ? kk * rsb + 16 * dc - 4 : -1);
-          fmw[X][y][1] = ldbuf32(rmod, inwin ? kk * rsb + 16 * dc + 16 : -1);
+          fmw[X][y][0] = ldbuf32(rmod, inwin ? kk * rsbk + 16 * dc - 4 : -1);
+          fmw[X][y][1] = ldbuf32(rmod, inwin ? kk * rsbk + 16 * dc + 16 : -1);
         }
       }
       if constexpr (BIAS) fb[X][y] = inwin ? mbias : 0.f;
@@ -294,13 +322,14 @@ __device__ __forceinline__ void key_body(
   };
 
   // Per-row-block statistic, 64 row blocks at a time: lane l holds the value
-  // of row block (rb & ~63) + l (A: -LSE * log2 e, B: Delta), taken with a
+  // of row block (R & ~63) + l (A: -LSE * log2 e, B: Delta), taken with a
   // lane read. The next 64 values are loaded half a window ahead. stat_at
-  // must be called for every row block in order.
+  // must be called for every row block in order (R = hg nrb4 + rb).
   const float* statp = roleA ? lse : delta;
-  auto stat_load = [&](int rb0) {
-    const int ii = min(j0 + (rb0 + lane) / G, N - 1);
-    const float x = statp[stat + ii];
+  auto stat_load = [&](int rb0) {  // rb0: R of the first of 64 row blocks
+    const int rg = rb0 + lane, hq = FUSED ? 0 : rg / nrb4;
+    const int ii = min(j0 + (rg - hq * nrb4) / G, N - 1);
+    const float x = statp[stat + static_cast<size_t>(min(hq, QG - 1)) * N + ii];
     return roleA ? -x * kLog2e : x;
   };
   float st_l = stat_load(0), st_nx = 0.f;
@@ -326,11 +355,11 @@ __device__ __forceinline__ void key_body(
   // 32 g + 16 u + 8 + 4 h + {0..3}: the 8 keys, in the order of the P and dS
   // fragments, that lane half h needs for MFMA (g, u).
   if constexpr (FUSED) {
-    const __amdgpu_buffer_rsrc_t rk = make_rsrc(k + base, hb), rv = make_rsrc(v + base, hb);
+    const __amdgpu_buffer_rsrc_t rk = make_rsrc(k + basek, hbk), rv = make_rsrc(v + basek, hbk);
     constexpr int NTH = key_threads<D, FUSED>();
     for (int x = tid; x < 2 * KW * T::CH; x += NTH) {
       const int tens = x / (KW * T::CH), key = (x / T::CH) % KW, ch = x % T::CH;
-      const u32x4_t w = ldbuf128(tens ? rv : rk, (j0 + key) * rsb + 16 * ch);
+      const u32x4_t w = ldbuf128(tens ? rv : rk, (j0 + key) * rsbk + 16 * ch);
       const int r16 = key & 15;
       const int chunk = 4 * (key >> 5) + 2 * ((key >> 4) & 1) + ((r16 >> 2) & 1);
       const int pos = 4 * (r16 >> 3) + (r16 & 3);
@@ -372,10 +401,12 @@ __device__ __forceinline__ void key_body(
       step(rb + 2, ic<2>{}, guard);
       step(rb + 3, ic<3>{}, guard);
     };
-    int rb = 0;
-    for (; rb < rb_lo; rb += kSlots) quad(rb, ic<1>{});
-    for (; rb < rb_hi; rb += kSlots) quad(rb, ic<0>{});
-    for (; rb < nrb4; rb += kSlots) quad(rb, ic<1>{});
+    for (hg = 0; hg < QG; ++hg) {
+      int rb = 0;
+      for (; rb < rb_lo; rb += kSlots) quad(rb, ic<1>{});
+      for (; rb < rb_hi; rb += kSlots) quad(rb, ic<0>{});
+      for (; rb < nrb4; rb += kSlots) quad(rb, ic<1>{});
+    }
   };
 
   if (roleA) {
@@ -392,7 +423,7 @@ __device__ __forceinline__ void key_body(
     // P of row block rb from its logits, packed, and written to the exchange
     // buffer at xb for the partner.
     auto probs = [&](int rb, float nlse2, const f32x16_t& sacc, int xb, u32x4_t* pf) __attribute__((always_inline)) {
-      const int i = j0 + rb / G;
+      const int i = j0 + loc(rb) / G;
       const bool colok = jme <= i && jme > i - w1 && jme < N;
       const float nl = nlse2 - (colok ? 0.f : __builtin_inff());
       // p = 2^min(x, 0): at most 1, so rows formed as zeros (whose statistic
@@ -436,8 +467,8 @@ __device__ __forceinline__ void key_body(
       constexpr int S1 = (S + 1) % kSlots, S2 = (S + 2) % kSlots;
       constexpr bool kGuard = decltype(guard)::value != 0;
       const bool act0 = !kGuard || is_active(rb, j0 + rb / G);
-      const bool act1 = !kGuard || is_active(rb + 1, j0 + (rb + 1) / G);
-      const float nl1 = stat_at(rb + 1);
+      const bool act1 = !kGuard || is_active(loc(rb + 1), j0 + loc(rb + 1) / G);
+      const float nl1 = stat_at(hg * nrb4 + rb + 1);
       f32x16_t snext;
       u32x4_t pnext[2];
       if constexpr (!kGuard && FUSED) {
@@ -557,8 +588,8 @@ __device__ __forceinline__ void key_body(
       constexpr int S1 = (S + 1) % kSlots, S2 = (S + 2) % kSlots;
       constexpr bool kGuard = decltype(guard)::value != 0;
       const bool act0 = !kGuard || is_active(rb, j0 + rb / G);
-      const bool act1 = !kGuard || is_active(rb + 1, j0 + (rb + 1) / G);
-      const float dlt = stat_at(rb);
+      const bool act1 = !kGuard || is_active(loc(rb + 1), j0 + loc(rb + 1) / G);
+      const float dlt = stat_at(hg * nrb4 + rb);
       f32x16_t dpnext;
       if constexpr (!kGuard && !FUSED) {
         // Straight-line: reads first, then the dP products of row block rb + 1
@@ -640,7 +671,7 @@ __device__ __forceinline__ void key_body(
     // second read) in the slot 32 (l & 1) + (key ^ (8 (l & 1) + 4 u')) of
     // block u' = (lane / 16) & 1.
     const __amdgpu_buffer_rsrc_t rq = make_rsrc(q + base, hb), rdo = make_rsrc(dout + base, hb),
-                                 rkp = make_rsrc(kp + base, hb);
+                                 rkp = make_rsrc(kp + basek, hbk);
     const int grp = lane >> 4, sl = lane & 15;
     const int hp = grp >> 1, uq = grp & 1, hs1 = sl & 1;
     const int xr0 = L::xOff + 1024 * uq + 512 * hs1 + 16 * (8 * hs1 + 4 * (hp ^ uq) + (sl >> 2)) +
@@ -664,7 +695,7 @@ __device__ __forceinline__ void key_body(
     constexpr int IPTC = T::CH / 8, RPIC = 32 / IPTC;  // items per thread of role C's 256
     const int fu = xs * 64 + lane;
     const int frho = fu % RPIC, fdc = fu / RPIC;
-    const __amdgpu_buffer_rsrc_t rkp_f = make_rsrc(kp + base, hb);
+    const __amdgpu_buffer_rsrc_t rkp_f = make_rsrc(kp + basek, hbk);
     int foff[IPTC];
 #pragma unroll
     for (int y = 0; y < IPTC; ++y) foff[y] = T::off(frho + RPIC * y, fdc);
@@ -678,7 +709,7 @@ __device__ __forceinline__ void key_body(
       for (int y = 0; y < IPTC; ++y) {
         const int kk = i - ((i - frho - RPIC * y) & 31);
         const bool inwin = kk > i - w2 && (!BIAS || kk >= 0);
-        xm[y] = ldbuf128(rm, inwin ? kk * rsb + 16 * fdc : -1);
+        xm[y] = ldbuf128(rm, inwin ? kk * rsbk + 16 * fdc : -1);
         xb[y] = inwin ? bias : 0.f;
       }
     };
@@ -735,15 +766,15 @@ __device__ __forceinline__ void key_body(
       for (int qq = 0; qq < 4; ++qq) r[4 * qq + S3] = (mine && q4 == qq) ? x : r[4 * qq + S3];
     };
     // Element col of row `row` (0 outside the sequence).
-    auto ld1 = [&](__amdgpu_buffer_rsrc_t r, int row) {
-      return bf16_to_f32(__builtin_amdgcn_raw_buffer_load_b16(r, row * rsb + 2 * col, 0, 0));
+    auto ld1 = [&](__amdgpu_buffer_rsrc_t r, int row, int stride) {
+      return bf16_to_f32(__builtin_amdgcn_raw_buffer_load_b16(r, row * stride + 2 * col, 0, 0));
     };
     float dvr[16], dkr[16], kpr[16];
 #pragma unroll
     for (int vv = 0; vv < 16; ++vv) {
       // k' ring for the row block before the first: k-rows j0 - 32 .. j0 - 1
       const int kap = j0 - 32 + acc_row(vv, h);
-      kpr[vv] = plus_bias<BIAS>(ld1(rkp, kap), kap >= 0 ? s.kp_bias : 0.f);
+      kpr[vv] = plus_bias<BIAS>(ld1(rkp, kap, rsbk), kap >= 0 ? s.kp_bias : 0.f);
       dvr[vv] = 0.f;
       dkr[vv] = 0.f;
     }
@@ -753,7 +784,7 @@ __device__ __forceinline__ void key_body(
     float* const pv = part + fp.pv_off + wg * fp.RK * D + col - (j0 - 31) * D;
     // dO_i of row block rb (its U~), q_i and k'_i of row block rb - 1 (its dQ~),
     // each loaded one iteration ahead.
-    float do_c = ld1(rdo, j0), q_c = 0.f, kp_c = 0.f;
+    float do_c = ld1(rdo, j0, rsb), q_c = 0.f, kp_c = 0.f;
     // q~ halves of tiles 0 and 1, loads for tiles 2 and 3
     fetchq(0, ic<0>{});
     put_rows(0, cq[0], cm[0], cbq[0]);
@@ -770,7 +801,7 @@ __device__ __forceinline__ void key_body(
       constexpr int S = decltype(slot)::value;
       constexpr bool kGuard = decltype(guard)::value != 0;
       const int i = j0 + rb;
-      const float do_n = ld1(rdo, i + 1), q_n = ld1(rq, i), kp_n = ld1(rkp, i);
+      const float do_n = ld1(rdo, i + 1, rsb), q_n = ld1(rq, i, rsb), kp_n = ld1(rkp, i, rsbk);
       constexpr int S2 = (S + 2) % kSlots;
       // dv' from U~ of row block rb; dq and dk' from dQ~ of row block rb - 1
       // (k' ring for query i - 1 first)
@@ -898,7 +929,7 @@ __device__ __forceinline__ void key_body(
           u32x4_t w;
 #pragma unroll
           for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(src[2 * e], src[2 * e + 1]);
-          *reinterpret_cast<u32x4_t*>(dst + base + static_cast<size_t>(j) * s.H * D + 8 * col) = w;
+          *reinterpret_cast<u32x4_t*>(dst + basek + static_cast<size_t>(j) * Hkv * D + 8 * col) = w;
         }
       }
     }
@@ -928,7 +959,7 @@ hipError_t launch_key(const Shape& s, const void* q, const void* k, const void* 
                       const void* vp, const void* dout, const float* lse, const float* delta, void* dk,
                       void* dv, hipStream_t st, const FusedPlan& fp = FusedPlan{}, float* part = nullptr) {
   constexpr int KW = 32 * key_groups<FUSED>();
-  const long tot = static_cast<long>((s.N + KW - 1) / KW) * s.B * s.H;
+  const long tot = static_cast<long>((s.N + KW - 1) / KW) * s.B * s.Hkv;
   auto kern = [] {
     if constexpr (FUSED)
       return bwd_fused_kernel<D, BIAS>;

@@ -163,8 +163,11 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
   float* ws_tail_kp = ws_head_vp + plan.halo_floats;
   float* ws_tail_vp = ws_tail_kp + plan.halo_floats;
   const int rsb = static_cast<int>(rs) * 2;
-  const unsigned hb = head_bytes(N, rsb, D);
-  const __amdgpu_buffer_rsrc_t rk = make_rsrc(k + base, hb), rv = make_rsrc(v + base, hb);
+  // K, K', V, V' of the K-side head of query head hh (grouped-query attention)
+  const int rsbk = s.Hkv * D * 2;
+  const size_t basek = (static_cast<size_t>(b) * s.N * s.Hkv + hh / (s.H / s.Hkv)) * D;
+  const unsigned hb = head_bytes(N, rsb, D), hbk = head_bytes(N, rsbk, D);
+  const __amdgpu_buffer_rsrc_t rk = make_rsrc(k + basek, hbk), rv = make_rsrc(v + basek, hbk);
 
   for (int x = tid; x < 2 * RB * L::rStride; x += NTH) ring_kp[x] = 0.f;
 
@@ -199,10 +202,11 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
   // zeros from the buffer range check. A tile's k' and v' rows (and q, dO of
   // its queries) are in the rings before its prologue; the RL rows after them
   // are loaded during the tile and written in its epilogue.
-  const __amdgpu_buffer_rsrc_t rrow = make_rsrc(
-      (wave == 0 ? kp : wave == 1 ? vp : wave == 2 ? q : dout) + base, hb);
+  const __amdgpu_buffer_rsrc_t rrow = wave < 2 ? make_rsrc((wave == 0 ? kp : vp) + basek, hbk)
+                                                : make_rsrc((wave == 2 ? q : dout) + base, hb);
+  const int rrsb = wave < 2 ? rsbk : rsb;
   const int rl_row = lane / T::CH, rl_ch = lane % T::CH;
-  auto row_load = [&](int r0) { return ldbuf128(rrow, (r0 + rl_row) * rsb + 16 * rl_ch); };
+  auto row_load = [&](int r0) { return ldbuf128(rrow, (r0 + rl_row) * rrsb + 16 * rl_ch); };
   auto row_put = [&](int r0, u32x4_t x) {
     const int r = r0 + rl_row;
     if (wave < 2) {
@@ -244,7 +248,7 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
       const int kx = x * WAVES + wave;
       const int p = 64 * kx + lane;
       const int row = p / T::CH, ch = (p % T::CH) ^ T::swz(row);
-      const int off = kx < T::instrs ? (jb + row) * rsb + 16 * ch : -1;
+      const int off = kx < T::instrs ? (jb + row) * rsbk + 16 * ch : -1;
       skr[x] = ldbuf128(rk, off);
       svr[x] = ldbuf128(rv, off);
     }

@@ -104,6 +104,9 @@ __global__ __launch_bounds__(kQThreads, 1) void bwd_query_kernel(
   const size_t rs = static_cast<size_t>(s.H) * D;
   const int rsb = static_cast<int>(rs) * 2;
   const size_t base = (static_cast<size_t>(b) * s.N * s.H + hh) * D;
+  // K, K', V, V' of the K-side head of query head hh (grouped-query attention)
+  const int rsbk = s.Hkv * D * 2;
+  const size_t basek = (static_cast<size_t>(b) * s.N * s.Hkv + hh / (s.H / s.Hkv)) * D;
   const int N = s.N, w1 = s.w1, w2 = s.w2;
   const int cs = chunk * plan.CQ, ce = min(N, cs + plan.CQ);
   const int kbase = cs - W2P + 1;  // k-row k: acc ring row (k - kbase) % RB, k' ring row (k - kbase) % RK
@@ -114,7 +117,7 @@ __global__ __launch_bounds__(kQThreads, 1) void bwd_query_kernel(
   float* ws_head_vp = ws_head_kp + plan.halo_floats;
   float* ws_tail_kp = ws_head_vp + plan.halo_floats;
   float* ws_tail_vp = ws_tail_kp + plan.halo_floats;
-  const unsigned hb = head_bytes(N, rsb, D);
+  const unsigned hb = head_bytes(N, rsb, D), hbk = head_bytes(N, rsbk, D);
 
   for (int x = tid; x < 2 * RB * L::rStride; x += kQThreads) ring_kp[x] = 0.f;
 
@@ -147,10 +150,11 @@ __global__ __launch_bounds__(kQThreads, 1) void bwd_query_kernel(
   // load (0: k', 1: v', 2: q, 3: dO); rows outside [0, N) load as zeros ----
   const int rw = wave & 3;
   const bool rowloader = wave < 4;
-  const __amdgpu_buffer_rsrc_t rrow =
-      make_rsrc((rw == 0 ? kp : rw == 1 ? vp : rw == 2 ? q : dout) + base, hb);
+  const __amdgpu_buffer_rsrc_t rrow = rw < 2 ? make_rsrc((rw == 0 ? kp : vp) + basek, hbk)
+                                              : make_rsrc((rw == 2 ? q : dout) + base, hb);
+  const int rrsb = rw < 2 ? rsbk : rsb;
   const int rl_row = lane / T::CH, rl_ch = lane % T::CH;
-  auto row_load = [&](int r0) { return ldbuf128(rrow, (r0 + rl_row) * rsb + 16 * rl_ch); };
+  auto row_load = [&](int r0) { return ldbuf128(rrow, (r0 + rl_row) * rrsb + 16 * rl_ch); };
   auto row_put = [&](int r0, u32x4_t x) {
     const int r = r0 + rl_row;
     if (rw < 2) {
@@ -181,7 +185,7 @@ __global__ __launch_bounds__(kQThreads, 1) void bwd_query_kernel(
   const int nb = (w1 + QW - 1 + 31) / 32;
   const int ntiles = (ce - cs + QW - 1) / QW;
   const int total_it = ntiles * nb;
-  const __amdgpu_buffer_rsrc_t rk = make_rsrc(k + base, hb), rv = make_rsrc(v + base, hb);
+  const __amdgpu_buffer_rsrc_t rk = make_rsrc(k + basek, hbk), rv = make_rsrc(v + basek, hbk);
   const bool stager = wave < F::instrs;
   const int st_row = (64 * wave + lane) / F::CH, st_ch = (64 * wave + lane) % F::CH;
   const int st_slot = F::slot(st_row, st_ch);
@@ -189,7 +193,7 @@ __global__ __launch_bounds__(kQThreads, 1) void bwd_query_kernel(
   auto stage_fetch = [&](int it) {
     const int tile = it / nb, blk = it - tile * nb;
     const int jb = cs + tile * QW - w1 + 1 + 32 * blk;
-    const int off = stager && it < total_it ? (jb + st_row) * rsb + 16 * st_ch : -1;
+    const int off = stager && it < total_it ? (jb + st_row) * rsbk + 16 * st_ch : -1;
     skr = ldbuf128(rk, off);
     svr = ldbuf128(rv, off);
   };

@@ -109,7 +109,7 @@ hipError_t gqa_expand(const Shape& s, const void* const src[4], void* const dst[
 }
 
 hipError_t gqa_group_sum(const Shape& s, const void* const src[4], void* const dst[4],
-                         hipStream_t st) {
+                         hipStream_t st, int ntens) {
   Quad p;
   for (int t = 0; t < 4; ++t) {
     p.src[t] = src[t];
@@ -117,7 +117,7 @@ hipError_t gqa_group_sum(const Shape& s, const void* const src[4], void* const d
   }
   const int qpr = s.D / 4;
   const long long rows = static_cast<long long>(s.B) * s.N * s.Hkv;
-  const dim3 grid(grid_for(rows * qpr), 4);
+  const dim3 grid(grid_for(rows * qpr), ntens);
   if (s.dtype == SA_DTYPE_BF16)
     hipLaunchKernelGGL(group_sum_kernel<true>, grid, dim3(kThreads), 0, st, p, rows, s.H / s.Hkv,
                        qpr);

@@ -17,8 +17,10 @@ struct Shape {
   float scale;
   int dtype;  // SA_DTYPE_*
   // Heads of K, K', V, V' (grouped-query attention: query head h reads K/V
-  // head h / (H / Hkv)). Only the forward kernels and the GQA helpers below
-  // read it; the backward kernels run per query head with Hkv == H.
+  // head h / (H / Hkv)). The forward and the MFMA backward kernels read the
+  // K side with this head count (the key side walks a group's query heads;
+  // the query side writes per-query-head dK', dV' for gqa_group_sum); the
+  // generic backward runs with Hkv == H.
   int Hkv;
   // Logit form: 0 trilinear (Section 4), 1 sum of 3 x 3 determinants over
   // 3-component chunks (Section 5).
@@ -121,9 +123,10 @@ hipError_t mfma_bwd_query(const Shape& s, const BwdPlan& plan, const void* q, co
 hipError_t gqa_expand(const Shape& s, const void* const src[4], void* const dst[4],
                       hipStream_t st);
 // gqa_group_sum: dst[t] [B, N, Hkv, D] = fp32 sum over each group's query
-// heads (ascending) of src[t] [B, N, H, D], rounded once to the data type.
+// heads (ascending) of src[t] [B, N, H, D], rounded once to the data type,
+// for t < ntens.
 hipError_t gqa_group_sum(const Shape& s, const void* const src[4], void* const dst[4],
-                         hipStream_t st);
+                         hipStream_t st, int ntens = 4);
 
 // Delta_i = <dO_i, O_i> for every query, [B, H, N] float32.
 hipError_t launch_delta(const Shape& s, const void* out, const void* dout, float* delta,

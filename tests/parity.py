@@ -215,25 +215,58 @@ def gqa_oracle_backward(q, kv, do, w1, w2, scale, b_heads=None, queries=None):
     return dq, dkv
 
 
-def gqa_composite_backward(q, kv, out, do, lse, w1, w2, scale):
+def gqa_composite_backward(q, kv, out, do, lse, w1, w2, scale, with_abs=False):
     """The grouped-query backward composed from the library's per-head entry
     point on the GPU: K, K', V, V' repeated per query head, the plain backward,
     then each group's K-side gradients summed in fp32 in ascending head order
-    and rounded once. The library's GQA backward is specified to equal this bit
-    for bit."""
+    and rounded once. with_abs: also return, per K-side gradient, the fp32 sum
+    over each group of the per-query-head magnitudes (a bound's scale)."""
     H, Hkv = q.shape[2], kv[0].shape[2]
     g = H // Hkv
     rep = [x.repeat_interleave(g, dim=2).contiguous() for x in kv]
     grads = simplicial_attn_bwd(q, *rep, out, do, lse, w1, w2, scale)
     torch.cuda.synchronize()
-    summed = []
+    summed, mags = [], []
     for t in range(1, 5):
         x = grads[t].unflatten(2, (Hkv, g))
         acc = x[:, :, :, 0].float()
+        mag = acc.abs()
         for j in range(1, g):
             acc = acc + x[:, :, :, j].float()
+            mag = mag + x[:, :, :, j].float().abs()
         summed.append(acc.to(grads[t].dtype).contiguous())
-    return (grads[0], *summed)
+        mags.append(mag)
+    comp = (grads[0], *summed)
+    return (comp, [None, *mags]) if with_abs else comp
+
+
+def gqa_native(h, hkv, d, w2, dtype):
+    """Shapes whose grouped-query backward reads K, K', V, V' in place (MFMA
+    kernels): the key side sums dK, dV over a group's query heads in fp32
+    before rounding once, where the composite rounds each head's share first."""
+    return dtype == "bf16" and d in (64, 128) and w2 <= 64 and hkv < h
+
+
+def check_gqa_against_composite(grads, comp, mags, native, label=""):
+    """dQ, dK', dV' equal the composite bit for bit (same kernels, same group
+    sum). dK, dV on the native path: the composite rounds each query head's
+    share to bf16 (relative error 2^-9 each) and then the sum, the native path
+    rounds the fp32 sum once, so the two differ by at most
+    2^-9 (sum_h |g_h| + |S| + |comp|) <= 2^-8 (sum_h |g_h| + |comp|) per element.
+    Both sides also add each head's thousands of products in fp32 in different
+    orders (one accumulator for the whole group against one per head); where
+    those products cancel, that difference is set by their size, not by the
+    result's, hence an absolute allowance of 2^-12 of the tensor's largest
+    magnitude (a wrong or missing head's share is of the order of the largest
+    values and still fails)."""
+    for t, (name, g1, g2) in enumerate(zip(GRAD_NAMES, grads, comp)):
+        if native and t in (1, 3):
+            diff = (g1.float() - g2.float()).abs()
+            bound = 2.0 ** -8 * (mags[t] + g2.float().abs()) + 2.0 ** -12 * float(g2.float().abs().max())
+            worst = float((diff - bound).max())
+            assert worst <= 0, f"{label}: {name} exceeds the rounding bound by {worst}"
+        else:
+            assert torch.equal(g1, g2), f"{label}: {name} differs from the per-head composite"
 
 
 def sample_rows(n, w1, w2, extra=4, seed=0):

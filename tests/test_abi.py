@@ -172,12 +172,16 @@ def test_gqa_workspace_size(lib):
     assert f(1, 64, 4, 2, 48, 16, 8, 1) == 0
     # Hkv == H: the plain backward's workspace
     assert f(2, 8192, 8, 8, 128, 512, 32, 1) == plain(2, 8192, 8, 128, 512, 32, 1)
-    # Hkv < H: plus eight [B, N, H, D] tensors of the data type
-    for (b, n, h, hkv, d, w1, w2, dt, es) in [(1, 64, 4, 2, 128, 16, 8, 1, 2),
-                                              (2, 100, 6, 1, 32, 9, 5, 0, 4)]:
+    # Hkv < H: plus [B, N, H, D] tensors of the data type, two where the MFMA
+    # kernels read the K side in place (bf16, D 64/128, w2 <= 64), else eight
+    for (b, n, h, hkv, d, w1, w2, dt, es, nt) in [(1, 64, 4, 2, 128, 16, 8, 1, 2, 2),
+                                                  (1, 64, 4, 2, 64, 16, 64, 1, 2, 2),
+                                                  (1, 200, 4, 2, 128, 16, 65, 1, 2, 8),
+                                                  (1, 64, 4, 2, 128, 16, 8, 0, 4, 8),
+                                                  (2, 100, 6, 1, 32, 9, 5, 0, 4, 8)]:
         ws = f(b, n, h, hkv, d, w1, w2, dt)
-        assert ws >= plain(b, n, h, d, w1, w2, dt) + 8 * b * n * h * d * es
-        assert ws <= plain(b, n, h, d, w1, w2, dt) + 8 * (b * n * h * d * es + 255) + 255
+        assert ws >= plain(b, n, h, d, w1, w2, dt) + nt * b * n * h * d * es
+        assert ws <= plain(b, n, h, d, w1, w2, dt) + nt * (b * n * h * d * es + 255) + 255
 
 
 @only_without_gpu
