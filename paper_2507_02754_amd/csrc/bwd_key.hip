@@ -97,7 +97,10 @@ using ic = std::integral_constant<int, X>;
 // FORM 1: determinant logits (Section 5): role A forms q~ = k'_k x q_i per
 // 3-component chunk (unscaled), so S = q~ K^T is the determinant logit and
 // dK = scale sum_r dS_rj q~_r as for the trilinear form.
-template <int D, int G, bool BIAS, int FORM, bool FUSED>
+// GQ: grouped-query attention with fewer K-side heads than query heads (the
+// workgroup walks several query heads' row blocks); otherwise one query head
+// per K-side head, with no group indexing in the loop.
+template <int D, int G, bool BIAS, int FORM, bool FUSED, bool GQ>
 __device__ __forceinline__ void key_body(
     Shape s, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ kp, const uint16_t* __restrict__ v, const uint16_t* __restrict__ vp,
@@ -105,7 +108,7 @@ __device__ __forceinline__ void key_body(
     uint16_t* __restrict__ dk, uint16_t* __restrict__ dv, FusedPlan fp, float* __restrict__ part) {
   constexpr int NT = D / 16, NDT = D / 32;
   constexpr int W2P = 32 * G;
-  static_assert(!FUSED || (G == 1 && FORM == 0), "fused backward: w2 <= 32, trilinear logits");
+  static_assert(!FUSED || (G == 1 && FORM == 0 && !GQ), "fused backward: w2 <= 32, trilinear logits, Hkv = H");
   using L = KeyLds<D, FUSED>;
   using T = typename L::T;
   // tile items (row, 16-byte chunk) per thread of a forming role (64 NKG threads)
@@ -117,8 +120,7 @@ __device__ __forceinline__ void key_body(
   // Grouped-query attention: a workgroup owns keys of one K-side head hk and
   // walks the row blocks of its QG query heads hk QG .. hk QG + QG - 1 in turn
   // (dK, dV accumulate over all of them).
-  // The fused kernel runs with one query head per K-side head only.
-  const int Hkv = FUSED ? s.H : s.Hkv, QG = FUSED ? 1 : s.H / s.Hkv;
+  const int Hkv = GQ ? s.Hkv : s.H, QG = GQ ? s.H / s.Hkv : 1;
   const int jblocks = (s.N + KW - 1) / KW;
   const int total = jblocks * s.B * Hkv;
   const int per_xcd = (total + 7) / 8;
@@ -239,13 +241,13 @@ __device__ __forceinline__ void key_body(
   // of head hg) to its local index and head.
   int hg = 0;
   auto loc = [&](int r) {
-    if constexpr (FUSED)
+    if constexpr (!GQ)
       return r;
     else
       return r < nrb4 ? r : r - nrb4;
   };
   auto hof = [&](int r) {
-    if constexpr (FUSED)
+    if constexpr (!GQ)
       return 0;
     else
       return r < nrb4 ? hg : hg + 1;
@@ -327,7 +329,7 @@ __device__ __forceinline__ void key_body(
   // must be called for every row block in order (R = hg nrb4 + rb).
   const float* statp = roleA ? lse : delta;
   auto stat_load = [&](int rb0) {  // rb0: R of the first of 64 row blocks
-    const int rg = rb0 + lane, hq = FUSED ? 0 : rg / nrb4;
+    const int rg = rb0 + lane, hq = GQ ? rg / nrb4 : 0;
     const int ii = min(j0 + (rg - hq * nrb4) / G, N - 1);
     const float x = statp[stat + static_cast<size_t>(min(hq, QG - 1)) * N + ii];
     return roleA ? -x * kLog2e : x;
@@ -937,13 +939,13 @@ __device__ __forceinline__ void key_body(
 }
 
 // The split path's key-side kernel and the fused backward kernel (one body).
-template <int D, int G, bool BIAS, int FORM>
+template <int D, int G, bool BIAS, int FORM, bool GQ>
 __global__ __launch_bounds__((key_threads<D, false>()), 1) void bwd_key_kernel(
     Shape s, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ kp, const uint16_t* __restrict__ v, const uint16_t* __restrict__ vp,
     const uint16_t* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ delta,
     uint16_t* __restrict__ dk, uint16_t* __restrict__ dv, FusedPlan fp, float* __restrict__ part) {
-  key_body<D, G, BIAS, FORM, false>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, fp, part);
+  key_body<D, G, BIAS, FORM, false, GQ>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, fp, part);
 }
 template <int D, bool BIAS>
 __global__ __launch_bounds__((key_threads<D, true>()), 1) void bwd_fused_kernel(
@@ -951,10 +953,10 @@ __global__ __launch_bounds__((key_threads<D, true>()), 1) void bwd_fused_kernel(
     const uint16_t* __restrict__ kp, const uint16_t* __restrict__ v, const uint16_t* __restrict__ vp,
     const uint16_t* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ delta,
     uint16_t* __restrict__ dk, uint16_t* __restrict__ dv, FusedPlan fp, float* __restrict__ part) {
-  key_body<D, 1, BIAS, 0, true>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, fp, part);
+  key_body<D, 1, BIAS, 0, true, false>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, fp, part);
 }
 
-template <int D, int G, bool BIAS, int FORM = 0, bool FUSED = false>
+template <int D, int G, bool BIAS, int FORM = 0, bool FUSED = false, bool GQ = false>
 hipError_t launch_key(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
                       const void* vp, const void* dout, const float* lse, const float* delta, void* dk,
                       void* dv, hipStream_t st, const FusedPlan& fp = FusedPlan{}, float* part = nullptr) {
@@ -964,7 +966,7 @@ hipError_t launch_key(const Shape& s, const void* q, const void* k, const void* 
     if constexpr (FUSED)
       return bwd_fused_kernel<D, BIAS>;
     else
-      return bwd_key_kernel<D, G, BIAS, FORM>;
+      return bwd_key_kernel<D, G, BIAS, FORM, GQ>;
   }();
   hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(((tot + 7) / 8) * 8)), dim3(key_threads<D, FUSED>()), 0,
                      st, s, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
@@ -1033,6 +1035,17 @@ hipError_t mfma_bwd_key_b(const Shape& s, const void* q, const void* k, const vo
                           const void* vp, const void* dout, const float* lse, const float* delta,
                           void* dk, void* dv, hipStream_t st) {
   const int G = s.w2 <= 32 ? 1 : 2;
+  if constexpr (!BIAS) {
+    if (s.Hkv < s.H) {  // grouped-query attention (no bias constants there)
+      if (s.D == 128)
+        return G == 1 ? launch_key<128, 1, false, 0, false, true>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, st)
+                      : launch_key<128, 2, false, 0, false, true>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, st);
+      if (s.D == 64)
+        return G == 1 ? launch_key<64, 1, false, 0, false, true>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, st)
+                      : launch_key<64, 2, false, 0, false, true>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, st);
+      return hipErrorInvalidValue;
+    }
+  }
   if (s.D == 128)
     return G == 1 ? launch_key<128, 1, BIAS>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, st)
                   : launch_key<128, 2, BIAS>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, st);
@@ -1092,13 +1105,14 @@ hipError_t mfma_bwd_fused_reduce(const Shape& s, void* dq, void* dkp, void* dvp,
 hipError_t mfma_bwd_key(const Shape& s, const void* q, const void* k, const void* kp, const void* v,
                         const void* vp, const void* dout, const float* lse, const float* delta,
                         void* dk, void* dv, hipStream_t st) {
+  const bool bias = s.kp_bias != 0.f || s.vp_bias != 0.f;
+  if (s.Hkv < s.H && (s.form != 0 || bias)) return hipErrorInvalidValue;  // grouped-query: trilinear, no constants
   if (s.form == 1) {  // determinant logits: w2 <= 32, no bias constants
     if (s.w2 > 32) return hipErrorInvalidValue;
     return s.D == 128 ? launch_key<128, 1, false, 1>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, st)
                       : launch_key<64, 1, false, 1>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, st);
   }
-  return s.kp_bias != 0.f || s.vp_bias != 0.f
-             ? mfma_bwd_key_b<true>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, st)
+  return bias ? mfma_bwd_key_b<true>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, st)
              : mfma_bwd_key_b<false>(s, q, k, kp, v, vp, dout, lse, delta, dk, dv, st);
 }
 
