@@ -236,25 +236,29 @@ __device__ __forceinline__ void key_body(
   unsigned frw[2][2], fmw[2][IPT][2];
   const float mbias = roleA ? s.kp_bias : s.vp_bias;
   // Row blocks of a workgroup: those of query head 0 of the group, padded to
-  // nrb4, then those of head 1, ... (R = hg nrb4 + rb). The steps take the
-  // local rb of head hg; loc / hof map rb + k (k <= 4, possibly past the end
-  // of head hg) to its local index and head.
-  int hg = 0;
-  auto loc = [&](int r) {
-    if constexpr (!GQ)
+  // nrb4, then those of head 1, ... (R = hg nrb4 + rb = hgb + rb). The steps
+  // take the local rb of head hg; loc / hof map rb + k (k <= 4, possibly past
+  // the end of head hg) to its local index and head. Only the guarded steps
+  // (cross: std::true_type) reach past the end of a head: the straight-line
+  // ones end 4 row blocks before nrb4.
+  int hg = 0, hgb = 0;
+  auto loc = [&](int r, auto cross) {
+    if constexpr (!GQ || !decltype(cross)::value)
       return r;
     else
       return r < nrb4 ? r : r - nrb4;
   };
-  auto hof = [&](int r) {
+  auto hof = [&](int r, auto cross) {
     if constexpr (!GQ)
       return 0;
+    else if constexpr (!decltype(cross)::value)
+      return hg;
     else
       return r < nrb4 ? hg : hg + 1;
   };
-  auto fetch = [&](int rb, auto set) __attribute__((always_inline)) {
+  auto fetch = [&](int rb, auto set, auto cross) __attribute__((always_inline)) {
     constexpr int X = decltype(set)::value;
-    const int r = loc(rb), hq = hof(rb);  // row block r of query head hq of the group
+    const int r = loc(rb, cross), hq = hof(rb, cross);  // row block r of query head hq of the group
     const int i = j0 + r / G, g = r % G;
     const int qoff = hq < QG ? i * rsb + hq * 2 * D + 16 * dc : -1;
     fr[X] = ldbuf128(rrow, qoff);
@@ -376,12 +380,12 @@ __device__ __forceinline__ void key_body(
   }
   // tiles 0 and 1 (fused: role B forms the do~ halves, role C the q~ halves)
   if (FUSED ? role == 1 : true) {
-    fetch(0, ic<0>{});
+    fetch(0, ic<0>{}, std::false_type{});
     form_put(0, ic<0>{});
-    fetch(1, ic<0>{});
+    fetch(1, ic<0>{}, std::false_type{});
     form_put(L::tileBytes, ic<0>{});
-    fetch(2, ic<0>{});
-    if (roleA) fetch(3, ic<1>{});
+    fetch(2, ic<0>{}, std::false_type{});
+    if (roleA) fetch(3, ic<1>{}, std::false_type{});
   }
   // The loops start with every load complete (the wait-count pass would
   // otherwise keep the K/V operand loads pending into every iteration).
@@ -403,7 +407,7 @@ __device__ __forceinline__ void key_body(
       step(rb + 2, ic<2>{}, guard);
       step(rb + 3, ic<3>{}, guard);
     };
-    for (hg = 0; hg < QG; ++hg) {
+    for (hg = 0, hgb = 0; hg < QG; ++hg, hgb += nrb4) {
       int rb = 0;
       for (; rb < rb_lo; rb += kSlots) quad(rb, ic<1>{});
       for (; rb < rb_hi; rb += kSlots) quad(rb, ic<0>{});
@@ -424,8 +428,9 @@ __device__ __forceinline__ void key_body(
     };
     // P of row block rb from its logits, packed, and written to the exchange
     // buffer at xb for the partner.
-    auto probs = [&](int rb, float nlse2, const f32x16_t& sacc, int xb, u32x4_t* pf) __attribute__((always_inline)) {
-      const int i = j0 + loc(rb) / G;
+    auto probs = [&](int rb, float nlse2, const f32x16_t& sacc, int xb, u32x4_t* pf, auto cross)
+                     __attribute__((always_inline)) {
+      const int i = j0 + loc(rb, cross) / G;
       const bool colok = jme <= i && jme > i - w1 && jme < N;
       const float nl = nlse2 - (colok ? 0.f : __builtin_inff());
       // p = 2^min(x, 0): at most 1, so rows formed as zeros (whose statistic
@@ -455,7 +460,7 @@ __device__ __forceinline__ void key_body(
     if constexpr (FUSED) lds_barrier();  // role C has formed tiles 0 and 1
     {
       const float nl0 = stat_at(0);
-      if (is_active(0, j0)) probs(0, nl0, logits(0), 0, pcur);
+      if (is_active(0, j0)) probs(0, nl0, logits(0), 0, pcur, std::false_type{});
     }
     lds_barrier();
     // Iteration rb, tile slot S = rb % 4. The q~ half of tile rb + 2 is formed
@@ -469,8 +474,8 @@ __device__ __forceinline__ void key_body(
       constexpr int S1 = (S + 1) % kSlots, S2 = (S + 2) % kSlots;
       constexpr bool kGuard = decltype(guard)::value != 0;
       const bool act0 = !kGuard || is_active(rb, j0 + rb / G);
-      const bool act1 = !kGuard || is_active(loc(rb + 1), j0 + loc(rb + 1) / G);
-      const float nl1 = stat_at(hg * nrb4 + rb + 1);
+      const bool act1 = !kGuard || is_active(loc(rb + 1, guard), j0 + loc(rb + 1, guard) / G);
+      const float nl1 = stat_at(hgb + rb + 1);
       f32x16_t snext;
       u32x4_t pnext[2];
       if constexpr (!kGuard && FUSED) {
@@ -491,7 +496,7 @@ __device__ __forceinline__ void key_body(
         for (int uu = 0; uu < 2; ++uu)
 #pragma unroll
           for (int dt = 0; dt < NDT; ++dt) acc[dt] = mfma32(pcur[uu], otr[uu][dt], acc[dt]);
-        probs(rb + 1, nl1, snext, (S1 & 1) * L::xBuf, pnext);
+        probs(rb + 1, nl1, snext, (S1 & 1) * L::xBuf, pnext, guard);
 #pragma unroll
         for (int x = 0; x < NT; ++x) {
           __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // q~ row fragment
@@ -522,7 +527,7 @@ __device__ __forceinline__ void key_body(
         for (int uu = 0; uu < 2; ++uu)
 #pragma unroll
           for (int dt = 0; dt < NDT; ++dt) acc[dt] = mfma32(pcur[uu], otr[uu][dt], acc[dt]);
-        probs(rb + 1, nl1, snext, (S1 & 1) * L::xBuf, pnext);
+        probs(rb + 1, nl1, snext, (S1 & 1) * L::xBuf, pnext, guard);
         __builtin_amdgcn_sched_group_barrier(0x100, NT, 0);  // q~ row fragments
 #pragma unroll
         for (int x = 0; x < NT; ++x) {
@@ -548,10 +553,10 @@ __device__ __forceinline__ void key_body(
 #pragma unroll
             for (int dt = 0; dt < NDT; ++dt) acc[dt] = mfma32(pcur[uu], otr[uu][dt], acc[dt]);
         }
-        if (act1) probs(rb + 1, nl1, snext, (S1 & 1) * L::xBuf, pnext);
+        if (act1) probs(rb + 1, nl1, snext, (S1 & 1) * L::xBuf, pnext, guard);
         if constexpr (!FUSED) form_put(S2 * L::tileBytes, ic<S & 1>{});
       }
-      if constexpr (!FUSED) fetch(rb + 4, ic<S & 1>{});
+      if constexpr (!FUSED) fetch(rb + 4, ic<S & 1>{}, guard);
       pcur[0] = pnext[0];
       pcur[1] = pnext[1];
       __builtin_amdgcn_s_setprio(0);
@@ -590,8 +595,8 @@ __device__ __forceinline__ void key_body(
       constexpr int S1 = (S + 1) % kSlots, S2 = (S + 2) % kSlots;
       constexpr bool kGuard = decltype(guard)::value != 0;
       const bool act0 = !kGuard || is_active(rb, j0 + rb / G);
-      const bool act1 = !kGuard || is_active(loc(rb + 1), j0 + loc(rb + 1) / G);
-      const float dlt = stat_at(hg * nrb4 + rb);
+      const bool act1 = !kGuard || is_active(loc(rb + 1, guard), j0 + loc(rb + 1, guard) / G);
+      const float dlt = stat_at(hgb + rb);
       f32x16_t dpnext;
       if constexpr (!kGuard && !FUSED) {
         // Straight-line: reads first, then the dP products of row block rb + 1
@@ -656,7 +661,7 @@ __device__ __forceinline__ void key_body(
         }
         form_put(S2 * L::tileBytes, ic<0>{});
       }
-      fetch(rb + 3, ic<0>{});
+      fetch(rb + 3, ic<0>{}, guard);
       dpcur = dpnext;
       __builtin_amdgcn_s_setprio(0);
       lds_barrier();
