@@ -134,6 +134,8 @@ GQA = [
     (1, 8, 2, 257, 128, 100, 17, "bf16"),  # head-folded, w1 and w2 not multiples of 32
     (2, 16, 1, 70, 128, 512, 32, "bf16"),  # head-folded, windows longer than the sequence
     (1, 4, 1, 1, 128, 512, 32, "bf16"),    # head-folded, a single query
+    (1, 6, 2, 150, 128, 64, 32, "bf16"),   # three query heads per K-side head (odd group)
+    (2, 6, 3, 97, 64, 40, 64, "bf16"),     # w2 = 64 and head_dim 64, ragged length, two batches
 ]
 
 
