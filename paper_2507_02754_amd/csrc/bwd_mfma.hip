@@ -568,11 +568,12 @@ __global__ __launch_bounds__(64 * WAVES) void bwd_q_kernel(
       lds_barrier();
     }
 
-    // Rows no later query of the chunk touches are complete.
+    // Rows no later query of the chunk touches are complete. No barrier
+    // after the flush: the rows it reads and clears are next written by the
+    // ring phases of a later tile, past the next tile's barriers.
     const int fl_lo = i0 - W2P + 1;
     const int fl_hi = min(i0 + QW, ce) - W2P;  // inclusive
     for (int kr = fl_lo + wave; kr <= fl_hi; kr += WAVES) flush_row(kr, false);
-    lds_barrier();
   }
   // Rows still open at the end of the chunk.
   for (int kr = ce - W2P + 1 + wave; kr <= ce - 1; kr += WAVES) flush_row(kr, ce < N);

@@ -432,8 +432,9 @@ __global__ __launch_bounds__(kQThreads, 1) void bwd_query_kernel(
       }
       lds_barrier();  // matches B's barrier after its dq reduction
       ring_add(ring_vp, au, rowvalid, kk, [](auto) {});
+      // No barrier after the flush: the rows it reads and clears are next
+      // written by the ring phases of the next tile, past its barriers.
       flush_tile(i0);
-      lds_barrier();
     }
   } else {
     u32x4_t ot[NT];
@@ -541,7 +542,6 @@ __global__ __launch_bounds__(kQThreads, 1) void bwd_query_kernel(
         lds_barrier();  // matches the barrier before role A's ring phases
         ring_add(ring_kp, adq, false, kk, [](auto) {});
         flush_tile(i0);
-        lds_barrier();
         continue;
       }
       // dq_i = scale * sum_k k'_k o dQ~_(i,k): every lane multiplies its
@@ -597,7 +597,6 @@ __global__ __launch_bounds__(kQThreads, 1) void bwd_query_kernel(
         }
       }
       flush_tile(i0);
-      lds_barrier();
     }
   }
   // Rows still open at the end of the chunk.
